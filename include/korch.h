@@ -1,0 +1,218 @@
+/*
+ * korch.h -- C ABI of an MI355X (gfx950) executor for Korch-style primitive
+ * graphs under kernel-orchestration plans.
+ *
+ * Model (Korch, Sections 3-5):
+ *   - A primitive graph G = (P, E) is a DAG whose nodes are tensor-algebra
+ *     primitives of four kinds (Section 3): elementwise, reduce/broadcast,
+ *     layout transformation and linear transformation.  Graph inputs
+ *     (activations and weights) are nodes without a producer.
+ *   - A kernel is a convex set of primitives P' (Definition 1) with a
+ *     non-empty possible output set O (Definition 3) that it materializes.
+ *   - A plan is an ordered list of kernels.  Every kernel reads only graph
+ *     inputs and tensors materialized by earlier kernels (the dependency
+ *     constraint of Section 4.2, with an order), every graph output is
+ *     materialized by some kernel (the output constraint), a primitive may be
+ *     executed by several kernels (redundant execution) and a primitive in no
+ *     kernel is never executed (implicit pruning).
+ *   - Kernels run sequentially on one stream (Section 5.3).
+ *
+ * Conventions for every entry point:
+ *   - Return value: KORCH_OK (0) or a negative korch_status.  korch_last_error()
+ *     returns a thread-local message naming the rule / kernel that failed.
+ *     No C++ exception and no abort crosses this boundary.
+ *   - Handles are owned by the caller and released with the destroy calls,
+ *     which accept NULL.
+ *   - Device memory (inputs, outputs, workspace) is allocated and owned by the
+ *     caller.  Tensors are dense, row-major, and every device pointer must be
+ *     16-byte aligned (KORCH_E_ALIGN otherwise).  The library owns only its
+ *     compiled code objects and a small per-plan counter buffer that
+ *     korch_plan_load allocates once.
+ *   - Nothing here synchronizes the stream.  Device faults in asynchronous
+ *     kernels surface at the caller's next synchronization.
+ *   - hipStream_t is passed as void* so this header needs no HIP header.
+ */
+#ifndef KORCH_H
+#define KORCH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct korch_graph korch_graph;
+typedef struct korch_plan korch_plan;
+
+typedef enum {
+  KORCH_OK = 0,
+  KORCH_E_ARG = -1,               /* bad argument, NULL handle, bad node id      */
+  KORCH_E_SHAPE = -2,             /* shape inference failed                      */
+  KORCH_E_CYCLE = -3,             /* graph is not a DAG / not finalized          */
+  KORCH_E_STATE = -4,             /* call not allowed in the object's state      */
+  KORCH_E_PLAN_EMPTY = -10,       /* empty plan or kernel, or a graph input in P' */
+  KORCH_E_PLAN_NONCONVEX = -11,   /* Definition 1 violated                       */
+  KORCH_E_PLAN_BAD_OUTPUT = -12,  /* O not a possible output set (Definition 3)  */
+  KORCH_E_PLAN_DEP_ORDER = -13,   /* a kernel reads a tensor no earlier kernel made */
+  KORCH_E_PLAN_OUTPUT_UNCOVERED = -14, /* a graph output is never materialized   */
+  KORCH_E_PLAN_MULTI_OUTPUT = -15,/* |O| > 1 while KORCH_STRICT_SINGLE_OUTPUT=1  */
+  KORCH_E_UNSUPPORTED = -20,      /* no kernel family implements this kernel (cost = infinity) */
+  KORCH_E_ALIGN = -21,            /* device pointer not 16-byte aligned          */
+  KORCH_E_WORKSPACE = -22,        /* workspace missing or too small              */
+  KORCH_E_COMPILE = -23,          /* runtime compilation of a kernel failed      */
+  KORCH_E_HIP = -30               /* a HIP runtime call failed                   */
+} korch_status;
+
+typedef enum { KORCH_F32 = 0, KORCH_F16 = 1, KORCH_BF16 = 2 } korch_dtype;
+
+/* Primitive kinds (Section 3 and its table of representative operators). */
+typedef enum {
+  KORCH_INPUT = 0,
+  /* elementwise, unary: O[x] = f(I[x]) */
+  KORCH_NEG = 1, KORCH_EXP, KORCH_LOG, KORCH_TANH, KORCH_SQRT, KORCH_RSQRT, KORCH_RELU,
+  KORCH_SQUARE, KORCH_RECIP, KORCH_GELU_TANH, KORCH_ABS, KORCH_IDENTITY,
+  /* elementwise, binary: O[x] = f(I1[x], I2[x]); implicit broadcast (right-aligned,
+     size-1 dims stretch), or f(I1[x], scalar) when attrs.has_scalar */
+  KORCH_ADD = 32, KORCH_SUB, KORCH_MUL, KORCH_DIV, KORCH_MAX, KORCH_MIN,
+  /* reduce along attrs.axis (sum / mean = sum/n / max), keepdim per attrs;
+     broadcast to attrs.shape */
+  KORCH_REDUCE_SUM = 64, KORCH_REDUCE_MEAN, KORCH_REDUCE_MAX, KORCH_BROADCAST,
+  /* layout: O[x] = I[L(x)] with L one-to-one */
+  KORCH_TRANSPOSE = 96,  /* output dim k = input dim attrs.perm[k]          */
+  KORCH_RESHAPE,         /* row-major reinterpretation to attrs.shape       */
+  KORCH_SLICE,           /* [attrs.begin, attrs.end) per dim, unit step     */
+  KORCH_PAD,             /* attrs.begin = low pads, attrs.end = high pads, value attrs.pad_value */
+  KORCH_CONCAT,          /* along attrs.axis, n_in >= 2                     */
+  /* linear */
+  KORCH_MATMUL = 128,    /* [..., M, K] x [..., K, N] -> [..., M, N], batch dims broadcast */
+  KORCH_CONV2D           /* NHWC x HWIO cross-correlation, zero pad attrs.pad, stride attrs.stride */
+} korch_op;
+
+#define KORCH_MAX_RANK 8
+
+typedef struct {
+  int32_t axis;                     /* reduce / concat axis (negative counts from the end) */
+  int32_t keepdim;                  /* reduce: keep the reduced dim as size 1              */
+  int32_t rank;                     /* length of perm / shape / begin / end                */
+  int32_t perm[KORCH_MAX_RANK];
+  int64_t shape[KORCH_MAX_RANK];    /* reshape / broadcast target                          */
+  int64_t begin[KORCH_MAX_RANK];    /* slice begin, or pad low                             */
+  int64_t end[KORCH_MAX_RANK];      /* slice end, or pad high                              */
+  double scalar;                    /* right operand of a binary op when has_scalar        */
+  int32_t has_scalar;
+  int32_t stride, pad;              /* conv2d                                              */
+  double pad_value;                 /* pad                                                 */
+} korch_attrs;
+
+/* A kernel (P', O): primitive node ids and the ids it materializes. */
+typedef struct {
+  int32_t n_prims;
+  const int32_t* prims;
+  int32_t n_outs;
+  const int32_t* outs;
+} korch_kernel_desc;
+
+/* Kernel families (what implements a kernel on the GPU). */
+typedef enum {
+  KORCH_FAM_NONE = 0,
+  KORCH_FAM_POINTWISE = 1,   /* elementwise + broadcast + layout chains          */
+  KORCH_FAM_ROW = 2,         /* row programs with last-axis reductions (softmax, LayerNorm) */
+  KORCH_FAM_COLREDUCE = 3,   /* one reduction over a non-last axis               */
+  KORCH_FAM_GEMM = 4,        /* MFMA matrix product with fused prologue / epilogue */
+  KORCH_FAM_CONV = 5,        /* implicit-GEMM NHWC convolution + epilogue         */
+  KORCH_FAM_ATTENTION = 6,   /* scores, row softmax and second product in one kernel */
+  KORCH_FAM_SPLITK = 7       /* long-contraction product split over workgroups, deterministic */
+} korch_family;
+
+const char* korch_last_error(void);
+const char* korch_status_name(int status);
+
+/* ---- graph (Section 4: G = (P, E)) ------------------------------------ */
+int korch_graph_create(korch_graph** g);
+void korch_graph_destroy(korch_graph* g);
+/* Adds a graph input (activation or weight) of the given shape and dtype. */
+int korch_graph_input(korch_graph* g, korch_dtype dtype, int32_t rank, const int64_t* shape, int32_t* node);
+/* Adds a primitive reading n_in earlier nodes; attrs may be NULL when unused;
+   out_dtype is the storage dtype of the primitive's tensor.  The output shape
+   is inferred immediately (KORCH_E_SHAPE on mismatch). */
+int korch_graph_op(korch_graph* g, korch_op op, int32_t n_in, const int32_t* in, const korch_attrs* attrs,
+                   korch_dtype out_dtype, int32_t* node);
+/* Marks a primitive as a graph output (order of calls = output order). */
+int korch_graph_output(korch_graph* g, int32_t node);
+/* Freezes the graph: checks it is a DAG with at least one output and builds
+   reachability.  Required before plans are made. */
+int korch_graph_finalize(korch_graph* g);
+int korch_graph_num_nodes(const korch_graph* g, int32_t* n);
+/* Shape / dtype / op of a node; shape must hold KORCH_MAX_RANK entries. */
+int korch_graph_node_info(const korch_graph* g, int32_t node, int32_t* op, int32_t* dtype, int32_t* rank,
+                          int64_t* shape);
+int korch_graph_num_inputs(const korch_graph* g, int32_t* n);
+int korch_graph_num_outputs(const korch_graph* g, int32_t* n);
+int korch_graph_input_node(const korch_graph* g, int32_t i, int32_t* node);
+int korch_graph_output_node(const korch_graph* g, int32_t i, int32_t* node);
+
+/* ---- orchestration analysis (Section 4.1) ------------------------------ */
+/* Definition 1 on an arbitrary node set; *convex = 1 or 0. */
+int korch_is_convex(const korch_graph* g, int32_t n, const int32_t* nodes, int32_t* convex);
+/* Execution states (Definition 2) reached by the depth-first search of
+   Algorithm 1, including the empty state.  Each state is reported as a 0/1
+   array over all node ids (graph inputs are always 0).  Returns
+   KORCH_E_ARG when more than max_states states exist. */
+int korch_enumerate_states(const korch_graph* g, int32_t max_states,
+                           int (*cb)(const uint8_t* member, int32_t n_nodes, void* user), void* user);
+/* Candidate kernels of Algorithm 1: every P' = D2 \ D1 of states D1 < D2 with
+   |P'| <= max_prims, paired with each non-empty possible output set O (all
+   subsets when the maximal set has <= max_outs members, otherwise the maximal
+   set and each singleton).  When only_supported != 0, candidates no family
+   implements are skipped.  The callback returns non-zero to stop early. */
+int korch_enumerate_candidates(const korch_graph* g, int32_t max_prims, int32_t max_outs, int32_t only_supported,
+                               int (*cb)(const korch_kernel_desc* k, void* user), void* user);
+/* Which family implements kernel k (KORCH_FAM_NONE = unsupported, cost infinity). */
+int korch_kernel_family(const korch_graph* g, const korch_kernel_desc* k, int32_t* family);
+
+/* ---- plans -------------------------------------------------------------- */
+/* Validates an ordered plan (rules of Definitions 1 and 3 and the output and
+   dependency constraints of Section 4.2) and copies the graph, so the plan
+   does not depend on the graph's lifetime. */
+int korch_plan_create(const korch_graph* g, int32_t n_kernels, const korch_kernel_desc* kernels, korch_plan** p);
+/* The unfused plan: one kernel per primitive, except reshapes of materialized
+   tensors, which are views and need no kernel. */
+int korch_plan_unfused(const korch_graph* g, korch_plan** p);
+void korch_plan_destroy(korch_plan* p);
+int korch_plan_num_kernels(const korch_plan* p, int32_t* n);
+/* Family match, code generation and runtime compilation for gfx950 of every
+   kernel (disk-cached).  Needs no GPU.  KORCH_E_UNSUPPORTED names the kernel. */
+int korch_plan_compile(korch_plan* p);
+/* Loads the compiled code objects on the current device and allocates the
+   plan's counter buffer (needs a GPU; korch_plan_execute calls it lazily). */
+int korch_plan_load(korch_plan* p);
+int korch_plan_workspace_bytes(const korch_plan* p, size_t* bytes);
+/* Launches the plan's kernels in order on `stream` (a hipStream_t, NULL =
+   default stream).  inputs[i] / outputs[i] follow graph input / output order.
+   Never allocates; never synchronizes. */
+int korch_plan_execute(korch_plan* p, const void* const* inputs, void* const* outputs, void* workspace,
+                       size_t workspace_bytes, void* stream);
+/* Per-kernel family, algorithmic bytes (compulsory reads of its external
+   tensors plus writes of its outputs) and flops (2*M*N*K per contraction). */
+int korch_plan_kernel_info(const korch_plan* p, int32_t k, int32_t* family, double* alg_bytes, double* alg_flops);
+/* Generated HIP source and kernel symbol name of kernel k (after compile). */
+int korch_plan_kernel_source(const korch_plan* p, int32_t k, char* buf, size_t cap, size_t* len);
+int korch_plan_kernel_name(const korch_plan* p, int32_t k, char* buf, size_t cap);
+/* Launch geometry of kernel k (after compile). */
+int korch_plan_kernel_launch(const korch_plan* p, int32_t k, int32_t grid[3], int32_t block[3], int32_t* lds_bytes);
+
+/* ---- profiler (Section 5.2, kernel profiler; Algorithm 1's Profiling) --- */
+/* Times the single kernel (P', O) in isolation: compiles it, fills its inputs
+   with seeded N(0,1) values in device buffers the profiler allocates, runs
+   `warmup` untimed launches, then `reps` launches each preceded by a write of
+   `flush_bytes` to a scratch buffer (to evict L2 and the Infinity Cache) and
+   bracketed by HIP events on `stream`; *median_us is the median.  Returns
+   KORCH_E_UNSUPPORTED (cost infinity) when no family implements it. */
+int korch_profile_candidate(const korch_graph* g, const korch_kernel_desc* k, int32_t warmup, int32_t reps,
+                            size_t flush_bytes, void* stream, float* median_us);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KORCH_H */

@@ -1,0 +1,54 @@
+// Helper kernels of the profiler: a cache-flushing write and a seeded fill.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+// Streams `n` 16-byte words into `p`, evicting L2 and the Infinity Cache.
+__global__ void flush_kernel(uint4* __restrict__ p, size_t n, uint32_t v) {
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = make_uint4(v, i, v, i);
+}
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  x += 0x9E3779B97F4A7C15ULL;
+  x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  x = (x ^ (x >> 27)) * 0x94D049BB133111EBULL;
+  return x ^ (x >> 31);
+}
+
+// Element i = 0.5 + u_i, u_i uniform in [0, 1) from a counter-based hash of (seed, i).
+__global__ void fill_kernel(void* __restrict__ p, size_t n, int dtype, uint64_t seed) {
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    uint64_t h = splitmix64(seed * 0x100000001B3ULL + i);
+    float u = 0.5f + (float)(h >> 40) * (1.0f / 16777216.0f);
+    if (dtype == 0)
+      ((float*)p)[i] = u;
+    else if (dtype == 1)
+      ((_Float16*)p)[i] = (_Float16)u;
+    else
+      ((__bf16*)p)[i] = (__bf16)u;
+  }
+}
+
+}  // namespace
+
+namespace korch {
+
+hipError_t launch_flush(void* p, size_t bytes, hipStream_t s) {
+  size_t n = bytes / 16;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(flush_kernel, dim3(4096), dim3(256), 0, s, (uint4*)p, n, 0x5a5a5a5au);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(void* p, size_t n, int dtype, uint64_t seed, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n, dtype, seed);
+  return hipGetLastError();
+}
+
+}  // namespace korch

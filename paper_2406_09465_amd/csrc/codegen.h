@@ -1,0 +1,110 @@
+// Kernel-family matching and HIP source generation for gfx950.
+//
+// A kernel (P', O) of a plan is matched to one hand-written kernel family
+// (pointwise, row program, column reduction, MFMA GEMM / implicit-GEMM conv,
+// split-K contraction, attention).  The family's skeleton is specialized by
+// emitting the kernel's own per-element expressions as C++ and compiling the
+// result at run time for gfx950.  A kernel no family implements is
+// "unsupported", the infinite cost of Korch's profiler (Section 4.1).
+#pragma once
+
+#include <functional>
+#include <map>
+#include <set>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "ir.h"
+
+namespace korch {
+
+// One pointer argument of a generated kernel.
+struct ArgRef {
+  enum Kind { Tensor, Output, Scratch, Counter } kind = Tensor;
+  int node = -1;       // Tensor: node whose storage is read; Output: node written
+  size_t bytes = 0;    // Scratch / Counter: size
+};
+
+struct GenKernel {
+  int family = KORCH_FAM_NONE;
+  std::string name;
+  std::string source;
+  int grid[3] = {1, 1, 1};
+  int block[3] = {256, 1, 1};
+  int lds_bytes = 0;  // static LDS (informational)
+  std::vector<ArgRef> args;
+  double alg_bytes = 0, alg_flops = 0;
+};
+
+// Family matcher only (no source); returns the family or KORCH_FAM_NONE with a reason.
+int match_family(const Graph& g, const KernelDesc& k, std::string* why);
+// Full specialization; throws Error(KORCH_E_UNSUPPORTED) when no family matches.
+GenKernel generate_kernel(const Graph& g, const KernelDesc& k, int index);
+
+// ---------------------------------------------------------------------------
+// Shared code-generation machinery (used by the family generators).
+// ---------------------------------------------------------------------------
+
+// Integer index expression  base + c*e  where e is the vector-lane variable of
+// the current emission (0..VEC-1).  `al` records that base is a multiple of al.
+struct Ix {
+  std::string b = "0";
+  int64_t c = 0;
+  int64_t al = 1;
+  bool affine = true;
+  bool konst = true;
+  int64_t kv = 0;
+  static Ix k(int64_t v);
+  static Ix var(const std::string& name, int64_t coef = 0, int64_t align = 1);
+  std::string at(const std::string& e = "e") const;  // full C++ expression
+  bool is_zero() const { return konst && kv == 0 && c == 0; }
+};
+
+Ix ix_add(const Ix& a, const Ix& b);
+Ix ix_addk(const Ix& a, int64_t v);
+Ix ix_mulk(const Ix& a, int64_t v, int vec);
+Ix ix_divk(const Ix& a, int64_t s, int vec);
+Ix ix_modk(const Ix& a, int64_t s, int vec);
+
+std::string ctype(int dtype);                 // "float" / "f16" / "bf16"
+std::string flit(double v);                   // float literal
+std::string unary_expr(int op, const std::string& x);
+std::string binary_expr(int op, const std::string& x, const std::string& y);
+
+// Row-major strides of a shape.
+std::vector<int64_t> strides_of(const Shape& s);
+
+// Generic per-element emitter.  Produces the fp32 value of a node at an index
+// (one Ix per dimension) by walking the kernel's elementwise / broadcast /
+// layout nodes down to external tensors (loads) or to values supplied by the
+// family skeleton through `provide` (e.g. a matrix-product accumulator).
+struct Emitter {
+  const Graph& g;
+  std::set<int> inset;                 // nodes computed inside this kernel
+  std::map<int, int> argslot;          // external storage node -> pointer slot
+  int vec = 1;
+  std::ostringstream pre;              // statements before the lane loop
+  std::ostringstream body;             // statements inside the lane loop
+  std::function<bool(int, const std::vector<Ix>&, std::string*)> provide;
+  bool force_gather = false;           // all loads per-lane (guarded contexts)
+  int tmp = 0;
+  int guard_depth = 0;
+  int n_gather = 0, n_vector = 0, n_uniform = 0;
+  std::vector<std::map<std::string, std::string>> memo{1};
+
+  Emitter(const Graph& gg) : g(gg) {}
+  std::string value(int node, const std::vector<Ix>& idx);
+  std::string load(int node, const std::vector<Ix>& idx);
+  std::string fresh(const char* p) { return "_" + std::string(p) + std::to_string(tmp++); }
+  static std::string key(int node, const std::vector<Ix>& idx);
+};
+
+// Index of every dimension of `shape` when the tensor is read with numpy-style
+// right-aligned broadcasting at iteration index `it` (size-1 dims -> 0).
+std::vector<Ix> broadcast_index(const Shape& shape, const Shape& itshape, const std::vector<Ix>& it);
+
+// Common header for generated sources.
+std::string source_header(int nargs);
+
+}  // namespace korch

@@ -1,0 +1,94 @@
+// Device prelude included by every generated gfx950 kernel.
+//
+// Storage dtypes are fp32, fp16 (_Float16) and bf16 (__bf16); all arithmetic
+// is fp32 in registers.  Conversions to fp16 / bf16 round to nearest even.
+#pragma once
+
+typedef long long i64;
+typedef _Float16 f16;
+typedef __bf16 bf16;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+struct KArgs {
+  void* p[KORCH_NARGS];
+};
+
+// ---- scalar conversions ----------------------------------------------------
+__device__ __forceinline__ float tof(float x) { return x; }
+__device__ __forceinline__ float tof(f16 x) { return (float)x; }
+__device__ __forceinline__ float tof(bf16 x) { return (float)x; }
+template <typename T> __device__ __forceinline__ T fromf(float x);
+template <> __device__ __forceinline__ float fromf<float>(float x) { return x; }
+template <> __device__ __forceinline__ f16 fromf<f16>(float x) { return (f16)x; }
+template <> __device__ __forceinline__ bf16 fromf<bf16>(float x) { return (bf16)x; }
+
+// ---- vector loads / stores of V consecutive elements (16-B aligned when V*size == 16)
+template <int V, typename T> struct VecOf {
+  typedef T type __attribute__((ext_vector_type(V)));
+};
+template <typename T> struct VecOf<1, T> {
+  typedef T type;
+};
+
+template <int V, typename T>
+__device__ __forceinline__ void ldv(float* d, const T* __restrict__ p) {
+  if constexpr (V == 1) {
+    d[0] = tof(*p);
+  } else {
+    typedef typename VecOf<V, T>::type VT;
+    VT v = *reinterpret_cast<const VT*>(p);
+#pragma unroll
+    for (int i = 0; i < V; ++i) d[i] = tof(v[i]);
+  }
+}
+
+template <int V, typename T>
+__device__ __forceinline__ void stv(T* __restrict__ p, const float* s) {
+  if constexpr (V == 1) {
+    *p = fromf<T>(s[0]);
+  } else {
+    typedef typename VecOf<V, T>::type VT;
+    VT v;
+#pragma unroll
+    for (int i = 0; i < V; ++i) v[i] = fromf<T>(s[i]);
+    *reinterpret_cast<VT*>(p) = v;
+  }
+}
+
+template <typename T> __device__ __forceinline__ float ld1(const T* __restrict__ p) { return tof(*p); }
+template <typename T> __device__ __forceinline__ void st1(T* __restrict__ p, float v) { *p = fromf<T>(v); }
+
+// ---- elementwise functions (fp32) -----------------------------------------
+__device__ __forceinline__ float k_relu(float x) { return x > 0.0f ? x : 0.0f; }
+__device__ __forceinline__ float k_rsqrt(float x) { return 1.0f / sqrtf(x); }
+__device__ __forceinline__ float k_gelu_tanh(float x) {
+  // 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))
+  const float c = 0.7978845608028654f;
+  return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+}
+__device__ __forceinline__ float k_max(float a, float b) { return a > b ? a : b; }
+__device__ __forceinline__ float k_min(float a, float b) { return a < b ? a : b; }
+
+// Mish written as x * n / (n + 2) with n = e^x (e^x + 2), which equals
+// x * tanh(log(1 + e^x)) exactly; for large x the quotient is 1 in fp32.
+__device__ __forceinline__ float k_mish(float x) {
+  if (x > 20.0f) return x;
+  float ex = __expf(x);
+  float n = ex * (ex + 2.0f);
+  return x * (n / (n + 2.0f));
+}
+
+// ---- reductions across a group of G lanes of a wavefront (G power of two <= 64)
+template <int G> __device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+  for (int m = G / 2; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+template <int G> __device__ __forceinline__ float group_max(float v) {
+#pragma unroll
+  for (int m = G / 2; m >= 1; m >>= 1) v = k_max(v, __shfl_xor(v, m, 64));
+  return v;
+}

@@ -1,0 +1,232 @@
+// Plan compilation, code-object loading, sequential execution on one stream
+// (Korch, Section 5.3) and the single-candidate profiler (Section 5.2).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdlib>
+#include <thread>
+
+#include "plan.h"
+
+namespace korch {
+
+std::vector<char> rtc_compile(const std::string& src, const std::string& name);
+hipError_t launch_flush(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_fill(void* p, size_t n, int dtype, uint64_t seed, hipStream_t s);
+
+#define HIPCHECK(x)                                                                             \
+  do {                                                                                          \
+    hipError_t e_ = (x);                                                                        \
+    if (e_ != hipSuccess) fail(KORCH_E_HIP, std::string(#x) + ": " + hipGetErrorString(e_));    \
+  } while (0)
+
+void generate_plan(Plan& p) {
+  if (!p.ck.empty()) return;
+  std::vector<CompiledKernel> ck(p.kernels.size());
+  for (size_t k = 0; k < p.kernels.size(); ++k) {
+    ck[k].desc = p.kernels[k];
+    ck[k].gen = generate_kernel(p.g, ck[k].desc, (int)k);
+  }
+  p.ck = std::move(ck);
+  plan_workspace(p);
+}
+
+void compile_plan(Plan& p) {
+  if (p.compiled) return;
+  generate_plan(p);
+  int n = (int)p.ck.size();
+  int nt = std::min(n, 8);
+  std::atomic<int> next{0};
+  std::vector<std::string> errors(n);
+  std::vector<int> codes(n, 0);
+  auto work = [&]() {
+    for (int k = next++; k < n; k = next++) {
+      try {
+        p.ck[k].code = rtc_compile(p.ck[k].gen.source, p.ck[k].gen.name);
+      } catch (Error& e) {
+        errors[k] = e.what();
+        codes[k] = e.code;
+      } catch (std::exception& e) {
+        errors[k] = e.what();
+        codes[k] = KORCH_E_COMPILE;
+      }
+    }
+  };
+  std::vector<std::thread> th;
+  for (int t = 1; t < nt; ++t) th.emplace_back(work);
+  work();
+  for (auto& t : th) t.join();
+  for (int k = 0; k < n; ++k)
+    if (codes[k]) fail(codes[k], "kernel " + std::to_string(k) + ": " + errors[k]);
+  p.compiled = true;
+}
+
+static void unload(Plan& p) {
+  for (auto& ck : p.ck) {
+    if (ck.module) hipModuleUnload((hipModule_t)ck.module);
+    ck.module = nullptr;
+    ck.function = nullptr;
+    ck.device = -1;
+  }
+  if (p.counters) hipFree(p.counters);
+  p.counters = nullptr;
+  p.loaded = false;
+}
+
+void destroy_plan_device(Plan& p) { unload(p); }
+
+void load_plan(Plan& p) {
+  compile_plan(p);
+  int dev = 0;
+  HIPCHECK(hipGetDevice(&dev));
+  if (p.loaded && p.counter_device == dev) return;
+  unload(p);
+  for (auto& ck : p.ck) {
+    hipModule_t m;
+    HIPCHECK(hipModuleLoadData(&m, ck.code.data()));
+    hipFunction_t f;
+    hipError_t e = hipModuleGetFunction(&f, m, ck.gen.name.c_str());
+    if (e != hipSuccess) {
+      hipModuleUnload(m);
+      fail(KORCH_E_HIP, "hipModuleGetFunction(" + ck.gen.name + "): " + hipGetErrorString(e));
+    }
+    ck.module = m;
+    ck.function = f;
+    ck.device = dev;
+  }
+  if (p.counter_bytes) {
+    HIPCHECK(hipMalloc(&p.counters, p.counter_bytes));
+    HIPCHECK(hipMemset(p.counters, 0, p.counter_bytes));
+  }
+  p.counter_device = dev;
+  p.loaded = true;
+}
+
+static bool aligned16(const void* q) { return ((uintptr_t)q & 15) == 0; }
+
+void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
+                  hipStream_t stream) {
+  load_plan(p);
+  const Graph& g = p.g;
+  for (size_t i = 0; i < g.inputs.size(); ++i) {
+    if (!inputs || !inputs[i]) fail(KORCH_E_ARG, "input " + std::to_string(i) + " is NULL");
+    if (!aligned16(inputs[i])) fail(KORCH_E_ALIGN, "input " + std::to_string(i) + " is not 16-byte aligned");
+  }
+  for (size_t i = 0; i < g.outputs.size(); ++i) {
+    if (!outputs || !outputs[i]) fail(KORCH_E_ARG, "output " + std::to_string(i) + " is NULL");
+    if (!aligned16(outputs[i])) fail(KORCH_E_ALIGN, "output " + std::to_string(i) + " is not 16-byte aligned");
+  }
+  if (p.ws_bytes) {
+    if (!ws || ws_bytes < p.ws_bytes)
+      fail(KORCH_E_WORKSPACE, "workspace needs " + std::to_string(p.ws_bytes) + " bytes");
+    if (!aligned16(ws)) fail(KORCH_E_ALIGN, "workspace is not 16-byte aligned");
+  }
+  for (size_t k = 0; k < p.ck.size(); ++k) {
+    auto& ck = p.ck[k];
+    std::vector<void*> ptr(ck.arg_storage.size());
+    for (size_t a = 0; a < ck.arg_storage.size(); ++a) {
+      const Storage& s = ck.arg_storage[a];
+      switch (s.kind) {
+        case Storage::GraphInput: ptr[a] = const_cast<void*>(inputs[s.index]); break;
+        case Storage::GraphOutput: ptr[a] = outputs[s.index]; break;
+        case Storage::Workspace: ptr[a] = (char*)ws + s.offset; break;
+        case Storage::Counters: ptr[a] = (char*)p.counters + s.offset; break;
+      }
+    }
+    void* params[] = {ptr.data()};
+    HIPCHECK(hipModuleLaunchKernel((hipFunction_t)ck.function, ck.gen.grid[0], ck.gen.grid[1], ck.gen.grid[2],
+                                   ck.gen.block[0], ck.gen.block[1], ck.gen.block[2], 0, stream, params, nullptr));
+  }
+}
+
+// The candidate kernel as a stand-alone graph: its external tensors become
+// graph inputs and its output set becomes the graph outputs.
+Graph extract_subgraph(const Graph& g, const KernelDesc& kd) {
+  Graph s;
+  std::map<int, int> m;
+  for (int u : external_inputs(g, kd)) m[u] = s.add_input(g.nodes[u].dtype, g.nodes[u].shape);
+  for (int v : kd.prims) {
+    const Node& n = g.nodes[v];
+    std::vector<int> in;
+    for (int u : n.in) in.push_back(m.at(u));
+    m[v] = s.add_op(n.op, in, &n.attrs, n.dtype);
+  }
+  for (int o : kd.outs) s.add_output(m.at(o));
+  s.finalize();
+  return s;
+}
+
+float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
+                        hipStream_t stream) {
+  Plan p;
+  p.g = extract_subgraph(g, kd);
+  KernelDesc one;
+  for (size_t i = 0; i < p.g.nodes.size(); ++i)
+    if (p.g.is_prim((int)i)) one.prims.push_back((int)i);
+  one.outs = p.g.outputs;
+  std::sort(one.outs.begin(), one.outs.end());
+  p.kernels = {one};
+  validate_plan(p.g, p.kernels, false);
+  compile_plan(p);
+  load_plan(p);
+  std::vector<void*> bufs;
+  std::vector<const void*> in;
+  std::vector<void*> out;
+  auto alloc = [&](size_t bytes) {
+    void* q = nullptr;
+    HIPCHECK(hipMalloc(&q, std::max<size_t>(bytes, 256)));
+    bufs.push_back(q);
+    return q;
+  };
+  hipEvent_t* ev = nullptr;
+  std::vector<float> times;
+  try {
+    uint64_t seed = 1;
+    for (int i : p.g.inputs) {
+      const Node& n = p.g.nodes[i];
+      void* q = alloc((size_t)numel(n.shape) * dtype_bytes(n.dtype));
+      HIPCHECK(launch_fill(q, (size_t)numel(n.shape), n.dtype, seed++, stream));
+      in.push_back(q);
+    }
+    for (int o : p.g.outputs) {
+      const Node& n = p.g.nodes[o];
+      out.push_back(alloc((size_t)numel(n.shape) * dtype_bytes(n.dtype)));
+    }
+    void* ws = p.ws_bytes ? alloc(p.ws_bytes) : nullptr;
+    void* fl = flush_bytes ? alloc(flush_bytes) : nullptr;
+    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream);
+    ev = new hipEvent_t[2 * std::max(reps, 1)];
+    for (int r = 0; r < 2 * reps; ++r) HIPCHECK(hipEventCreate(&ev[r]));
+    for (int r = 0; r < reps; ++r) {
+      if (fl) HIPCHECK(launch_flush(fl, flush_bytes, stream));
+      HIPCHECK(hipEventRecord(ev[2 * r], stream));
+      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream);
+      HIPCHECK(hipEventRecord(ev[2 * r + 1], stream));
+    }
+    HIPCHECK(hipStreamSynchronize(stream));
+    for (int r = 0; r < reps; ++r) {
+      float ms = 0;
+      HIPCHECK(hipEventElapsedTime(&ms, ev[2 * r], ev[2 * r + 1]));
+      times.push_back(ms * 1000.0f);
+    }
+  } catch (...) {
+    hipStreamSynchronize(stream);
+    if (ev) {
+      for (int r = 0; r < 2 * reps; ++r) hipEventDestroy(ev[r]);
+      delete[] ev;
+    }
+    for (void* q : bufs) hipFree(q);
+    unload(p);
+    throw;
+  }
+  for (int r = 0; r < 2 * reps; ++r) hipEventDestroy(ev[r]);
+  delete[] ev;
+  for (void* q : bufs) hipFree(q);
+  unload(p);
+  if (times.empty()) return 0.0f;
+  std::sort(times.begin(), times.end());
+  return times[times.size() / 2];
+}
+
+}  // namespace korch

@@ -1,0 +1,625 @@
+// MFMA GEMM family (and implicit-GEMM convolution): C = epi(pro(A) * pro(B)).
+//
+// Linear-transformation primitives (Korch, Section 3) are the dense
+// contractions of a graph; here they run on gfx950 matrix cores
+// (v_mfma_f32_16x16x32_{f16,bf16}, v_mfma_f32_16x16x4_f32) with fp32
+// accumulation.  Elementwise / broadcast / layout primitives feeding an
+// operand are evaluated while the operand tile is staged into LDS (prologue);
+// elementwise primitives consuming the product are evaluated on the fp32 tile
+// before the single store (epilogue).  Several products that share their left
+// operand may run as one kernel, their right operands side by side in the tile.
+#include <algorithm>
+
+#include "families.h"
+#include "gemm_common.h"
+
+namespace korch {
+
+static bool in_vec(const std::vector<int>& v, int x) { return std::find(v.begin(), v.end(), x) != v.end(); }
+
+bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_reduce) {
+  const Graph& g = ki.g;
+  if (ki.linear.empty()) {
+    *why = "gemm: no linear primitive";
+    return false;
+  }
+  const Node& l0 = g.nodes[ki.linear[0]];
+  if (l0.op == KORCH_CONV2D) {
+    if (ki.linear.size() != 1) {
+      *why = "conv: more than one linear primitive";
+      return false;
+    }
+    sp.conv = true;
+    sp.mms = {ki.linear[0]};
+    sp.A = l0.in[0];
+    sp.Bs = {l0.in[1]};
+    if (ki.in.count(sp.A) || ki.in.count(sp.Bs[0])) {
+      *why = "conv: operands must be materialized tensors";
+      return false;
+    }
+    const Shape& x = g.nodes[sp.A].shape;
+    const Shape& w = g.nodes[sp.Bs[0]].shape;
+    sp.OUT = l0.shape;
+    sp.nb = (int)x.size() - 3;
+    sp.nmdims = 2;
+    sp.H = x[x.size() - 3];
+    sp.W = x[x.size() - 2];
+    sp.Cin = x.back();
+    sp.KH = w[0];
+    sp.KW = w[1];
+    sp.stride = l0.attrs.stride;
+    sp.pad = l0.attrs.pad;
+    sp.Ho = sp.OUT[sp.OUT.size() - 3];
+    sp.Wo = sp.OUT[sp.OUT.size() - 2];
+    sp.M = sp.Ho * sp.Wo;
+    sp.N = sp.OUT.back();
+    sp.K = sp.KH * sp.KW * sp.Cin;
+    sp.Nj = {sp.N};
+  } else {
+    for (int v : ki.linear)
+      if (g.nodes[v].op != KORCH_MATMUL) {
+        *why = "gemm: mixed linear primitives";
+        return false;
+      }
+    sp.A = l0.in[0];
+    // primary product first: largest N
+    std::vector<int> mms = ki.linear;
+    std::stable_sort(mms.begin(), mms.end(),
+                     [&](int a, int b) { return g.nodes[a].shape.back() > g.nodes[b].shape.back(); });
+    sp.mms = mms;
+    for (int v : mms) {
+      if (g.nodes[v].in[0] != sp.A) {
+        *why = "gemm: products do not share their left operand";
+        return false;
+      }
+      sp.Bs.push_back(g.nodes[v].in[1]);
+    }
+    for (int a : mms)
+      for (int b : mms)
+        if (a != b && ki.ancestor(a, b)) {
+          *why = "gemm: one product feeds another";
+          return false;
+        }
+    sp.OUT = g.nodes[mms[0]].shape;
+    sp.nb = (int)sp.OUT.size() - 2;
+    sp.nmdims = 1;
+    sp.M = sp.OUT[sp.OUT.size() - 2];
+    sp.N = sp.OUT.back();
+    sp.K = g.nodes[sp.A].shape.back();
+    for (int v : mms) {
+      const Shape& s = g.nodes[v].shape;
+      if (!std::equal(s.begin(), s.end() - 1, sp.OUT.begin()) || (s.back() != sp.N && s.back() != 1)) {
+        *why = "gemm: products differ in shape";
+        return false;
+      }
+      sp.Nj.push_back(s.back());
+    }
+  }
+  sp.mtype = g.nodes[sp.A].dtype;
+  for (int b : sp.Bs)
+    if (g.nodes[b].dtype != sp.mtype) {
+      *why = "gemm: operand dtypes differ";
+      return false;
+    }
+  int vb = 16 / dtype_bytes(sp.mtype);
+  int64_t off = 0;
+  for (auto n : sp.Nj) {
+    sp.offj.push_back(off);
+    off += (n + vb - 1) / vb * vb;
+  }
+  sp.Ntot = sp.mms.size() == 1 ? sp.N : off;
+  sp.batch = 1;
+  for (int d = 0; d < sp.nb; ++d) sp.batch *= sp.OUT[d];
+  // classify nodes
+  std::vector<int> operands = sp.Bs;
+  operands.push_back(sp.A);
+  for (int v : ki.k.prims) {
+    if (in_vec(sp.mms, v)) continue;
+    bool pro = false, below = false;
+    for (int o : operands)
+      if (v == o || ki.ancestor(v, o)) pro = true;
+    for (int m : sp.mms)
+      if (ki.ancestor(m, v)) below = true;
+    const Node& n = g.nodes[v];
+    Kind kd = op_kind(n.op);
+    if (pro) {
+      if (!(kd == Kind::Unary || kd == Kind::Binary || kd == Kind::Broadcast || kd == Kind::Layout)) {
+        *why = std::string("gemm: prologue cannot hold ") + op_name(n.op);
+        return false;
+      }
+      if (in_vec(ki.k.outs, v)) {
+        *why = "gemm: a prologue node cannot be a kernel output";
+        return false;
+      }
+      sp.pro.insert(v);
+    } else if (below) {
+      if (kd == Kind::Reduce) {
+        if (!allow_reduce) {
+          *why = "gemm: reduction in the epilogue";
+          return false;
+        }
+        sp.rowred.push_back(v);
+      } else if (!(kd == Kind::Unary || kd == Kind::Binary || kd == Kind::Broadcast)) {
+        *why = std::string("gemm: epilogue cannot hold ") + op_name(n.op);
+        return false;
+      }
+      sp.epi.insert(v);
+    } else {
+      if (!allow_reduce || kd != Kind::Reduce) {
+        *why = "gemm: node is neither prologue nor epilogue";
+        return false;
+      }
+      sp.side.push_back(v);
+    }
+  }
+  // prologue nodes may only feed prologue nodes or products
+  for (int v : sp.pro)
+    for (int c : g.consumers[v])
+      if (ki.in.count(c) && !sp.pro.count(c) && !in_vec(sp.mms, c) && !in_vec(sp.side, c)) {
+        *why = "gemm: a prologue value is also used after the product";
+        return false;
+      }
+  if (sp.conv && !sp.pro.empty()) {
+    *why = "conv: operand prologue not supported";
+    return false;
+  }
+  // epilogue shapes broadcast to the iteration space
+  for (int v : sp.epi) {
+    const Shape& s = g.nodes[v].shape;
+    if (s.size() > sp.OUT.size()) {
+      *why = "gemm: epilogue rank too large";
+      return false;
+    }
+    for (size_t d = 0; d < s.size(); ++d) {
+      int64_t t = sp.OUT[d + sp.OUT.size() - s.size()];
+      if (s[d] != t && s[d] != 1) {
+        *why = "gemm: epilogue shape does not broadcast to the product";
+        return false;
+      }
+    }
+    for (int u : g.nodes[v].in)
+      if (ki.in.count(u) && !sp.epi.count(u) && !in_vec(sp.mms, u)) {
+        *why = "gemm: epilogue reads a prologue value";
+        return false;
+      }
+  }
+  for (int o : ki.k.outs) {
+    if (sp.pro.count(o)) {
+      *why = "gemm: prologue output";
+      return false;
+    }
+    if (sp.epi.count(o) && g.nodes[o].shape != sp.OUT && sp.rowred.empty()) {
+      // broadcast-shaped epilogue outputs are stored where broadcast dims are 0
+    }
+  }
+  return true;
+}
+
+bool match_gemm(const KInfo& ki, std::string* why) {
+  GemmSpec sp;
+  if (!analyze_gemm(ki, sp, why, false)) return false;
+  if (sp.conv) return false;
+  if (sp.mms.size() > 1 && sp.Ntot > 128) {
+    *why = "gemm: combined right operands wider than one tile";
+    return false;
+  }
+  return true;
+}
+
+bool match_conv(const KInfo& ki, std::string* why) {
+  GemmSpec sp;
+  if (!analyze_gemm(ki, sp, why, false)) return false;
+  return sp.conv;
+}
+
+// ---------------------------------------------------------------------------
+
+void choose_tiles(GemmSpec& sp, bool split) {
+  bool f32 = sp.mtype == KORCH_F32;
+  sp.kstep = f32 ? 4 : 32;
+  if (f32)
+    sp.BK = 16;
+  else if (sp.K % 64 == 0)
+    sp.BK = 64;
+  else if (sp.K % 32 == 0 || sp.K < 64)
+    sp.BK = 32;
+  else
+    sp.BK = 64;
+  int64_t nt = sp.mms.size() > 1 ? sp.Ntot : sp.N;
+  if (nt <= 16)
+    sp.BN = 16;
+  else if (nt <= 32)
+    sp.BN = 32;
+  else if (nt <= 64)
+    sp.BN = 64;
+  else
+    sp.BN = 128;
+  sp.BM = 128;
+  int64_t tiles = (sp.M + 127) / 128 * ((sp.N + sp.BN - 1) / sp.BN) * sp.batch;
+  if (!split && tiles < 240 && sp.M > 64) sp.BM = 64;
+  if (split) sp.BM = sp.M <= 16 ? 16 : (sp.M <= 32 ? 32 : 64);
+  sp.WN = sp.BN >= 64 ? 2 : 1;
+  sp.WM = 4 / sp.WN;
+  while (sp.BM / sp.WM < 16) {
+    // fewer waves along M; put the rest along N when possible
+    if (sp.WN < 4 && sp.BN / (sp.WN * 2) >= 16) {
+      sp.WN *= 2;
+      sp.WM = 4 / sp.WN;
+    } else {
+      break;
+    }
+  }
+  if (sp.BM / sp.WM < 16) sp.WM = std::max(1, sp.BM / 16);
+  sp.WTM = sp.BM / sp.WM;
+  sp.WTN = sp.BN / sp.WN;
+  sp.FM = sp.WTM / 16;
+  sp.FN = sp.WTN / 16;
+  sp.VA = 16 / dtype_bytes(sp.mtype);
+  sp.VB = sp.VA;
+  sp.BKP = sp.BK + (f32 ? 4 : 8);
+  sp.LDC = sp.BN + 4;
+}
+
+// Emits a lambda `fetchX(k0)` that evaluates the operand (with its prologue)
+// for this thread's slots of a BM x BK (A) or BN x BK (B) tile into registers,
+// and `stashX(buf)` that converts and writes them to LDS in [row][k] layout.
+std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot) {
+  const Graph& g = ki.g;
+  int V = isA ? sp.VA : sp.VB;
+  int rows = isA ? sp.BM : sp.BN;
+  int nslots = rows * sp.BK / V;
+  int per = (nslots + 255) / 256;
+  std::string X = isA ? "A" : "B";
+  std::string T = ctype(sp.mtype);
+  std::string lds = isA ? "As" : "Bs";
+  std::ostringstream s;
+  // batch coordinates of the operand
+  auto batch_idx = [&](int node) {
+    const Shape& sh = g.nodes[node].shape;
+    Shape ob(sp.OUT.begin(), sp.OUT.begin() + sp.nb);
+    Shape nbsh(sh.begin(), sh.end() - 2);
+    std::vector<Ix> zc;
+    for (int d = 0; d < sp.nb; ++d) zc.push_back(Ix::var("z" + std::to_string(d)));
+    return broadcast_index(nbsh, ob, zc);
+  };
+  // Generates loader code for one product operand: value at (row, k) for `node`.
+  // axis_k: vector along k (row fixed) else vector along the row.
+  auto emit_operand = [&](int node, bool axis_k, bool guarded, const std::string& rowv, const std::string& kv,
+                          const std::string& rowlim, int64_t colshift) -> std::string {
+    Emitter em(g);
+    em.inset = sp.pro;
+    em.argslot = slot;
+    em.vec = V;
+    em.force_gather = guarded;
+    std::vector<Ix> idx = batch_idx(node);
+    Ix r = axis_k ? Ix::var(rowv, 0, 1) : Ix::var(rowv, 1, V);
+    Ix k = axis_k ? Ix::var(kv, 1, V) : Ix::var(kv, 0, 1);
+    if (colshift) r = ix_addk(r, -colshift);
+    if (isA) {
+      idx.push_back(r);
+      idx.push_back(k);
+    } else {
+      idx.push_back(k);
+      idx.push_back(r);
+    }
+    std::string val = em.value(node, idx);
+    std::ostringstream o;
+    if (!guarded) {
+      o << em.pre.str() << "#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) {\n"
+        << em.body.str() << "        dst[e] = " << val << ";\n      }\n";
+    } else {
+      std::string cond = axis_k ? "(" + rowv + " < " + rowlim + " && " + kv + " + e < " + std::to_string(sp.K) + ")"
+                                : "(" + rowv + " + e < " + rowlim + " && " + kv + " < " + std::to_string(sp.K) + ")";
+      o << "#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) {\n        dst[e] = 0.0f;\n        if "
+        << cond << " {\n"
+        << em.pre.str() << em.body.str() << "        dst[e] = " << val << ";\n        }\n      }\n";
+    }
+    return o.str();
+  };
+  auto count_gathers = [&](int node, bool axis_k) {
+    Emitter em(g);
+    em.inset = sp.pro;
+    em.argslot = slot;
+    em.vec = V;
+    std::vector<Ix> idx = batch_idx(node);
+    Ix r = axis_k ? Ix::var("r_", 0, 1) : Ix::var("r_", 1, V);
+    Ix k = axis_k ? Ix::var("k_", 1, V) : Ix::var("k_", 0, 1);
+    if (isA) {
+      idx.push_back(r);
+      idx.push_back(k);
+    } else {
+      idx.push_back(k);
+      idx.push_back(r);
+    }
+    em.value(node, idx);
+    return em.n_gather;
+  };
+  std::vector<int> nodes = isA ? std::vector<int>{sp.A} : sp.Bs;
+  bool axis_k = true;
+  if (!sp.conv) {
+    int gk = 0, gr = 0;
+    for (int n : nodes) {
+      gk += count_gathers(n, true);
+      gr += count_gathers(n, false);
+    }
+    axis_k = !(gr < gk);
+  } else {
+    axis_k = isA ? true : false;  // X: channels contiguous; W as [K, N]: N contiguous
+  }
+  int kper = axis_k ? sp.BK / V : sp.BK;
+  // slot s -> (row, k): axis_k: row = s / (BK/V), kk = (s % (BK/V)) * V
+  //                     axis_row: kk = s / (rows/V), row = (s % (rows/V)) * V
+  s << "  float r" << X << "[" << per << "][" << V << "];\n";
+  s << "  auto fetch" << X << " = [&](const i64 k0) {\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+  s << "    const int sl = tid + i * 256;\n";
+  if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+  if (axis_k)
+    s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
+  else
+    s << "    const int kl = sl / " << rows / V << ", rl = (sl % " << rows / V << ") * " << V << ";\n";
+  std::string base = isA ? "m0" : "n0";
+  s << "    const i64 rg = " << base << " + rl, kg = k0 + kl;\n";
+  s << "    float* dst = r" << X << "[i];\n";
+  if (sp.conv && isA) {
+    // implicit GEMM: row = output pixel, k = (ky, kx, ci)
+    bool vecok = sp.Cin % V == 0;
+    s << "    {\n      const i64 oy = rg / " << sp.Wo << ", ox = rg % " << sp.Wo << ";\n";
+    s << "      const i64 tap = kg / " << sp.Cin << ", ci = kg % " << sp.Cin << ";\n";
+    s << "      const i64 iy = oy * " << sp.stride << " + tap / " << sp.KW << " - " << sp.pad << ";\n";
+    s << "      const i64 ix = ox * " << sp.stride << " + tap % " << sp.KW << " - " << sp.pad << ";\n";
+    std::string P = "((const " + T + "*)a.p[" + std::to_string(slot.at(sp.A)) + "])";
+    std::string bofs = sp.nb ? "z0 * " + std::to_string(sp.H * sp.W * sp.Cin) + "LL + " : "";
+    s << "      const bool ok = rg < " << sp.M << "LL && kg < " << sp.K << "LL && iy >= 0 && iy < " << sp.H
+      << " && ix >= 0 && ix < " << sp.W << ";\n";
+    if (vecok) {
+      s << "      if (ok) ldv<" << V << ">(dst, " << P << " + " << bofs << "(iy * " << sp.W << " + ix) * " << sp.Cin
+        << "LL + ci);\n";
+      s << "      else {\n#pragma unroll\n        for (int e = 0; e < " << V << "; ++e) dst[e] = 0.0f;\n      }\n";
+    } else {
+      s << "#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) {\n";
+      s << "        const i64 k2 = kg + e, tap2 = k2 / " << sp.Cin << ", ci2 = k2 % " << sp.Cin << ";\n";
+      s << "        const i64 iy2 = oy * " << sp.stride << " + tap2 / " << sp.KW << " - " << sp.pad << ";\n";
+      s << "        const i64 ix2 = ox * " << sp.stride << " + tap2 % " << sp.KW << " - " << sp.pad << ";\n";
+      s << "        dst[e] = (rg < " << sp.M << "LL && k2 < " << sp.K << "LL && iy2 >= 0 && iy2 < " << sp.H
+        << " && ix2 >= 0 && ix2 < " << sp.W << ") ? ld1(" << P << " + " << bofs << "(iy2 * " << sp.W
+        << " + ix2) * " << sp.Cin << "LL + ci2) : 0.0f;\n      }\n";
+    }
+    s << "    }\n";
+  } else if (sp.conv && !isA) {
+    // weights [KH, KW, Cin, Cout] are a row-major [K, N] matrix
+    std::string P = "((const " + T + "*)a.p[" + std::to_string(slot.at(sp.Bs[0])) + "])";
+    s << "    if (kg < " << sp.K << "LL && rg + " << V << " <= " << sp.N << "LL) ldv<" << V << ">(dst, " << P
+      << " + kg * " << sp.N << "LL + rg);\n";
+    s << "    else {\n#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) dst[e] = (kg < " << sp.K
+      << "LL && rg + e < " << sp.N << "LL) ? ld1(" << P << " + kg * " << sp.N << "LL + rg + e) : 0.0f;\n    }\n";
+  } else {
+    // one or several product operands (B columns side by side)
+    for (size_t j = 0; j < nodes.size(); ++j) {
+      int64_t lo = isA ? 0 : (sp.mms.size() > 1 ? sp.offj[j] : 0);
+      int64_t nj = isA ? sp.M : sp.Nj[j];
+      std::string rowv = "rg";
+      std::string lim = std::to_string(lo + nj);
+      if (nodes.size() > 1) {
+        int64_t hi = j + 1 < nodes.size() ? sp.offj[j + 1] : (int64_t)1 << 40;
+        s << "    " << (j ? "else " : "") << "if (rg < " << hi << "LL) {\n";
+      } else {
+        s << "    {\n";
+      }
+      std::string fastc = axis_k ? "(rg < " + lim + "LL && kg + " + std::to_string(V) + " <= " +
+                                       std::to_string(sp.K) + "LL)"
+                                 : "(rg + " + std::to_string(V) + " <= " + lim + "LL && kg < " +
+                                       std::to_string(sp.K) + "LL)";
+      s << "      if " << fastc << " {\n"
+        << emit_operand(nodes[j], axis_k, false, rowv, "kg", lim + "LL", lo) << "      } else {\n"
+        << emit_operand(nodes[j], axis_k, true, rowv, "kg", lim + "LL", lo) << "      }\n    }\n";
+    }
+    if (nodes.size() > 1)
+      s << "    else {\n#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) dst[e] = 0.0f;\n    }\n";
+  }
+  s << "  }\n  };\n";
+  // stash: fp32 registers -> LDS [row][k] of the MFMA operand type
+  s << "  auto stash" << X << " = [&](const int buf) {\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+  s << "    const int sl = tid + i * 256;\n";
+  if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+  if (axis_k) {
+    s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
+    s << "    stv<" << V << ">(" << lds << " + buf * " << rows * sp.BKP << " + rl * " << sp.BKP << " + kl, r" << X
+      << "[i]);\n";
+  } else {
+    s << "    const int kl = sl / " << rows / V << ", rl = (sl % " << rows / V << ") * " << V << ";\n";
+    s << "#pragma unroll\n    for (int e = 0; e < " << V << "; ++e) " << lds << "[buf * " << rows * sp.BKP
+      << " + (rl + e) * " << sp.BKP << " + kl] = fromf<" << T << ">(r" << X << "[i][e]);\n";
+  }
+  s << "  }\n  };\n";
+  return s.str();
+}
+
+// The MFMA main loop over k-tiles [kt0, kt1) of the contraction.
+std::string mfma_mainloop(const GemmSpec& sp) {
+  std::ostringstream s;
+  bool f32 = sp.mtype == KORCH_F32;
+  std::string T = ctype(sp.mtype);
+  s << "  f32x4 acc[" << sp.FM << "][" << sp.FN << "];\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
+    << "; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
+  s << "  auto compute = [&](const int buf) {\n";
+  s << "    const " << T << "* Ab = As + buf * " << sp.BM * sp.BKP << ";\n";
+  s << "    const " << T << "* Bb = Bs + buf * " << sp.BN * sp.BKP << ";\n";
+  s << "#pragma unroll\n    for (int kk = 0; kk < " << sp.BK / sp.kstep << "; ++kk) {\n";
+  if (f32) {
+    s << "      float af[" << sp.FM << "], bf[" << sp.FN << "];\n";
+    s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i) af[i] = Ab[(wm * " << sp.WTM
+      << " + i * 16 + (l & 15)) * " << sp.BKP << " + kk * 4 + (l >> 4)];\n";
+    s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = Bb[(wn * " << sp.WTN
+      << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 4 + (l >> 4)];\n";
+    s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n      for (int j = 0; j < "
+      << sp.FN << "; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i], bf[j], acc[i][j], 0, 0, 0);\n";
+  } else {
+    std::string V8 = sp.mtype == KORCH_F16 ? "f16x8" : "bf16x8";
+    std::string fn = sp.mtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16"
+                                           : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
+    s << "      " << V8 << " af[" << sp.FM << "], bf[" << sp.FN << "];\n";
+    s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i) af[i] = *(const " << V8 << "*)(Ab + (wm * "
+      << sp.WTM << " + i * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
+    s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = *(const " << V8 << "*)(Bb + (wn * "
+      << sp.WTN << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
+    s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n      for (int j = 0; j < "
+      << sp.FN << "; ++j) acc[i][j] = " << fn << "(af[i], bf[j], acc[i][j], 0, 0, 0);\n";
+  }
+  s << "    }\n  };\n";
+  s << "  fetchA((i64)kt0 * " << sp.BK << "); fetchB((i64)kt0 * " << sp.BK << ");\n";
+  s << "  stashA(0); stashB(0);\n  __syncthreads();\n";
+  s << "  for (int kt = kt0; kt < kt1; ++kt) {\n";
+  s << "    const int cur = (kt - kt0) & 1;\n";
+  s << "    if (kt + 1 < kt1) { fetchA((i64)(kt + 1) * " << sp.BK << "); fetchB((i64)(kt + 1) * " << sp.BK << "); }\n";
+  s << "    compute(cur);\n";
+  s << "    if (kt + 1 < kt1) { stashA(cur ^ 1); stashB(cur ^ 1); }\n";
+  s << "    __syncthreads();\n  }\n";
+  // accumulators -> LDS C tile (fp32)
+  s << "  float* Cs = (float*)smem;\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
+    << "; ++j)\n#pragma unroll\n  for (int r = 0; r < 4; ++r) Cs[(wm * " << sp.WTM << " + i * 16 + (l >> 4) * 4 + r) * "
+    << sp.LDC << " + wn * " << sp.WTN << " + j * 16 + (l & 15)] = acc[i][j][r];\n";
+  s << "  __syncthreads();\n";
+  return s.str();
+}
+
+size_t gemm_smem_bytes(const GemmSpec& sp) {
+  size_t ab = (size_t)2 * (sp.BM + sp.BN) * sp.BKP * dtype_bytes(sp.mtype);
+  size_t c = (size_t)sp.BM * sp.LDC * 4;
+  return std::max(ab, c);
+}
+
+// Pointwise epilogue over the C tile: every kernel output at (batch, m, n).
+std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
+                          const std::string& cs_row) {
+  const Graph& g = ki.g;
+  int maxb = 2;
+  for (int o : ki.k.outs) maxb = std::max(maxb, dtype_bytes(g.nodes[o].dtype));
+  int VE = 16 / maxb;
+  while (VE > 1 && (sp.N % VE || sp.BN % VE)) VE /= 2;
+  int cols = (int)std::min<int64_t>(sp.BN, sp.mms.size() > 1 ? sp.N : sp.BN);
+  cols = (cols + VE - 1) / VE * VE;
+  Emitter em(g);
+  em.inset = sp.epi;
+  for (int m : sp.mms) em.inset.insert(m);
+  em.argslot = slot;
+  em.vec = VE;
+  // iteration coordinates of OUT
+  std::vector<Ix> it;
+  for (int d = 0; d < sp.nb; ++d) it.push_back(Ix::var("z" + std::to_string(d)));
+  if (sp.conv) {
+    it.push_back(Ix::var("oy"));
+    it.push_back(Ix::var("ox"));
+  } else {
+    it.push_back(Ix::var("m"));
+  }
+  it.push_back(Ix::var("n", 1, VE));
+  std::map<std::string, std::string> canon;
+  for (size_t j = 0; j < sp.mms.size(); ++j) {
+    int mm = sp.mms[j];
+    auto bi = broadcast_index(g.nodes[mm].shape, sp.OUT, it);
+    std::string base = cs_row + " + " + std::to_string(sp.mms.size() > 1 ? sp.offj[j] : 0);
+    if (sp.Nj[j] == 1 && sp.N != 1)
+      canon[Emitter::key(mm, bi)] = "Cs[" + base + "]";
+    else
+      canon[Emitter::key(mm, bi)] = "Cs[" + base + " + nl + e]";
+  }
+  em.provide = [&](int node, const std::vector<Ix>& idx, std::string* out) {
+    if (!in_vec(sp.mms, node)) return false;
+    auto f = canon.find(Emitter::key(node, idx));
+    if (f == canon.end()) fail(KORCH_E_UNSUPPORTED, "gemm: epilogue reads the product at another index");
+    *out = f->second;
+    return true;
+  };
+  std::ostringstream decl, after;
+  for (int o : ki.k.outs) {
+    const Node& on = g.nodes[o];
+    auto bi = broadcast_index(on.shape, sp.OUT, it);
+    std::string v = em.value(o, bi);
+    std::string T = ctype(on.dtype);
+    std::string P = "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])";
+    auto st = strides_of(on.shape);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], st[d], VE));
+    if (on.shape == sp.OUT && off.affine && off.c == 1 && off.al % VE == 0) {
+      std::string arr = "_o" + std::to_string(o);
+      decl << "      float " << arr << "[" << VE << "];\n";
+      em.body << "        " << arr << "[e] = " << v << ";\n";
+      after << "      stv<" << VE << ">(" << P << " + " << off.b << ", " << arr << ");\n";
+    } else {
+      std::string cond;
+      int lead = (int)sp.OUT.size() - (int)on.shape.size();
+      for (int d = 0; d < (int)sp.OUT.size(); ++d) {
+        bool bc = d < lead || (on.shape[d - lead] == 1 && sp.OUT[d] != 1);
+        if (!bc) continue;
+        if (!cond.empty()) cond += " && ";
+        cond += "(" + it[d].at() + " == 0)";
+      }
+      em.body << "        if (" << (cond.empty() ? "true" : cond) << ") st1(" << P << " + " << off.at() << ", " << v
+              << ");\n";
+    }
+  }
+  std::ostringstream s;
+  s << "  for (int s_ = tid; s_ < " << sp.BM * (cols / VE) << "; s_ += 256) {\n";
+  s << "    const int ml = s_ / " << cols / VE << ", nl = (s_ % " << cols / VE << ") * " << VE << ";\n";
+  s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
+  s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n";
+  if (sp.conv) s << "      const i64 oy = m / " << sp.Wo << "LL, ox = m % " << sp.Wo << "LL;\n";
+  s << em.pre.str() << decl.str();
+  s << "#pragma unroll\n      for (int e = 0; e < " << VE << "; ++e) {\n" << em.body.str() << "      }\n";
+  s << after.str() << "    }\n  }\n";
+  return s.str();
+}
+
+std::string gemm_prologue_common(const GemmSpec& sp) {
+  std::ostringstream s;
+  std::string T = ctype(sp.mtype);
+  s << "  __shared__ __attribute__((aligned(16))) char smem[" << gemm_smem_bytes(sp) << "];\n";
+  s << "  " << T << "* As = (" << T << "*)smem;\n";
+  s << "  " << T << "* Bs = As + " << 2 * sp.BM * sp.BKP << ";\n";
+  s << "  const int tid = threadIdx.x, l = tid & 63, wave = tid >> 6;\n";
+  s << "  const int wm = wave / " << sp.WN << ", wn = wave % " << sp.WN << ";\n";
+  s << "  (void)wm; (void)wn;\n";
+  return s.str();
+}
+
+GenKernel gen_gemm(const KInfo& ki, int index) {
+  GemmSpec sp;
+  std::string why;
+  if (!analyze_gemm(ki, sp, &why, false)) fail(KORCH_E_UNSUPPORTED, why);
+  choose_tiles(sp, false);
+  GenKernel gk;
+  gk.family = sp.conv ? KORCH_FAM_CONV : KORCH_FAM_GEMM;
+  gk.name = kernel_name(index, sp.conv ? "conv" : "gemm");
+  std::map<int, int> slot;
+  ki.assign_args(gk, slot);
+  int64_t ntn = sp.mms.size() > 1 ? 1 : (sp.N + sp.BN - 1) / sp.BN;
+  int64_t ntm = (sp.M + sp.BM - 1) / sp.BM;
+  int64_t KT = (sp.K + sp.BK - 1) / sp.BK;
+  std::ostringstream s;
+  s << source_header((int)gk.args.size());
+  s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
+  s << gemm_prologue_common(sp);
+  s << "  const i64 n0 = (i64)blockIdx.x * " << sp.BN << ", m0 = (i64)blockIdx.y * " << sp.BM << ";\n";
+  s << "  i64 q_ = blockIdx.z;\n";
+  for (int d = sp.nb - 1; d >= 0; --d)
+    s << "  const i64 z" << d << " = q_ % " << sp.OUT[d] << "LL; q_ /= " << sp.OUT[d] << "LL;\n";
+  s << "  const int kt0 = 0, kt1 = " << KT << ";\n";
+  s << operand_loader(ki, sp, true, slot);
+  s << operand_loader(ki, sp, false, slot);
+  s << mfma_mainloop(sp);
+  s << gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(sp.LDC));
+  s << "}\n";
+  gk.source = s.str();
+  gk.grid[0] = (int)ntn;
+  gk.grid[1] = (int)ntm;
+  gk.grid[2] = (int)sp.batch;
+  gk.lds_bytes = (int)gemm_smem_bytes(sp);
+  ki.fill_cost(gk);
+  return gk;
+}
+
+}  // namespace korch

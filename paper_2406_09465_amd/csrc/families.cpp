@@ -1,0 +1,645 @@
+// Family matching and the memory-bound families: pointwise chains, row
+// programs (last-axis reductions with prologue / broadcast-back epilogue, as
+// in softmax and LayerNorm fission) and single column reductions.
+//
+// A candidate with no linear primitive is memory-intensive and one with a
+// linear primitive is compute-intensive (Korch, Section 5.2); here each class
+// maps to hand-written gfx950 skeletons instead of a tuner or a vendor library.
+#include <algorithm>
+#include <cmath>
+
+#include "families.h"
+
+namespace korch {
+
+KInfo::KInfo(const Graph& gg, const KernelDesc& kk) : g(gg), k(kk) {
+  in.insert(k.prims.begin(), k.prims.end());
+  ext = external_inputs(g, k);
+  for (int v : k.prims) {
+    Kind kd = op_kind(g.nodes[v].op);
+    if (kd == Kind::Linear) linear.push_back(v);
+    if (kd == Kind::Reduce) reduces.push_back(v);
+    if (kd == Kind::Layout) layouts.push_back(v);
+  }
+}
+
+bool KInfo::ancestor(int u, int v) const { return g.reach[u].test(v); }
+
+void KInfo::assign_args(GenKernel& gk, std::map<int, int>& slot) const {
+  for (int u : ext) {
+    slot[u] = (int)gk.args.size();
+    ArgRef r;
+    r.kind = ArgRef::Tensor;
+    r.node = u;
+    gk.args.push_back(r);
+  }
+  for (int o : k.outs) {
+    ArgRef r;
+    r.kind = ArgRef::Output;
+    r.node = o;
+    gk.args.push_back(r);
+  }
+}
+
+int KInfo::out_slot(int o) const {
+  auto it = std::find(k.outs.begin(), k.outs.end(), o);
+  return (int)ext.size() + (int)(it - k.outs.begin());
+}
+
+void KInfo::fill_cost(GenKernel& gk) const {
+  double bytes = 0, flops = 0;
+  for (int u : ext) bytes += (double)numel(g.nodes[u].shape) * dtype_bytes(g.nodes[u].dtype);
+  for (int o : k.outs) bytes += (double)numel(g.nodes[o].shape) * dtype_bytes(g.nodes[o].dtype);
+  for (int v : linear) {
+    const Node& n = g.nodes[v];
+    if (n.op == KORCH_MATMUL) {
+      int64_t kdim = g.nodes[n.in[0]].shape.back();
+      flops += 2.0 * (double)numel(n.shape) * (double)kdim;
+    } else {
+      const Shape& w = g.nodes[n.in[1]].shape;
+      flops += 2.0 * (double)numel(n.shape) * (double)(w[0] * w[1] * w[2]);
+    }
+  }
+  gk.alg_bytes = bytes;
+  gk.alg_flops = flops;
+}
+
+std::string kernel_name(int index, const char* fam) { return "korch_k" + std::to_string(index) + "_" + fam; }
+
+static int64_t pow2ceil(int64_t x) {
+  int64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// ---------------------------------------------------------------------------
+// Pointwise family: elementwise, broadcast and layout primitives evaluated per
+// output element; layout primitives become load address maps.
+// ---------------------------------------------------------------------------
+
+bool match_pointwise(const KInfo& ki, std::string* why) {
+  if (!ki.linear.empty() || !ki.reduces.empty()) {
+    *why = "pointwise: has linear or reduce primitives";
+    return false;
+  }
+  // outputs must broadcast to the largest output
+  const Graph& g = ki.g;
+  int big = ki.k.outs[0];
+  for (int o : ki.k.outs)
+    if (numel(g.nodes[o].shape) > numel(g.nodes[big].shape)) big = o;
+  const Shape& IT = g.nodes[big].shape;
+  for (int o : ki.k.outs) {
+    const Shape& s = g.nodes[o].shape;
+    if (s.size() > IT.size()) {
+      *why = "pointwise: output ranks differ";
+      return false;
+    }
+    for (size_t d = 0; d < s.size(); ++d) {
+      int64_t t = IT[d + IT.size() - s.size()];
+      if (s[d] != t && s[d] != 1) {
+        *why = "pointwise: outputs do not broadcast to one iteration space";
+        return false;
+      }
+    }
+  }
+  return true;
+}
+
+GenKernel gen_pointwise(const KInfo& ki, int index) {
+  const Graph& g = ki.g;
+  GenKernel gk;
+  gk.family = KORCH_FAM_POINTWISE;
+  gk.name = kernel_name(index, "pointwise");
+  std::map<int, int> slot;
+  ki.assign_args(gk, slot);
+  int big = ki.k.outs[0];
+  for (int o : ki.k.outs)
+    if (numel(g.nodes[o].shape) > numel(g.nodes[big].shape)) big = o;
+  Shape IT = g.nodes[big].shape;
+  if (IT.empty()) IT = {1};
+  int R = (int)IT.size();
+  int maxb = 2;
+  for (int o : ki.k.outs) maxb = std::max(maxb, dtype_bytes(g.nodes[o].dtype));
+  int vec = 16 / maxb;
+  while (vec > 1 && IT.back() % vec) vec /= 2;
+  int64_t total = numel(IT);
+  int64_t nt = total / vec;
+  Emitter em(g);
+  em.inset = ki.in;
+  em.argslot = slot;
+  em.vec = vec;
+  std::vector<Ix> it(R);
+  for (int d = 0; d < R; ++d)
+    it[d] = d == R - 1 ? Ix::var("c" + std::to_string(d), 1, vec) : Ix::var("c" + std::to_string(d), 0, 1);
+  std::ostringstream stores, decl, after;
+  for (int o : ki.k.outs) {
+    const Node& on = g.nodes[o];
+    Shape os = on.shape;
+    auto idx = broadcast_index(os, IT, it);
+    std::string v = em.value(o, idx);
+    std::string T = ctype(on.dtype);
+    std::string P = "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])";
+    if (numel(os) == total) {
+      std::string arr = "o" + std::to_string(o);
+      decl << "  float " << arr << "[" << vec << "];\n";
+      em.body << "    " << arr << "[e] = " << v << ";\n";
+      after << "  stv<" << vec << ">(" << P << " + t * " << vec << ", " << arr << ");\n";
+    } else {
+      auto st = strides_of(os);
+      Ix off = Ix::k(0);
+      for (size_t d = 0; d < os.size(); ++d) off = ix_add(off, ix_mulk(idx[d], st[d], vec));
+      std::string cond;
+      int lead = R - (int)os.size();
+      for (int d = 0; d < R; ++d) {
+        bool bcast = d < lead || (os[d - lead] == 1 && IT[d] != 1);
+        if (!bcast) continue;
+        if (!cond.empty()) cond += " && ";
+        cond += "(" + it[d].at() + " == 0)";
+      }
+      em.body << "    if (" << (cond.empty() ? "true" : cond) << ") st1(" << P << " + " << off.at() << ", " << v
+              << ");\n";
+    }
+  }
+  std::ostringstream s;
+  s << source_header((int)gk.args.size());
+  s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
+  s << "  const i64 t = (i64)blockIdx.x * 256 + threadIdx.x;\n";
+  s << "  if (t >= " << nt << "LL) return;\n";
+  s << "  i64 r_ = t;\n";
+  s << "  const i64 c" << R - 1 << " = (r_ % " << IT[R - 1] / vec << "LL) * " << vec << "; r_ /= " << IT[R - 1] / vec
+    << "LL;\n";
+  for (int d = R - 2; d >= 0; --d)
+    s << "  const i64 c" << d << " = r_ % " << IT[d] << "LL; r_ /= " << IT[d] << "LL;\n";
+  s << em.pre.str() << decl.str();
+  s << "#pragma unroll\n  for (int e = 0; e < " << vec << "; ++e) {\n" << em.body.str() << "  }\n";
+  s << after.str() << "}\n";
+  gk.source = s.str();
+  gk.grid[0] = (int)((nt + 255) / 256);
+  ki.fill_cost(gk);
+  return gk;
+}
+
+// ---------------------------------------------------------------------------
+// Row family: every node is a full row tensor F = [..., L], a keepdim row
+// statistic [..., 1] or a no-keepdim statistic [...]; reductions run over the
+// last axis.  A group of G lanes holds one row in registers (NC chunks of VEC
+// contiguous elements per lane); reductions are lane-butterflies.
+// ---------------------------------------------------------------------------
+
+enum RowCls { FULL = 0, STATK = 1, STATN = 2 };
+
+struct RowShape {
+  Shape F, FK, FN;
+  int64_t L = 0, R = 0;
+};
+
+static bool row_shapes(const KInfo& ki, RowShape& rs, std::map<int, int>& cls, std::string* why) {
+  const Graph& g = ki.g;
+  if (ki.reduces.empty()) {
+    *why = "row: no reduction";
+    return false;
+  }
+  for (int r : ki.reduces) {
+    const Node& n = g.nodes[r];
+    const Shape& s = g.nodes[n.in[0]].shape;
+    if (n.axis != (int)s.size() - 1) {
+      *why = "row: reduction is not over the last axis";
+      return false;
+    }
+    if (rs.F.empty())
+      rs.F = s;
+    else if (rs.F != s) {
+      *why = "row: reductions over different shapes";
+      return false;
+    }
+  }
+  rs.L = rs.F.back();
+  if (rs.L < 2) {
+    *why = "row: row length < 2";
+    return false;
+  }
+  rs.R = numel(rs.F) / rs.L;
+  rs.FK = rs.F;
+  rs.FK.back() = 1;
+  rs.FN = Shape(rs.F.begin(), rs.F.end() - 1);
+  for (int v : ki.k.prims) {
+    const Node& n = g.nodes[v];
+    Kind kd = op_kind(n.op);
+    if (kd != Kind::Unary && kd != Kind::Binary && kd != Kind::Reduce) {
+      *why = std::string("row: unsupported primitive ") + op_name(n.op);
+      return false;
+    }
+    if (n.shape == rs.F)
+      cls[v] = FULL;
+    else if (n.shape == rs.FK)
+      cls[v] = STATK;
+    else if (n.shape == rs.FN)
+      cls[v] = STATN;
+    else {
+      *why = "row: node shape is neither a row nor a row statistic";
+      return false;
+    }
+    if (kd == Kind::Reduce && cls[v] == FULL) {
+      *why = "row: reduce output has full shape";
+      return false;
+    }
+  }
+  // in-kernel inputs must be compatible with the consumer's class
+  for (int v : ki.k.prims) {
+    const Node& n = g.nodes[v];
+    for (int u : n.in) {
+      if (!ki.in.count(u)) continue;
+      int cu = cls[u], cv = cls[v];
+      if (op_kind(n.op) == Kind::Reduce) {
+        if (cu != FULL) {
+          *why = "row: reduce input is not a full row";
+          return false;
+        }
+        continue;
+      }
+      bool ok = (cv == FULL && (cu == FULL || cu == STATK)) || (cv == STATK && cu == STATK) ||
+                (cv == STATN && cu == STATN);
+      if (!ok) {
+        *why = "row: incompatible operand classes";
+        return false;
+      }
+    }
+  }
+  return true;
+}
+
+bool match_row(const KInfo& ki, std::string* why) {
+  if (!ki.linear.empty()) {
+    *why = "row: has linear primitives";
+    return false;
+  }
+  RowShape rs;
+  std::map<int, int> cls;
+  if (!row_shapes(ki, rs, cls, why)) return false;
+  return true;
+}
+
+// Lanes per row G, elements per vector VEC, chunks per lane NC.
+void choose_row_geometry(int64_t L, int elem_bytes, int& G, int& VEC, int& NC) {
+  int vmax = 16 / elem_bytes;
+  VEC = 1;
+  G = 64;
+  bool found = false;
+  for (int v = vmax; v >= 1; v /= 2) {
+    if (L % v) continue;
+    int64_t n = L / v;
+    if (n >= 64) {
+      if (n % 64 == 0) {
+        VEC = v;
+        G = 64;
+        found = true;
+        break;
+      }
+    } else {
+      VEC = v;
+      G = (int)pow2ceil(n);
+      found = true;
+      break;
+    }
+  }
+  if (!found) {
+    for (int v = vmax; v >= 1; v /= 2)
+      if (L % v == 0) {
+        VEC = v;
+        break;
+      }
+    G = 64;
+  }
+  NC = (int)((L / VEC + G - 1) / G);
+}
+
+GenKernel gen_row(const KInfo& ki, int index) {
+  const Graph& g = ki.g;
+  RowShape rs;
+  std::map<int, int> cls;
+  std::string why;
+  if (!row_shapes(ki, rs, cls, &why)) fail(KORCH_E_UNSUPPORTED, why);
+  GenKernel gk;
+  gk.family = KORCH_FAM_ROW;
+  gk.name = kernel_name(index, "row");
+  std::map<int, int> slot;
+  ki.assign_args(gk, slot);
+  int eb = 2;
+  for (int v : ki.k.prims) eb = std::max(eb, dtype_bytes(g.nodes[v].dtype));
+  for (int u : ki.ext) eb = std::max(eb, dtype_bytes(g.nodes[u].dtype));
+  int G, VEC, NC;
+  choose_row_geometry(rs.L, eb, G, VEC, NC);
+  if (NC * VEC > 64) fail(KORCH_E_UNSUPPORTED, "row: row too long for one wavefront's registers");
+  int RPB = 256 / G;
+  int RD = (int)rs.F.size() - 1;  // number of row dims
+  bool partial_last = (rs.L / VEC) % G != 0;
+  std::vector<Ix> rowc(RD);
+  for (int d = 0; d < RD; ++d) rowc[d] = Ix::var("r" + std::to_string(d));
+
+  std::ostringstream loads, comp, stores;
+  std::map<std::string, std::string> lmemo;
+  int tmp = 0;
+  auto chunk_guard = [&](int j) -> std::string {
+    if (j == NC - 1 && partial_last) return "cb" + std::to_string(j) + " < " + std::to_string(rs.L) + "LL";
+    return "";
+  };
+  // external tensor read in a full-row context at chunk j; returns an expression valid inside `for e`
+  auto ext_full = [&](int u, int j) -> std::string {
+    std::string key = std::to_string(u) + "/" + std::to_string(j);
+    auto f = lmemo.find(key);
+    if (f != lmemo.end()) return f->second;
+    std::vector<Ix> idx = rowc;
+    idx.push_back(Ix::var("cb" + std::to_string(j), 1, VEC));
+    auto bi = broadcast_index(g.nodes[u].shape, rs.F, idx);
+    auto st = strides_of(g.nodes[u].shape);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], st[d], VEC));
+    std::string T = ctype(g.nodes[u].dtype);
+    std::string P = "((const " + T + "*)a.p[" + std::to_string(slot.at(u)) + "])";
+    std::string name = "x" + std::to_string(tmp++);
+    std::string gd = chunk_guard(j);
+    std::string res;
+    if (off.affine && off.c == 0) {
+      loads << "  float " << name << " = 0.0f; " << (gd.empty() ? "" : "if (" + gd + ") ") << name << " = ld1(" << P
+            << " + " << off.b << ");\n";
+      res = name;
+    } else if (off.affine && off.c == 1 && off.al % VEC == 0) {
+      loads << "  float " << name << "[" << VEC << "]; " << (gd.empty() ? "" : "if (" + gd + ") ") << "ldv<" << VEC
+            << ">(" << name << ", " << P << " + " << off.b << ");\n";
+      res = name + "[e]";
+    } else {
+      res = "ld1(" + P + " + " + off.at() + ")";
+    }
+    lmemo[key] = res;
+    return res;
+  };
+  auto ext_stat = [&](int u, const Shape& ctx) -> std::string {
+    std::string key = std::to_string(u) + "/s" + std::to_string(ctx.size());
+    auto f = lmemo.find(key);
+    if (f != lmemo.end()) return f->second;
+    std::vector<Ix> idx = rowc;
+    if (ctx.size() == rs.F.size()) idx.push_back(Ix::k(0));
+    auto bi = broadcast_index(g.nodes[u].shape, ctx, idx);
+    auto st = strides_of(g.nodes[u].shape);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], st[d], 1));
+    std::string T = ctype(g.nodes[u].dtype);
+    std::string name = "x" + std::to_string(tmp++);
+    loads << "  const float " << name << " = ld1((const " << T << "*)a.p[" << slot.at(u) << "] + " << off.at()
+          << ");\n";
+    lmemo[key] = name;
+    return name;
+  };
+  auto operand = [&](int v, int u, int j) -> std::string {
+    // value of input u of node v, in v's context, at chunk j (full context) or as a statistic
+    int cv = cls[v];
+    if (ki.in.count(u)) {
+      if (cls[u] == FULL) return "v" + std::to_string(u) + "[" + std::to_string(j) + "][e]";
+      return "s" + std::to_string(u);
+    }
+    if (cv == FULL || op_kind(g.nodes[v].op) == Kind::Reduce) return ext_full(u, j);
+    return ext_stat(u, cv == STATK ? rs.FK : rs.FN);
+  };
+  for (int v : ki.k.prims) {
+    const Node& n = g.nodes[v];
+    Kind kd = op_kind(n.op);
+    std::string V = std::to_string(v);
+    if (kd == Kind::Reduce) {
+      bool isMax = n.op == KORCH_REDUCE_MAX;
+      comp << "  float s" << V << " = " << (isMax ? "-__builtin_huge_valf()" : "0.0f") << ";\n";
+      for (int j = 0; j < NC; ++j) {
+        std::string gd = chunk_guard(j);
+        comp << "  " << (gd.empty() ? "" : "if (" + gd + ") ") << "{\n#pragma unroll\n  for (int e = 0; e < " << VEC
+             << "; ++e) s" << V << " = "
+             << (isMax ? "k_max(s" + V + ", " + operand(v, n.in[0], j) + ")"
+                       : "s" + V + " + " + operand(v, n.in[0], j))
+             << ";\n  }\n";
+      }
+      comp << "  s" << V << " = " << (isMax ? "group_max<" : "group_sum<") << G << ">(s" << V << ");\n";
+      if (n.op == KORCH_REDUCE_MEAN) comp << "  s" << V << " = s" << V << " / " << flit((double)rs.L) << ";\n";
+      continue;
+    }
+    auto expr = [&](int j) {
+      if (kd == Kind::Unary) return unary_expr(n.op, operand(v, n.in[0], j));
+      if (n.attrs.has_scalar) return binary_expr(n.op, operand(v, n.in[0], j), flit(n.attrs.scalar));
+      return binary_expr(n.op, operand(v, n.in[0], j), operand(v, n.in[1], j));
+    };
+    if (cls[v] == FULL) {
+      comp << "  float v" << V << "[" << NC << "][" << VEC << "];\n";
+      for (int j = 0; j < NC; ++j) {
+        std::string gd = chunk_guard(j);
+        comp << "  " << (gd.empty() ? "" : "if (" + gd + ") ") << "{\n#pragma unroll\n  for (int e = 0; e < " << VEC
+             << "; ++e) v" << V << "[" << j << "][e] = " << expr(j) << ";\n  }\n";
+      }
+    } else {
+      comp << "  const float s" << V << " = " << expr(0) << ";\n";
+    }
+  }
+  for (int o : ki.k.outs) {
+    const Node& on = g.nodes[o];
+    std::string T = ctype(on.dtype);
+    std::string P = "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])";
+    if (cls[o] == FULL) {
+      for (int j = 0; j < NC; ++j) {
+        std::string gd = chunk_guard(j);
+        stores << "  if (rv" << (gd.empty() ? "" : " && " + gd) << ") stv<" << VEC << ">(" << P << " + row * "
+               << rs.L << "LL + cb" << j << ", v" << o << "[" << j << "]);\n";
+      }
+    } else {
+      stores << "  if (rv && lane == 0) st1(" << P << " + row, s" << o << ");\n";
+    }
+  }
+  std::ostringstream s;
+  s << source_header((int)gk.args.size());
+  s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
+  s << "  const int lane = threadIdx.x % " << G << ";\n";
+  s << "  const i64 row0 = (i64)blockIdx.x * " << RPB << " + threadIdx.x / " << G << ";\n";
+  s << "  const bool rv = row0 < " << rs.R << "LL;\n";
+  s << "  const i64 row = rv ? row0 : " << rs.R - 1 << "LL;\n";
+  s << "  i64 q_ = row;\n";
+  for (int d = RD - 1; d >= 0; --d) s << "  const i64 r" << d << " = q_ % " << rs.F[d] << "LL; q_ /= " << rs.F[d] << "LL;\n";
+  for (int j = 0; j < NC; ++j)
+    s << "  const i64 cb" << j << " = ((i64)" << j << " * " << G << " + lane) * " << VEC << ";\n";
+  s << loads.str() << comp.str() << stores.str() << "}\n";
+  gk.source = s.str();
+  gk.grid[0] = (int)((rs.R + RPB - 1) / RPB);
+  ki.fill_cost(gk);
+  return gk;
+}
+
+// ---------------------------------------------------------------------------
+// Column-reduction family: one reduction over a non-last axis, viewed as
+// [A, Lr, B]; lanes span B and Lr, partial results combine in LDS in a fixed
+// order (deterministic).  Elementwise / layout prologue and epilogue allowed.
+// ---------------------------------------------------------------------------
+
+bool match_colreduce(const KInfo& ki, std::string* why) {
+  const Graph& g = ki.g;
+  if (!ki.linear.empty() || ki.reduces.size() != 1) {
+    *why = "colreduce: needs exactly one reduction and no linear primitive";
+    return false;
+  }
+  int r = ki.reduces[0];
+  const Node& rn = g.nodes[r];
+  const Shape& S = g.nodes[rn.in[0]].shape;
+  if (rn.axis == (int)S.size() - 1) {
+    *why = "colreduce: last-axis reduction belongs to the row family";
+    return false;
+  }
+  for (int v : ki.k.prims) {
+    if (v == r) continue;
+    bool pro = ki.ancestor(v, r), epi = ki.ancestor(r, v);
+    if (!pro && !epi) {
+      *why = "colreduce: node unrelated to the reduction";
+      return false;
+    }
+    if (pro && g.nodes[v].shape != S && op_kind(g.nodes[v].op) != Kind::Layout) {
+      *why = "colreduce: prologue node shape differs";
+      return false;
+    }
+    if (pro && std::find(ki.k.outs.begin(), ki.k.outs.end(), v) != ki.k.outs.end()) {
+      *why = "colreduce: prologue node cannot be an output";
+      return false;
+    }
+    if (epi && g.nodes[v].shape != rn.shape) {
+      *why = "colreduce: epilogue node shape differs from the reduced shape";
+      return false;
+    }
+  }
+  return true;
+}
+
+GenKernel gen_colreduce(const KInfo& ki, int index) {
+  const Graph& g = ki.g;
+  std::string why;
+  if (!match_colreduce(ki, &why)) fail(KORCH_E_UNSUPPORTED, why);
+  GenKernel gk;
+  gk.family = KORCH_FAM_COLREDUCE;
+  gk.name = kernel_name(index, "colreduce");
+  std::map<int, int> slot;
+  ki.assign_args(gk, slot);
+  int r = ki.reduces[0];
+  const Node& rn = g.nodes[r];
+  int X = rn.in[0];
+  const Shape& S = g.nodes[X].shape;
+  int ax = rn.axis;
+  int64_t A = 1, B = 1, Lr = S[ax];
+  for (int d = 0; d < ax; ++d) A *= S[d];
+  for (size_t d = ax + 1; d < S.size(); ++d) B *= S[d];
+  int BB = B >= 64 ? 64 : (int)pow2ceil(B);
+  int LY = 256 / BB;
+  bool isMax = rn.op == KORCH_REDUCE_MAX;
+  std::string ident = isMax ? "-__builtin_huge_valf()" : "0.0f";
+  auto comb = [&](const std::string& x, const std::string& y) {
+    return isMax ? "k_max(" + x + ", " + y + ")" : "(" + x + " + " + y + ")";
+  };
+  std::vector<Ix> xi(S.size());
+  for (int d = 0; d < ax; ++d) xi[d] = Ix::var("a" + std::to_string(d));
+  xi[ax] = Ix::var("l");
+  for (size_t d = ax + 1; d < S.size(); ++d) xi[d] = Ix::var("b" + std::to_string(d));
+  Emitter pe(g);
+  pe.inset = ki.in;
+  pe.argslot = slot;
+  pe.vec = 1;
+  std::string xv = pe.value(X, xi);
+  // epilogue
+  std::vector<Ix> ri;
+  for (int d = 0; d < ax; ++d) ri.push_back(xi[d]);
+  if ((int)rn.shape.size() == (int)S.size()) ri.push_back(Ix::k(0));
+  for (size_t d = ax + 1; d < S.size(); ++d) ri.push_back(xi[d]);
+  Emitter ee(g);
+  ee.inset = ki.in;
+  ee.argslot = slot;
+  ee.vec = 1;
+  std::string rkey = Emitter::key(r, ri);
+  ee.provide = [&](int node, const std::vector<Ix>& idx, std::string* out) {
+    if (node != r) return false;
+    if (Emitter::key(node, idx) != rkey) fail(KORCH_E_UNSUPPORTED, "colreduce: reduction read at another index");
+    *out = "s";
+    return true;
+  };
+  std::ostringstream st;
+  for (int o : ki.k.outs) {
+    const Node& on = g.nodes[o];
+    auto bi = broadcast_index(on.shape, rn.shape, ri);
+    std::string v = ee.value(o, bi);
+    auto strd = strides_of(on.shape);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], strd[d], 1));
+    st << "      st1((" << ctype(on.dtype) << "*)a.p[" << ki.out_slot(o) << "] + " << off.at() << ", " << v << ");\n";
+  }
+  std::ostringstream s;
+  s << source_header((int)gk.args.size());
+  s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
+  s << "  __shared__ float red[256];\n";
+  s << "  const int bl = threadIdx.x % " << BB << ", ly = threadIdx.x / " << BB << ";\n";
+  s << "  const i64 bi0 = (i64)blockIdx.x * " << BB << " + bl;\n";
+  s << "  const bool bv = bi0 < " << B << "LL;\n";
+  s << "  const i64 bi = bv ? bi0 : " << B - 1 << "LL;\n";
+  s << "  i64 q_ = blockIdx.y;\n";
+  for (int d = ax - 1; d >= 0; --d) s << "  const i64 a" << d << " = q_ % " << S[d] << "LL; q_ /= " << S[d] << "LL;\n";
+  s << "  q_ = bi;\n";
+  for (int d = (int)S.size() - 1; d > ax; --d)
+    s << "  const i64 b" << d << " = q_ % " << S[d] << "LL; q_ /= " << S[d] << "LL;\n";
+  s << "  float acc = " << ident << ";\n";
+  s << "  for (i64 l = ly; l < " << Lr << "LL; l += " << LY << ") {\n  const int e = 0; (void)e;\n"
+    << pe.pre.str() << pe.body.str() << "    acc = " << comb("acc", xv) << ";\n  }\n";
+  s << "  red[threadIdx.x] = acc;\n  __syncthreads();\n";
+  s << "  if (ly == 0) {\n    float s = red[bl];\n";
+  s << "    for (int y = 1; y < " << LY << "; ++y) s = " << comb("s", "red[y * " + std::to_string(BB) + " + bl]")
+    << ";\n";
+  if (rn.op == KORCH_REDUCE_MEAN) s << "    s = s / " << flit((double)Lr) << ";\n";
+  s << "    if (bv) {\n      const i64 l = 0; (void)l; const int e = 0; (void)e;\n"
+    << ee.pre.str() << ee.body.str() << st.str() << "    }\n  }\n}\n";
+  gk.source = s.str();
+  gk.grid[0] = (int)((B + BB - 1) / BB);
+  gk.grid[1] = (int)A;
+  ki.fill_cost(gk);
+  return gk;
+}
+
+// ---------------------------------------------------------------------------
+// Dispatcher
+// ---------------------------------------------------------------------------
+
+int match_family(const Graph& g, const KernelDesc& k, std::string* why) {
+  std::string w;
+  if (!why) why = &w;
+  try {
+    KInfo ki(g, k);
+    if (!ki.linear.empty()) {
+      if (match_attention(ki, why)) return KORCH_FAM_ATTENTION;
+      if (match_conv(ki, why)) return KORCH_FAM_CONV;
+      if (match_splitk(ki, why)) return KORCH_FAM_SPLITK;
+      if (match_gemm(ki, why)) return KORCH_FAM_GEMM;
+      return KORCH_FAM_NONE;
+    }
+    if (!ki.reduces.empty()) {
+      if (match_row(ki, why)) return KORCH_FAM_ROW;
+      if (match_colreduce(ki, why)) return KORCH_FAM_COLREDUCE;
+      return KORCH_FAM_NONE;
+    }
+    if (match_pointwise(ki, why)) return KORCH_FAM_POINTWISE;
+  } catch (Error& e) {
+    *why = e.what();
+  }
+  return KORCH_FAM_NONE;
+}
+
+GenKernel generate_kernel(const Graph& g, const KernelDesc& k, int index) {
+  std::string why;
+  int fam = match_family(g, k, &why);
+  KInfo ki(g, k);
+  switch (fam) {
+    case KORCH_FAM_POINTWISE: return gen_pointwise(ki, index);
+    case KORCH_FAM_ROW: return gen_row(ki, index);
+    case KORCH_FAM_COLREDUCE: return gen_colreduce(ki, index);
+    case KORCH_FAM_GEMM: return gen_gemm(ki, index);
+    case KORCH_FAM_CONV: return gen_gemm(ki, index);
+    case KORCH_FAM_SPLITK: return gen_splitk(ki, index);
+    case KORCH_FAM_ATTENTION: return gen_attention(ki, index);
+  }
+  fail(KORCH_E_UNSUPPORTED, "kernel " + std::to_string(index) + ": no family implements it (" + why + ")");
+}
+
+}  // namespace korch

@@ -1,0 +1,44 @@
+// Shared pieces of the MFMA product families (GEMM, conv, split-K).
+#pragma once
+
+#include <map>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "families.h"
+
+namespace korch {
+
+struct GemmSpec {
+  bool conv = false;
+  std::vector<int> mms;     // products (primary first)
+  int A = -1;               // left operand node (conv: input X)
+  std::vector<int> Bs;      // right operand per product (conv: weights W)
+  std::set<int> pro, epi;   // prologue / epilogue primitives
+  std::vector<int> rowred;  // reductions over the product's last axis (epilogue)
+  std::vector<int> side;    // reductions that read the left operand's prologue
+  Shape OUT;                // iteration space of the epilogue
+  int nb = 0;               // leading batch dims of OUT
+  int nmdims = 1;           // dims of OUT that form the M index
+  int64_t M = 0, N = 0, K = 0, batch = 1;
+  std::vector<int64_t> Nj, offj;
+  int64_t Ntot = 0;
+  int mtype = KORCH_F16;
+  // convolution geometry
+  int64_t H = 0, W = 0, Cin = 0, KH = 0, KW = 0, stride = 1, pad = 0, Ho = 0, Wo = 0;
+  // tiling
+  int BM = 128, BN = 128, BK = 32, BKP = 40, kstep = 32, WM = 2, WN = 2, WTM = 64, WTN = 64, FM = 4, FN = 4;
+  int VA = 8, VB = 8, LDC = 132;
+};
+
+bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_reduce);
+void choose_tiles(GemmSpec& sp, bool split);
+std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot);
+std::string mfma_mainloop(const GemmSpec& sp);
+std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
+                          const std::string& cs_row);
+std::string gemm_prologue_common(const GemmSpec& sp);
+size_t gemm_smem_bytes(const GemmSpec& sp);
+
+}  // namespace korch

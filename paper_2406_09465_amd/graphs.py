@@ -1,0 +1,234 @@
+"""Primitive graphs of the five workloads, built through the C ABI, with their plans.
+
+Operator fission is applied by hand (Korch, Section 3): softmax becomes a row
+max, a subtraction, an exponential, a row sum and a division; LayerNorm
+becomes mean, subtraction, square, mean, add-eps, reciprocal square root,
+scaling and the affine pair; Mish becomes exp, add 1, log, tanh and a product.
+Broadcast is implicit in binary primitives (ONNX style, Section 5.1).
+
+Each builder returns a ``Workload`` with the graph handle, a name -> node map,
+and named plans:
+  * "fused":   the recommended orchestration (fewest kernels, redundant
+               recomputation where it saves traffic: Section 4.2);
+  * "layered": a plan that keeps each dense product in its own kernel;
+  * "unfused": one kernel per primitive (korch_plan_unfused).
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+from ._abi import Graph, Plan
+
+
+@dataclass
+class Workload:
+    name: str
+    dtype: str
+    graph: Graph
+    ids: dict
+    input_names: list
+    output_names: list
+    plans: dict = field(default_factory=dict)  # name -> list of (prim names, out names)
+    sizes: dict = field(default_factory=dict)
+
+    def node(self, name):
+        return self.ids[name]
+
+    def kernels(self, plan_name):
+        ks = []
+        for prims, outs in self.plans[plan_name]:
+            ks.append(([self.ids[p] for p in prims], [self.ids[o] for o in outs]))
+        return ks
+
+    def plan(self, plan_name):
+        if plan_name == "unfused":
+            return Plan(self.graph)
+        return Plan(self.graph, self.kernels(plan_name))
+
+
+class _B:
+    """Small helper that names nodes as they are created."""
+
+    def __init__(self, dtype):
+        self.g = Graph()
+        self.dtype = dtype
+        self.ids = {}
+        self.inputs = []
+
+    def inp(self, name, shape):
+        self.ids[name] = self.g.input(self.dtype, shape)
+        self.inputs.append(name)
+        return self.ids[name]
+
+    def op(self, name, op, ins, **attrs):
+        self.ids[name] = self.g.op(op, [self.ids[i] for i in ins], self.dtype, **attrs)
+        return self.ids[name]
+
+
+def _softmax(b, s):
+    b.op("m", "reduce_max", [s], axis=-1, keepdim=True)
+    b.op("Z", "sub", [s, "m"])
+    b.op("E", "exp", ["Z"])
+    b.op("s", "reduce_sum", ["E"], axis=-1, keepdim=True)
+    b.op("P", "div", ["E", "s"])
+
+
+def _layernorm(b, x, eps, p=""):
+    b.op(p + "mu", "reduce_mean", [x], axis=-1, keepdim=True)
+    b.op(p + "D", "sub", [x, p + "mu"])
+    b.op(p + "D2", "square", [p + "D"])
+    b.op(p + "var", "reduce_mean", [p + "D2"], axis=-1, keepdim=True)
+    b.op(p + "ve", "add", [p + "var"], scalar=eps)
+    b.op(p + "r", "rsqrt", [p + "ve"])
+    b.op(p + "Xh", "mul", [p + "D", p + "r"])
+    b.op(p + "Yg", "mul", [p + "Xh", "gamma"])
+    b.op(p + "Y", "add", [p + "Yg", "beta"])
+    return p + "Y"
+
+
+def attention(n=128, d=64, nk=None, dtype="f32"):
+    nk = n if nk is None else nk
+    b = _B(dtype)
+    b.inp("Q", (n, d))
+    b.inp("K", (nk, d))
+    b.inp("V", (nk, d))
+    b.op("KT", "transpose", ["K"], perm=(1, 0))
+    b.op("S0", "matmul", ["Q", "KT"])
+    b.op("S", "mul", ["S0"], scalar=1.0 / math.sqrt(d))
+    _softmax(b, "S")
+    b.op("O", "matmul", ["P", "V"])
+    b.g.output(b.ids["O"])
+    b.g.finalize()
+    w = Workload("attention", dtype, b.g, b.ids, b.inputs, ["O"], sizes=dict(n=n, d=d, nk=nk))
+    w.plans["fused"] = [(["KT", "S0", "S", "m", "Z", "E", "s", "P", "O"], ["O"])]
+    w.plans["layered"] = [(["KT", "S0", "S"], ["S"]), (["m", "Z", "E", "s", "P"], ["P"]), (["O"], ["O"])]
+    return w
+
+
+def mlp(m=4096, d=768, h=3072, dtype="f16", eps=1e-5):
+    b = _B(dtype)
+    b.inp("X", (m, d))
+    b.inp("W1", (d, h))
+    b.inp("W2", (h, d))
+    b.inp("gamma", (d,))
+    b.inp("beta", (d,))
+    _layernorm(b, "X", eps)
+    b.op("H0", "matmul", ["Y", "W1"])
+    b.op("Hg", "gelu_tanh", ["H0"])
+    b.op("Zo", "matmul", ["Hg", "W2"])
+    b.op("out", "add", ["Zo", "X"])
+    b.g.output(b.ids["out"])
+    b.g.finalize()
+    w = Workload("mlp", dtype, b.g, b.ids, b.inputs, ["out"], sizes=dict(m=m, d=d, h=h))
+    # The statistics kernel materializes the centred rows D and the row scale
+    # r (two outputs); normalization and affine run in the first product's
+    # operand prologue, GELU in its epilogue, the residual in the second
+    # product's epilogue.  (mu cannot be an output of a kernel that also holds
+    # its only consumer D: Definition 3.)
+    w.plans["fused"] = [
+        (["mu", "D", "D2", "var", "ve", "r"], ["D", "r"]),
+        (["Xh", "Yg", "Y", "H0", "Hg"], ["Hg"]),
+        (["Zo", "out"], ["out"]),
+    ]
+    w.plans["layered"] = [
+        (["mu", "D", "D2", "var", "ve", "r", "Xh", "Yg", "Y"], ["Y"]),
+        (["H0", "Hg"], ["Hg"]),
+        (["Zo", "out"], ["out"]),
+    ]
+    return w
+
+
+def sra(hh=128, ww=128, c=64, r=8, dtype="f16", eps=1e-5):
+    b = _B(dtype)
+    b.inp("X", (hh, ww, c))
+    b.inp("Wsr", (r * r * c, c))
+    b.inp("gamma", (c,))
+    b.inp("beta", (c,))
+    b.op("Xr", "reshape", ["X"], shape=(hh // r, r, ww // r, r, c))
+    b.op("Xt", "transpose", ["Xr"], perm=(0, 2, 1, 3, 4))
+    b.op("A", "reshape", ["Xt"], shape=((hh // r) * (ww // r), r * r * c))
+    b.op("KVp", "matmul", ["A", "Wsr"])
+    kv = _layernorm(b, "KVp", eps, p="ln_")
+    b.op("Qv", "reshape", ["X"], shape=(hh * ww, c))
+    b.op("KT", "transpose", [kv], perm=(1, 0))
+    b.op("S0", "matmul", ["Qv", "KT"])
+    b.op("S", "mul", ["S0"], scalar=1.0 / math.sqrt(c))
+    _softmax(b, "S")
+    b.op("O", "matmul", ["P", kv])
+    b.g.output(b.ids["O"])
+    b.g.finalize()
+    w = Workload("sra", dtype, b.g, b.ids, b.inputs, ["O"], sizes=dict(hh=hh, ww=ww, c=c, r=r))
+    ln = ["ln_mu", "ln_D", "ln_D2", "ln_var", "ln_ve", "ln_r", "ln_Xh", "ln_Yg", "ln_Y"]
+    w.plans["fused"] = [
+        (["Xt", "A", "KVp"] + ln, ["ln_Y"]),
+        (["KT", "S0", "S", "m", "Z", "E", "s", "P", "O"], ["O"]),
+    ]
+    w.plans["layered"] = [
+        (["Xt", "A", "KVp"], ["KVp"]),
+        (ln, ["ln_Y"]),
+        (["KT", "S0", "S"], ["S"]),
+        (["m", "Z", "E", "s", "P"], ["P"]),
+        (["O"], ["O"]),
+    ]
+    return w
+
+
+def conv(hh=416, ww=416, cin=32, cout=64, k=3, dtype="f16"):
+    b = _B(dtype)
+    b.inp("X", (hh, ww, cin))
+    b.inp("W", (k, k, cin, cout))
+    b.inp("scale", (cout,))
+    b.inp("shift", (cout,))
+    b.op("C", "conv2d", ["X", "W"], stride=1, pad=k // 2)
+    b.op("B1", "mul", ["C", "scale"])
+    b.op("B", "add", ["B1", "shift"])
+    b.op("E", "exp", ["B"])
+    b.op("E1", "add", ["E"], scalar=1.0)
+    b.op("SP", "log", ["E1"])
+    b.op("T", "tanh", ["SP"])
+    b.op("Y", "mul", ["B", "T"])
+    b.g.output(b.ids["Y"])
+    b.g.finalize()
+    w = Workload("conv", dtype, b.g, b.ids, b.inputs, ["Y"], sizes=dict(hh=hh, ww=ww, cin=cin, cout=cout, k=k))
+    w.plans["fused"] = [(["C", "B1", "B", "E", "E1", "SP", "T", "Y"], ["Y"])]
+    w.plans["layered"] = [(["C", "B1", "B"], ["B"]), (["E", "E1", "SP", "T", "Y"], ["Y"])]
+    return w
+
+
+def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6):
+    b = _B(dtype)
+    b.inp("Q", (heads, n, d))
+    b.inp("K", (heads, n, d))
+    b.inp("V", (heads, n, d))
+    b.op("Qr", "relu", ["Q"])
+    b.op("Kr", "relu", ["K"])
+    b.op("KrT", "transpose", ["Kr"], perm=(0, 2, 1))
+    b.op("KVm", "matmul", ["KrT", "V"])
+    b.op("sK", "reduce_sum", ["Kr"], axis=1, keepdim=True)
+    b.op("num", "matmul", ["Qr", "KVm"])
+    b.op("sKT", "transpose", ["sK"], perm=(0, 2, 1))
+    b.op("den0", "matmul", ["Qr", "sKT"])
+    b.op("den", "add", ["den0"], scalar=eps)
+    b.op("out", "div", ["num", "den"])
+    b.g.output(b.ids["out"])
+    b.g.finalize()
+    w = Workload("linattn", dtype, b.g, b.ids, b.inputs, ["out"], sizes=dict(heads=heads, n=n, d=d))
+    w.plans["fused"] = [
+        (["Kr", "KrT", "KVm", "sK"], ["KVm", "sK"]),
+        (["Qr", "num", "sKT", "den0", "den", "out"], ["out"]),
+    ]
+    w.plans["layered"] = [
+        (["Kr", "KrT", "KVm"], ["KVm"]),
+        (["Kr", "sK"], ["sK"]),
+        (["Qr", "num", "sKT", "den0", "den", "out"], ["out"]),
+    ]
+    return w
+
+
+BUILDERS = {"attention": attention, "mlp": mlp, "sra": sra, "conv": conv, "linattn": linattn}
+
+
+def build(workload: str, **sizes) -> Workload:
+    return BUILDERS[workload](**sizes)

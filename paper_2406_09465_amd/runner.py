@@ -1,0 +1,64 @@
+"""Executes a compiled plan on torch device tensors (memory and streams only).
+
+torch allocates device memory and supplies the stream; every primitive runs in
+the library's generated gfx950 kernels.  There is no CPU fallback: running a
+plan needs a GPU and the in-tree libkorch.so.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from ._abi import Plan
+
+TORCH_DTYPE = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+
+def to_device(arr: np.ndarray, dtype: str, device="cuda") -> torch.Tensor:
+    """Storage array (float32 / float16 / uint16 bf16 bits) -> device tensor of the same bytes."""
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(arr))
+    return t.to(device)
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+class PlanRunner:
+    """A compiled plan plus device buffers for one workload instance."""
+
+    def __init__(self, workload, plan="fused", kernels=None, device="cuda"):
+        if not torch.cuda.is_available():
+            raise RuntimeError("PlanRunner needs a GPU")
+        self.w = workload
+        self.device = device
+        self.plan = Plan(workload.graph, kernels) if kernels is not None else workload.plan(plan)
+        self.plan.compile()
+        self.ws_bytes = self.plan.workspace_bytes()
+        self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=device)
+        g = workload.graph
+        self.outs = []
+        for o in g.outputs():
+            _, dt, shape = g.node_info(o)
+            self.outs.append(torch.empty(shape, dtype=TORCH_DTYPE[dt], device=device))
+        self.ins = []
+
+    def set_inputs(self, storage: dict):
+        """storage: {input name: storage array} (synthetic.make_inputs output)."""
+        self.ins = [to_device(storage[n], self.w.dtype, self.device) for n in self.w.input_names]
+
+    def launch(self, stream=None):
+        s = stream if stream is not None else torch.cuda.current_stream()
+        self.plan.execute([t.data_ptr() for t in self.ins], [t.data_ptr() for t in self.outs],
+                          self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
+
+    def run(self, storage: dict = None):
+        if storage is not None:
+            self.set_inputs(storage)
+        self.launch()
+        torch.cuda.synchronize()
+        return {n: to_f64(t) for n, t in zip(self.w.output_names, self.outs)}
