@@ -1,0 +1,214 @@
+"""Fused-subgraph latency of one workload's orchestration plan on one MI355X.
+
+One step = one execution of the whole plan (every kernel of the fused
+orchestration) on inputs already resident in HBM.  Prints ONE JSON line:
+metric / value (microseconds per step) plus a roofline object for the plan's
+dominant kernel (algorithmic flops or bytes per launch over its average
+launch time, measured with HIP events around that kernel inside the timed
+loop) and the float64 oracle timed on the host cores on a bounded sample.
+
+Default workload: transformer MLP block, fp16, X [4096, 768], W1 [768, 3072],
+W2 [3072, 768] (the configuration the headline metric is quoted on).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fused-subgraph latency (µs) & achieved HBM GB/s or MFMA util vs peak, 1×MI355X"
+PEAK = {  # MI355X published peaks
+    "hbm_GBs": 8000.0,
+    "mfma_f16_TFLOPs": 2500.0,
+    "mfma_bf16_TFLOPs": 2500.0,
+    "f32_TFLOPs": 157.3,
+}
+DESCR = {
+    "attention": "single-head attention fp32, Q,K,V [128,64]",
+    "mlp": "transformer MLP block fp16: LayerNorm, X[4096,768] x W1[768,3072], tanh-GELU, x W2[3072,768], residual",
+    "sra": "spatial-reduction attention fp16: 128x128x64 map, 8x8 patch merge 4096->64, LayerNorm, 16384x256 softmax",
+    "conv": "conv3x3 NHWC fp16 416x416x32->64 + BatchNorm scale/shift + Mish",
+    "linattn": "ReLU linear attention bf16, 16 heads x 4096 tokens x d16",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="mlp", choices=list(DESCR))
+    ap.add_argument("--plan", default="fused")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work for the oracle sample")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before timing, run a plain device copy of this many MiB 3 times (PMC byte calibration)")
+    return ap.parse_args()
+
+
+def cpu_baseline(workload, seconds):
+    """The float64 oracle (unfused, one primitive at a time) on the host cores."""
+    import numpy as np
+    from oracle import configs as OC
+    from oracle.graph import run_unfused
+    from synthetic import storage_to_f64
+    from synthetic import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    dt = W.DEFAULT_DTYPE[workload]
+    raw = W.inputs(workload)
+    x64 = {k: storage_to_f64(v, dt) for k, v in raw.items()}
+    g = OC.build(workload)
+    times = []
+    t_end = time.perf_counter() + seconds
+    while True:
+        t0 = time.perf_counter()
+        run_unfused(g, x64)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() >= t_end or len(times) >= 50:
+            break
+    med = statistics.median(times)
+    return {"value": med * 1e6, "unit": "us", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(times)} full runs of the unfused float64 oracle on the whole workload "
+                      f"({sum(times):.1f} s of CPU work); value = median microseconds per run"}
+
+
+def traffic_from_profiles(kernel_name, source_hash):
+    """HBM bytes per launch of the dominant kernel from committed rocprofv3 PMC
+    summaries (FETCH_SIZE / WRITE_SIZE), or None if absent or stale."""
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        data = json.load(open(path))
+        rec = data["kernels"].get(kernel_name)
+        if not rec or rec.get("source_hash") != source_hash:
+            return None
+        return rec["hbm_bytes_per_launch"]
+    except Exception:
+        return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import hashlib
+
+    import torch
+
+    from paper_2406_09465_amd import graphs
+    from paper_2406_09465_amd.runner import PlanRunner
+    from synthetic import workloads as W
+
+    torch.cuda.set_device(0)
+    w = graphs.build(args.workload)
+    r = PlanRunner(w, args.plan)
+    r.set_inputs(W.inputs(args.workload))
+    nk = r.plan.num_kernels()
+    stream = torch.cuda.current_stream()
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # warmup, and per-kernel timing to pick the dominant kernel
+    for _ in range(args.warmup):
+        r.launch()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(nk)]
+    per = [[] for _ in range(nk)]
+    for _ in range(max(5, args.warmup)):
+        for k in range(nk):
+            ev[k][0].record(stream)
+            r.launch_kernels(k, 1)
+            ev[k][1].record(stream)
+        torch.cuda.synchronize()
+        for k in range(nk):
+            per[k].append(ev[k][0].elapsed_time(ev[k][1]) * 1e3)
+    dom = max(range(nk), key=lambda k: statistics.median(per[k]))
+
+    # timed region: exactly `steps` plan executions; the dominant kernel is
+    # bracketed by events on the launch stream
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        if dom > 0:
+            r.launch_kernels(0, dom)
+        starts[i].record(stream)
+        r.launch_kernels(dom, 1)
+        ends[i].record(stream)
+        if dom + 1 < nk:
+            r.launch_kernels(dom + 1, nk - dom - 1)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    dom_us = statistics.mean(s.elapsed_time(e) * 1e3 for s, e in zip(starts, ends))
+
+    fam, abytes, aflops = r.plan.kernel_info(dom)
+    name = r.plan.kernel_name(dom)
+    src_hash = hashlib.sha256(r.plan.kernel_source(dom).encode()).hexdigest()[:16]
+    if aflops > 0 and fam in ("gemm", "conv", "attention", "splitk") and aflops / max(abytes, 1) > 100:
+        peak = PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK[f"mfma_{w.dtype}_TFLOPs"]
+        achieved = aflops / (dom_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4)}
+    else:
+        achieved = abytes / (dom_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK["hbm_GBs"], "unit": "GB/s",
+                "frac": round(achieved / PEAK["hbm_GBs"], 4)}
+    roof["traffic"] = traffic_from_profiles(name, src_hash)
+    roof["kernel"] = name
+    roof["kernel_us"] = round(dom_us, 3)
+    roof["alg_bytes"] = abytes
+    roof["alg_flops"] = aflops
+
+    kernels = []
+    for k in range(nk):
+        f, b, fl = r.plan.kernel_info(k)
+        kernels.append({"name": r.plan.kernel_name(k), "family": f, "us": round(statistics.median(per[k]), 3),
+                        "alg_bytes": b, "alg_flops": fl})
+
+    out = {
+        "metric": METRIC,
+        "value": round(ms_per_step * 1e3, 3),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": DESCR[args.workload], "plan": args.plan, "kernels": nk},
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

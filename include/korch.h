@@ -193,6 +193,11 @@ int korch_plan_workspace_bytes(const korch_plan* p, size_t* bytes);
    Never allocates; never synchronizes. */
 int korch_plan_execute(korch_plan* p, const void* const* inputs, void* const* outputs, void* workspace,
                        size_t workspace_bytes, void* stream);
+/* Same as korch_plan_execute but launches only kernels [first, first+count)
+   of the plan (for timing one kernel in place); the caller is responsible for
+   having run the earlier kernels whose outputs these read. */
+int korch_plan_execute_kernels(korch_plan* p, int32_t first, int32_t count, const void* const* inputs,
+                               void* const* outputs, void* workspace, size_t workspace_bytes, void* stream);
 /* Per-kernel family, algorithmic bytes (compulsory reads of its external
    tensors plus writes of its outputs) and flops (2*M*N*K per contraction). */
 int korch_plan_kernel_info(const korch_plan* p, int32_t k, int32_t* family, double* alg_bytes, double* alg_flops);

@@ -88,6 +88,7 @@ _SIGS = {
     "korch_plan_load": ([_P], C.c_int),
     "korch_plan_workspace_bytes": ([_P, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute": ([_P, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
+    "korch_plan_execute_kernels": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
     "korch_plan_kernel_info": ([_P, _I, C.POINTER(_I), C.POINTER(C.c_double), C.POINTER(C.c_double)], C.c_int),
     "korch_plan_kernel_source": ([_P, _I, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_kernel_name": ([_P, _I, C.c_char_p, C.c_size_t], C.c_int),
@@ -303,6 +304,12 @@ class Plan:
         outs = (C.c_void_p * max(1, len(outputs)))(*[C.c_void_p(int(p)) for p in outputs])
         check(lib.korch_plan_execute(self.h, ins, outs, C.c_void_p(int(workspace)), int(workspace_bytes),
                                      C.c_void_p(int(stream))))
+
+    def execute_kernels(self, first, count, inputs, outputs, workspace=0, workspace_bytes=0, stream=0):
+        ins = (C.c_void_p * max(1, len(inputs)))(*[C.c_void_p(int(p)) for p in inputs])
+        outs = (C.c_void_p * max(1, len(outputs)))(*[C.c_void_p(int(p)) for p in outputs])
+        check(lib.korch_plan_execute_kernels(self.h, int(first), int(count), ins, outs, C.c_void_p(int(workspace)),
+                                             int(workspace_bytes), C.c_void_p(int(stream))))
 
     def kernel_info(self, k):
         fam, b, f = _I(), C.c_double(), C.c_double()

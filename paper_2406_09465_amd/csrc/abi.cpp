@@ -24,7 +24,7 @@ void generate_plan(Plan& p);
 void load_plan(Plan& p);
 void destroy_plan_device(Plan& p);
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
-                  hipStream_t stream);
+                  hipStream_t stream, int first, int count);
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream);
 }  // namespace korch
@@ -367,7 +367,16 @@ int korch_plan_execute(korch_plan* p, const void* const* inputs, void* const* ou
                        size_t workspace_bytes, void* stream) {
   return guard([&] {
     NEED(p);
-    execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream);
+    execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, 0, -1);
+  });
+}
+
+int korch_plan_execute_kernels(korch_plan* p, int32_t first, int32_t count, const void* const* inputs,
+                               void* const* outputs, void* workspace, size_t workspace_bytes, void* stream) {
+  return guard([&] {
+    NEED(p);
+    if (count < 0) fail(KORCH_E_ARG, "negative kernel count");
+    execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, first, count);
   });
 }
 

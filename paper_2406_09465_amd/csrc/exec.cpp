@@ -106,7 +106,7 @@ void load_plan(Plan& p) {
 static bool aligned16(const void* q) { return ((uintptr_t)q & 15) == 0; }
 
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
-                  hipStream_t stream) {
+                  hipStream_t stream, int first, int count) {
   load_plan(p);
   const Graph& g = p.g;
   for (size_t i = 0; i < g.inputs.size(); ++i) {
@@ -122,7 +122,10 @@ void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void
       fail(KORCH_E_WORKSPACE, "workspace needs " + std::to_string(p.ws_bytes) + " bytes");
     if (!aligned16(ws)) fail(KORCH_E_ALIGN, "workspace is not 16-byte aligned");
   }
-  for (size_t k = 0; k < p.ck.size(); ++k) {
+  int nk = (int)p.ck.size();
+  if (first < 0 || first > nk) fail(KORCH_E_ARG, "first kernel index out of range");
+  int last = count < 0 ? nk : std::min(nk, first + count);
+  for (int k = first; k < last; ++k) {
     auto& ck = p.ck[k];
     std::vector<void*> ptr(ck.arg_storage.size());
     for (size_t a = 0; a < ck.arg_storage.size(); ++a) {
@@ -195,13 +198,13 @@ float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int re
     }
     void* ws = p.ws_bytes ? alloc(p.ws_bytes) : nullptr;
     void* fl = flush_bytes ? alloc(flush_bytes) : nullptr;
-    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream);
+    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1);
     ev = new hipEvent_t[2 * std::max(reps, 1)];
     for (int r = 0; r < 2 * reps; ++r) HIPCHECK(hipEventCreate(&ev[r]));
     for (int r = 0; r < reps; ++r) {
       if (fl) HIPCHECK(launch_flush(fl, flush_bytes, stream));
       HIPCHECK(hipEventRecord(ev[2 * r], stream));
-      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream);
+      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1);
       HIPCHECK(hipEventRecord(ev[2 * r + 1], stream));
     }
     HIPCHECK(hipStreamSynchronize(stream));

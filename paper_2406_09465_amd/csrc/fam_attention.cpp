@@ -1,13 +1,286 @@
-// Attention family (placeholder until implemented).
+// Attention family: S0 = Q K^T, an elementwise score chain (e.g. scaling),
+// row softmax (row max, subtract, exp, row sum, divide) and O = P V in one
+// kernel, with every key and value of a batch resident in LDS.
+//
+// Korch admits hand-written attention kernels as a backend for candidates it
+// identifies as attention subgraphs (Related Work, hand-optimized kernels);
+// this family accepts exactly the fissioned softmax of Section 1 between two
+// products.  Scores stay in MFMA accumulator registers; the row reductions are
+// butterflies over the 16 lanes that share a row.
+#include <algorithm>
+
 #include "families.h"
 
 namespace korch {
 
-bool match_attention(const KInfo&, std::string* why) {
-  *why = "attention: not available";
-  return false;
+struct AttnSpec {
+  int s0 = -1, sfinal = -1, m = -1, z = -1, e = -1, s = -1, p = -1, o = -1;
+  int kt = -1;               // in-kernel transpose producing K^T (or -1)
+  int q = -1, kx = -1, v = -1;  // external tensors
+  bool k_is_kt = false;      // kx holds K^T [d, nk] directly
+  std::vector<int> chain;    // elementwise score nodes S0 -> ... -> sfinal
+  int64_t nq = 0, d = 0, nk = 0, dv = 0, batch = 1;
+  int nb = 0;
+  Shape bshape;
+  int dtype = KORCH_F16;
+};
+
+static bool single_in_kernel_input(const KInfo& ki, int v, int* which) {
+  const Node& n = ki.g.nodes[v];
+  int cnt = 0;
+  for (int u : n.in)
+    if (ki.in.count(u)) {
+      ++cnt;
+      *which = u;
+    }
+  return cnt == 1;
 }
 
-GenKernel gen_attention(const KInfo&, int) { fail(KORCH_E_UNSUPPORTED, "attention: not available"); }
+static bool analyze_attention(const KInfo& ki, AttnSpec& a, std::string* why) {
+  const Graph& g = ki.g;
+  auto bad = [&](const char* m) {
+    *why = std::string("attention: ") + m;
+    return false;
+  };
+  if (ki.linear.size() != 2) return bad("needs exactly two products");
+  for (int v : ki.linear)
+    if (g.nodes[v].op != KORCH_MATMUL) return bad("products must be matmuls");
+  a.s0 = ki.linear[0];
+  a.o = ki.linear[1];
+  if (ki.k.outs.size() != 1 || ki.k.outs[0] != a.o) return bad("the only output must be the second product");
+  const Node& o = g.nodes[a.o];
+  a.p = o.in[0];
+  a.v = o.in[1];
+  if (!ki.in.count(a.p) || ki.in.count(a.v)) return bad("second product must read P inside and V outside");
+  const Node& pn = g.nodes[a.p];
+  if (pn.op != KORCH_DIV || pn.attrs.has_scalar) return bad("P must be E / s");
+  a.e = pn.in[0];
+  a.s = pn.in[1];
+  const Node& sn = g.nodes[a.s];
+  if (sn.op != KORCH_REDUCE_SUM || sn.in[0] != a.e || !sn.attrs.keepdim) return bad("s must be a keepdim row sum of E");
+  const Node& en = g.nodes[a.e];
+  if (en.op != KORCH_EXP) return bad("E must be exp(Z)");
+  a.z = en.in[0];
+  const Node& zn = g.nodes[a.z];
+  if (zn.op != KORCH_SUB || zn.attrs.has_scalar) return bad("Z must be S - m");
+  a.sfinal = zn.in[0];
+  a.m = zn.in[1];
+  const Node& mn = g.nodes[a.m];
+  if (mn.op != KORCH_REDUCE_MAX || mn.in[0] != a.sfinal || !mn.attrs.keepdim) return bad("m must be a keepdim row max of S");
+  // reductions over the last axis
+  int r = (int)g.nodes[a.sfinal].shape.size();
+  if (sn.axis != r - 1 || mn.axis != r - 1) return bad("softmax must run over the last axis");
+  // chain S0 -> ... -> sfinal
+  std::vector<int> chain;
+  int cur = a.sfinal;
+  while (cur != a.s0) {
+    if (!ki.in.count(cur)) return bad("score chain leaves the kernel");
+    const Node& cn = g.nodes[cur];
+    Kind kd = op_kind(cn.op);
+    if (kd == Kind::Unary) {
+      chain.push_back(cur);
+      cur = cn.in[0];
+    } else if (kd == Kind::Binary && cn.attrs.has_scalar) {
+      chain.push_back(cur);
+      cur = cn.in[0];
+    } else {
+      return bad("score chain must be unary or scalar elementwise primitives");
+    }
+  }
+  std::reverse(chain.begin(), chain.end());
+  a.chain = chain;
+  const Node& s0 = g.nodes[a.s0];
+  a.q = s0.in[0];
+  int kop = s0.in[1];
+  if (ki.in.count(a.q)) return bad("Q must be a materialized tensor");
+  if (ki.in.count(kop)) {
+    const Node& kn = g.nodes[kop];
+    int rk = (int)kn.shape.size();
+    if (kn.op != KORCH_TRANSPOSE || ki.in.count(kn.in[0])) return bad("K^T must be a transpose of a materialized tensor");
+    for (int i = 0; i < rk - 2; ++i)
+      if (kn.attrs.perm[i] != i) return bad("K^T transpose must swap only the last two dims");
+    if (kn.attrs.perm[rk - 2] != rk - 1 || kn.attrs.perm[rk - 1] != rk - 2) return bad("K^T must swap the last two dims");
+    a.kt = kop;
+    a.kx = kn.in[0];
+    a.k_is_kt = false;
+  } else {
+    a.kx = kop;
+    a.k_is_kt = true;
+  }
+  // every kernel node accounted for
+  std::set<int> known = {a.s0, a.m, a.z, a.e, a.s, a.p, a.o};
+  if (a.kt >= 0) known.insert(a.kt);
+  for (int c : chain) known.insert(c);
+  if (known.size() != ki.in.size()) return bad("kernel holds primitives outside the attention pattern");
+  for (int v : ki.in)
+    if (!known.count(v)) return bad("kernel holds primitives outside the attention pattern");
+  // shapes
+  const Shape& qs = g.nodes[a.q].shape;
+  const Shape& vs = g.nodes[a.v].shape;
+  const Shape& os = o.shape;
+  a.nb = (int)os.size() - 2;
+  a.nq = qs[qs.size() - 2];
+  a.d = qs.back();
+  a.nk = vs[vs.size() - 2];
+  a.dv = vs.back();
+  a.bshape = Shape(os.begin(), os.end() - 2);
+  a.batch = numel(a.bshape);
+  for (int t : {a.q, a.kx, a.v})
+    if ((int)g.nodes[t].shape.size() != a.nb + 2 ||
+        !std::equal(a.bshape.begin(), a.bshape.end(), g.nodes[t].shape.begin()))
+      return bad("batch dims must match exactly");
+  a.dtype = g.nodes[a.q].dtype;
+  if (g.nodes[a.kx].dtype != a.dtype || g.nodes[a.v].dtype != a.dtype) return bad("operand dtypes differ");
+  if (a.nk > 256) return bad("more than 256 keys");
+  if (a.dv > 128) return bad("value width above 128");
+  if (a.d > 128) return bad("head dim above 128");
+  if (a.dtype != KORCH_F32 && a.d % 8) return bad("half-precision needs d % 8 == 0");
+  if (a.dtype == KORCH_F32 && a.d % 4) return bad("fp32 needs d % 4 == 0");
+  return true;
+}
+
+bool match_attention(const KInfo& ki, std::string* why) {
+  AttnSpec a;
+  return analyze_attention(ki, a, why);
+}
+
+GenKernel gen_attention(const KInfo& ki, int index) {
+  AttnSpec a;
+  std::string why;
+  if (!analyze_attention(ki, a, &why)) fail(KORCH_E_UNSUPPORTED, why);
+  const Graph& g = ki.g;
+  GenKernel gk;
+  gk.family = KORCH_FAM_ATTENTION;
+  gk.name = kernel_name(index, "attention");
+  std::map<int, int> slot;
+  ki.assign_args(gk, slot);
+  bool f32 = a.dtype == KORCH_F32;
+  std::string T = ctype(a.dtype);
+  int kstep = f32 ? 4 : 32;
+  int64_t dpad = (a.d + kstep - 1) / kstep * kstep;  // contraction of Q K^T padded with zeros
+  int64_t nkp = f32 ? (a.nk + 15) / 16 * 16 : (a.nk + 31) / 32 * 32;  // keys padded: zero K/V, -inf scores
+  int KSP = (int)dpad + (f32 ? 4 : 8);                // Ks row pitch (elements)
+  int NKP = (int)nkp + (f32 ? 4 : 8);                 // Ps / Vt row pitch
+  int64_t dvp = (a.dv + 15) / 16 * 16;                // value width padded with zero columns
+  int VP = (int)dvp + 4;                              // fp32 V row pitch
+  int NF = (int)(nkp / 16), OF = (int)(dvp / 16);
+  size_t ks_bytes = (size_t)nkp * KSP * dtype_bytes(a.dtype);
+  size_t v_bytes = f32 ? (size_t)nkp * VP * 4 : (size_t)dvp * NKP * 2;
+  size_t p_bytes = (size_t)4 * 16 * NKP * dtype_bytes(a.dtype);
+  size_t smem = ks_bytes + v_bytes + p_bytes;
+  std::string Q = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.q)) + "])";
+  std::string K = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.kx)) + "])";
+  std::string V = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.v)) + "])";
+  std::string O = "((" + ctype(g.nodes[a.o].dtype) + "*)a.p[" + std::to_string(ki.out_slot(a.o)) + "])";
+  std::ostringstream s;
+  s << source_header((int)gk.args.size());
+  s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
+  s << "  __shared__ __attribute__((aligned(16))) char smem[" << smem << "];\n";
+  s << "  " << T << "* Ks = (" << T << "*)smem;\n";
+  s << "  " << T << "* Vs = (" << T << "*)(smem + " << ks_bytes << ");\n";
+  s << "  " << T << "* Ps = (" << T << "*)(smem + " << ks_bytes + v_bytes << ");\n";
+  s << "  const int tid = threadIdx.x, l = tid & 63, wave = tid >> 6;\n";
+  s << "  const i64 bz = blockIdx.y;\n";
+  s << "  const i64 qoff = bz * " << a.nq * a.d << "LL, koff = bz * " << a.nk * a.d << "LL, voff = bz * "
+    << a.nk * a.dv << "LL, ooff = bz * " << a.nq * a.dv << "LL;\n";
+  // K into LDS as [key][dim] (zero-padded dims)
+  s << "  for (int i = tid; i < " << nkp * dpad << "; i += 256) {\n";
+  s << "    const int key = i / " << dpad << ", dim = i % " << dpad << ";\n";
+  if (a.k_is_kt)
+    s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K << "[koff + (i64)dim * " << a.nk
+      << " + key] : fromf<" << T << ">(0.0f);\n";
+  else
+    s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K << "[koff + (i64)key * " << a.d
+      << " + dim] : fromf<" << T << ">(0.0f);\n";
+  s << "  }\n";
+  // V into LDS: fp32 natural [key][dim]; half precision transposed [dim][key]
+  s << "  for (int i = tid; i < " << nkp * dvp << "; i += 256) {\n";
+  s << "    const int key = i / " << dvp << ", dim = i % " << dvp << ";\n";
+  s << "    const " << T << " x_ = (key < " << a.nk << " && dim < " << a.dv << ") ? " << V << "[voff + (i64)key * "
+    << a.dv << " + dim] : fromf<" << T << ">(0.0f);\n";
+  if (f32)
+    s << "    Vs[key * " << VP << " + dim] = x_;\n";
+  else
+    s << "    Vs[dim * " << NKP << " + key] = x_;\n";
+  s << "  }\n  __syncthreads();\n";
+  // this wave's 16 query rows
+  s << "  const i64 q0 = (i64)blockIdx.x * 64 + wave * 16;\n";
+  s << "  const i64 qr = q0 + (l & 15);\n";
+  s << "  const bool qv = qr < " << a.nq << "LL;\n";
+  s << "  f32x4 sc[" << NF << "];\n";
+  s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f) sc[f] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
+  if (f32) {
+    s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 4 << "; ++kk) {\n";
+    s << "    const int dim = kk * 4 + (l >> 4);\n";
+    s << "    const float qa = (qv && dim < " << a.d << ") ? " << Q << "[qoff + qr * " << a.d << " + dim] : 0.0f;\n";
+    s << "#pragma unroll\n    for (int f = 0; f < " << NF << "; ++f) sc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, Ks[(f * 16 + (l & 15)) * "
+      << KSP << " + dim], sc[f], 0, 0, 0);\n  }\n";
+  } else {
+    std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
+    std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
+    s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 32 << "; ++kk) {\n";
+    s << "    const int dim = kk * 32 + (l >> 4) * 8;\n";
+    s << "    " << V8 << " qa;\n";
+    s << "    if (qv && dim + 8 <= " << a.d << ") qa = *(const " << V8 << "*)(" << Q << " + qoff + qr * " << a.d << " + dim);\n";
+    s << "    else {\n#pragma unroll\n      for (int j = 0; j < 8; ++j) qa[j] = (qv && dim + j < " << a.d << ") ? " << Q
+      << "[qoff + qr * " << a.d << " + dim + j] : fromf<" << T << ">(0.0f);\n    }\n";
+    s << "#pragma unroll\n    for (int f = 0; f < " << NF << "; ++f) sc[f] = " << fn << "(qa, *(const " << V8
+      << "*)(Ks + (f * 16 + (l & 15)) * " << KSP << " + dim), sc[f], 0, 0, 0);\n  }\n";
+  }
+  // score chain, row max, exp, row sum, divide -- rows (l>>4)*4 + i, key f*16 + (l&15)
+  std::string chain_expr = "x";
+  for (int c : a.chain) {
+    const Node& cn = g.nodes[c];
+    if (op_kind(cn.op) == Kind::Unary)
+      chain_expr = unary_expr(cn.op, chain_expr);
+    else
+      chain_expr = binary_expr(cn.op, chain_expr, flit(cn.attrs.scalar));
+  }
+  s << "  float mx[4], sm[4];\n";
+  s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = -__builtin_huge_valf();\n";
+  s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
+  s << "    const float x = sc[f][i];\n    sc[f][i] = " << chain_expr << ";\n";
+  if (nkp != a.nk) s << "    if (f * 16 + (l & 15) >= " << a.nk << ") sc[f][i] = -__builtin_huge_valf();\n";
+  s << "    mx[i] = k_max(mx[i], sc[f][i]);\n  }\n";
+  s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = group_max<16>(mx[i]);\n";
+  s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = 0.0f;\n";
+  s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
+  s << "    sc[f][i] = expf(sc[f][i] - mx[i]);\n    sm[i] += sc[f][i];\n  }\n";
+  s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = group_sum<16>(sm[i]);\n";
+  s << "  " << T << "* Pw = Ps + wave * " << 16 * NKP << ";\n";
+  s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) Pw[((l >> 4) * 4 + i) * "
+    << NKP << " + f * 16 + (l & 15)] = fromf<" << T << ">(sc[f][i] / sm[i]);\n";
+  s << "  __syncthreads();\n";
+  // O = P V
+  s << "  f32x4 oc[" << OF << "];\n";
+  s << "#pragma unroll\n  for (int f = 0; f < " << OF << "; ++f) oc[f] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
+  if (f32) {
+    s << "#pragma unroll\n  for (int kk = 0; kk < " << nkp / 4 << "; ++kk) {\n";
+    s << "    const int key = kk * 4 + (l >> 4);\n";
+    s << "    const float pa = Pw[(l & 15) * " << NKP << " + key];\n";
+    s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, Vs[key * " << VP
+      << " + f * 16 + (l & 15)], oc[f], 0, 0, 0);\n  }\n";
+  } else {
+    std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
+    std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
+    s << "#pragma unroll\n  for (int kk = 0; kk < " << nkp / 32 << "; ++kk) {\n";
+    s << "    const int key = kk * 32 + (l >> 4) * 8;\n";
+    s << "    const " << V8 << " pa = *(const " << V8 << "*)(Pw + (l & 15) * " << NKP << " + key);\n";
+    s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = " << fn << "(pa, *(const " << V8
+      << "*)(Vs + (f * 16 + (l & 15)) * " << NKP << " + key), oc[f], 0, 0, 0);\n  }\n";
+  }
+  s << "#pragma unroll\n  for (int f = 0; f < " << OF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
+  s << "    const i64 row = q0 + (l >> 4) * 4 + i;\n";
+  s << "    const int col = f * 16 + (l & 15);\n";
+  s << "    if (row < " << a.nq << "LL && col < " << a.dv << ") st1(" << O << " + ooff + row * " << a.dv
+    << " + col, oc[f][i]);\n  }\n";
+  s << "}\n";
+  gk.source = s.str();
+  gk.grid[0] = (int)((a.nq + 63) / 64);
+  gk.grid[1] = (int)a.batch;
+  gk.lds_bytes = (int)smem;
+  ki.fill_cost(gk);
+  return gk;
+}
 
 }  // namespace korch

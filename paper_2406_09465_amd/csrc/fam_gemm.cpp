@@ -437,7 +437,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
 }
 
 // The MFMA main loop over k-tiles [kt0, kt1) of the contraction.
-std::string mfma_mainloop(const GemmSpec& sp) {
+std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
   std::ostringstream s;
   bool f32 = sp.mtype == KORCH_F32;
   std::string T = ctype(sp.mtype);
@@ -474,14 +474,17 @@ std::string mfma_mainloop(const GemmSpec& sp) {
   s << "  for (int kt = kt0; kt < kt1; ++kt) {\n";
   s << "    const int cur = (kt - kt0) & 1;\n";
   s << "    if (kt + 1 < kt1) { fetchA((i64)(kt + 1) * " << sp.BK << "); fetchB((i64)(kt + 1) * " << sp.BK << "); }\n";
-  s << "    compute(cur);\n";
+  int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
+  std::string wguard = nw < 4 ? "if (wave < " + std::to_string(nw) + ") " : "";
+  s << "    " << wguard << "compute(cur);\n";
+  if (!hook.empty()) s << "    {\n      const " << T << "* Ab = As + cur * " << sp.BM * sp.BKP << ";\n" << hook << "    }\n";
   s << "    if (kt + 1 < kt1) { stashA(cur ^ 1); stashB(cur ^ 1); }\n";
   s << "    __syncthreads();\n  }\n";
   // accumulators -> LDS C tile (fp32)
   s << "  float* Cs = (float*)smem;\n";
-  s << "#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
+  s << "  " << wguard << "{\n#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
     << "; ++j)\n#pragma unroll\n  for (int r = 0; r < 4; ++r) Cs[(wm * " << sp.WTM << " + i * 16 + (l >> 4) * 4 + r) * "
-    << sp.LDC << " + wn * " << sp.WTN << " + j * 16 + (l & 15)] = acc[i][j][r];\n";
+    << sp.LDC << " + wn * " << sp.WTN << " + j * 16 + (l & 15)] = acc[i][j][r];\n  }\n";
   s << "  __syncthreads();\n";
   return s.str();
 }
@@ -494,7 +497,7 @@ size_t gemm_smem_bytes(const GemmSpec& sp) {
 
 // Pointwise epilogue over the C tile: every kernel output at (batch, m, n).
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
-                          const std::string& cs_row) {
+                          const std::string& cs_row, const std::set<int>& skip) {
   const Graph& g = ki.g;
   int maxb = 2;
   for (int o : ki.k.outs) maxb = std::max(maxb, dtype_bytes(g.nodes[o].dtype));
@@ -536,6 +539,7 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
   };
   std::ostringstream decl, after;
   for (int o : ki.k.outs) {
+    if (skip.count(o)) continue;
     const Node& on = g.nodes[o];
     auto bi = broadcast_index(on.shape, sp.OUT, it);
     std::string v = em.value(o, bi);

@@ -35,9 +35,9 @@ struct GemmSpec {
 bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_reduce);
 void choose_tiles(GemmSpec& sp, bool split);
 std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot);
-std::string mfma_mainloop(const GemmSpec& sp);
+std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "");
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
-                          const std::string& cs_row);
+                          const std::string& cs_row, const std::set<int>& skip = {});
 std::string gemm_prologue_common(const GemmSpec& sp);
 size_t gemm_smem_bytes(const GemmSpec& sp);
 

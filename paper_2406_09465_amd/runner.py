@@ -56,6 +56,11 @@ class PlanRunner:
         self.plan.execute([t.data_ptr() for t in self.ins], [t.data_ptr() for t in self.outs],
                           self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
 
+    def launch_kernels(self, first, count, stream=None):
+        s = stream if stream is not None else torch.cuda.current_stream()
+        self.plan.execute_kernels(first, count, [t.data_ptr() for t in self.ins], [t.data_ptr() for t in self.outs],
+                                  self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
+
     def run(self, storage: dict = None):
         if storage is not None:
             self.set_inputs(storage)
