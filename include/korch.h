@@ -147,6 +147,9 @@ int korch_graph_num_nodes(const korch_graph* g, int32_t* n);
 /* Shape / dtype / op of a node; shape must hold KORCH_MAX_RANK entries. */
 int korch_graph_node_info(const korch_graph* g, int32_t node, int32_t* op, int32_t* dtype, int32_t* rank,
                           int64_t* shape);
+/* The producers a node reads, in operand order: *n receives the count and at
+   most `cap` ids are written to `ids` (which may be NULL when cap is 0). */
+int korch_graph_node_inputs(const korch_graph* g, int32_t node, int32_t* ids, int32_t cap, int32_t* n);
 int korch_graph_num_inputs(const korch_graph* g, int32_t* n);
 int korch_graph_num_outputs(const korch_graph* g, int32_t* n);
 int korch_graph_input_node(const korch_graph* g, int32_t i, int32_t* node);

@@ -72,6 +72,7 @@ _SIGS = {
     "korch_graph_finalize": ([_P], C.c_int),
     "korch_graph_num_nodes": ([_P, C.POINTER(_I)], C.c_int),
     "korch_graph_node_info": ([_P, _I, C.POINTER(_I), C.POINTER(_I), C.POINTER(_I), C.POINTER(C.c_int64)], C.c_int),
+    "korch_graph_node_inputs": ([_P, _I, C.POINTER(_I), _I, C.POINTER(_I)], C.c_int),
     "korch_graph_num_inputs": ([_P, C.POINTER(_I)], C.c_int),
     "korch_graph_num_outputs": ([_P, C.POINTER(_I)], C.c_int),
     "korch_graph_input_node": ([_P, _I, C.POINTER(_I)], C.c_int),
@@ -189,6 +190,13 @@ class Graph:
         shape = (C.c_int64 * MAX_RANK)()
         check(lib.korch_graph_node_info(self.h, int(node), C.byref(op), C.byref(dt), C.byref(rank), shape))
         return OP_NAMES[op.value], DTYPE_NAMES[dt.value], tuple(shape[i] for i in range(rank.value))
+
+    def node_inputs(self, node):
+        n = _I()
+        check(lib.korch_graph_node_inputs(self.h, int(node), None, 0, C.byref(n)))
+        buf = (_I * max(1, n.value))()
+        check(lib.korch_graph_node_inputs(self.h, int(node), buf, n.value, C.byref(n)))
+        return [buf[i] for i in range(n.value)]
 
     def inputs(self):
         n = _I()

@@ -167,6 +167,18 @@ int korch_graph_node_info(const korch_graph* g, int32_t node, int32_t* op, int32
   });
 }
 
+int korch_graph_node_inputs(const korch_graph* g, int32_t node, int32_t* ids, int32_t cap, int32_t* n) {
+  return guard([&] {
+    NEED(g);
+    NEED(n);
+    if (node < 0 || node >= (int)g->g.nodes.size()) fail(KORCH_E_ARG, "node id out of range");
+    if (cap < 0 || (cap > 0 && !ids)) fail(KORCH_E_ARG, "bad id buffer");
+    const auto& in = g->g.nodes[node].in;
+    *n = (int32_t)in.size();
+    for (int i = 0; i < (int)in.size() && i < cap; ++i) ids[i] = in[i];
+  });
+}
+
 int korch_graph_num_inputs(const korch_graph* g, int32_t* n) {
   return guard([&] {
     NEED(g);

@@ -72,6 +72,13 @@ std::string flit(double v);                   // float literal
 std::string unary_expr(int op, const std::string& x);
 std::string binary_expr(int op, const std::string& x, const std::string& y);
 
+// Kernels whose outputs are all fp16 / bf16 use the fast transcendental
+// variants (set per generated kernel; thread-local).
+void set_fast_math(bool on);
+bool fast_math();
+// The fissioned Mish pattern rooted at `node` (a product); returns its input or -1.
+int mish_operand(const Graph& g, const std::set<int>& inset, int node);
+
 // Row-major strides of a shape.
 std::vector<int64_t> strides_of(const Shape& s);
 

@@ -163,18 +163,24 @@ std::string flit(double v) {
   return "(" + s + "f)";
 }
 
+thread_local bool g_fast_math = false;
+
+void set_fast_math(bool on) { g_fast_math = on; }
+bool fast_math() { return g_fast_math; }
+
 std::string unary_expr(int op, const std::string& x) {
+  bool f = g_fast_math;
   switch (op) {
     case KORCH_NEG: return "(-" + x + ")";
-    case KORCH_EXP: return "expf(" + x + ")";
-    case KORCH_LOG: return "logf(" + x + ")";
-    case KORCH_TANH: return "tanhf(" + x + ")";
+    case KORCH_EXP: return (f ? "f_exp(" : "expf(") + x + ")";
+    case KORCH_LOG: return (f ? "f_log(" : "logf(") + x + ")";
+    case KORCH_TANH: return (f ? "f_tanh(" : "tanhf(") + x + ")";
     case KORCH_SQRT: return "sqrtf(" + x + ")";
-    case KORCH_RSQRT: return "k_rsqrt(" + x + ")";
+    case KORCH_RSQRT: return (f ? "f_rsqrt(" : "k_rsqrt(") + x + ")";
     case KORCH_RELU: return "k_relu(" + x + ")";
     case KORCH_SQUARE: return "(" + x + "*" + x + ")";
-    case KORCH_RECIP: return "(1.0f/" + x + ")";
-    case KORCH_GELU_TANH: return "k_gelu_tanh(" + x + ")";
+    case KORCH_RECIP: return f ? "f_div(1.0f, " + x + ")" : "(1.0f/" + x + ")";
+    case KORCH_GELU_TANH: return (f ? "f_gelu_tanh(" : "k_gelu_tanh(") + x + ")";
     case KORCH_ABS: return "fabsf(" + x + ")";
     case KORCH_IDENTITY: return x;
   }
@@ -186,7 +192,7 @@ std::string binary_expr(int op, const std::string& x, const std::string& y) {
     case KORCH_ADD: return "(" + x + " + " + y + ")";
     case KORCH_SUB: return "(" + x + " - " + y + ")";
     case KORCH_MUL: return "(" + x + " * " + y + ")";
-    case KORCH_DIV: return "(" + x + " / " + y + ")";
+    case KORCH_DIV: return g_fast_math ? "f_div(" + x + ", " + y + ")" : "(" + x + " / " + y + ")";
     case KORCH_MAX: return "k_max(" + x + ", " + y + ")";
     case KORCH_MIN: return "k_min(" + x + ", " + y + ")";
   }
@@ -213,6 +219,27 @@ std::vector<Ix> broadcast_index(const Shape& shape, const Shape& itshape, const 
       fail(KORCH_E_UNSUPPORTED, "operand shape does not broadcast to iteration shape");
   }
   return out;
+}
+
+// Recognizes the fissioned Mish product  Y = B * T,  T = tanh(SP),
+// SP = log(E1), E1 = E + 1, E = exp(B)  (all inside the kernel, no
+// broadcasting); returns B or -1.
+int mish_operand(const Graph& g, const std::set<int>& inset, int node) {
+  const Node& y = g.nodes[node];
+  if (y.op != KORCH_MUL || y.attrs.has_scalar || y.in.size() != 2) return -1;
+  for (int side = 0; side < 2; ++side) {
+    int b = y.in[side], t = y.in[1 - side];
+    auto is = [&](int v, int op) { return inset.count(v) && g.nodes[v].op == op && g.nodes[v].shape == y.shape; };
+    if (g.nodes[b].shape != y.shape || !is(t, KORCH_TANH)) continue;
+    int sp = g.nodes[t].in[0];
+    if (!is(sp, KORCH_LOG)) continue;
+    int e1 = g.nodes[sp].in[0];
+    if (!is(e1, KORCH_ADD) || !g.nodes[e1].attrs.has_scalar || g.nodes[e1].attrs.scalar != 1.0) continue;
+    int e = g.nodes[e1].in[0];
+    if (!is(e, KORCH_EXP) || g.nodes[e].in[0] != b) continue;
+    return b;
+  }
+  return -1;
 }
 
 std::string Emitter::key(int node, const std::vector<Ix>& idx) {
@@ -331,6 +358,14 @@ std::string Emitter::value(int node, const std::vector<Ix>& idx) {
     }
     case Kind::Binary: {
       std::string x, y;
+      int mb = mish_operand(g, inset, node);
+      if (mb >= 0) {
+        // B * tanh(log(exp(B) + 1)) evaluated through the exact identity x n / (n + 2)
+        x = value(mb, idx);
+        out = fresh("t");
+        body << "    const float " << out << " = " << (g_fast_math ? "f_mish(" : "k_mish(") << x << ");\n";
+        break;
+      }
       if (n.attrs.has_scalar) {
         x = value(n.in[0], idx);
         y = flit(n.attrs.scalar);

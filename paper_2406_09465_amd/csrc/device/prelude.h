@@ -33,6 +33,8 @@ template <typename T> struct VecOf<1, T> {
   typedef T type;
 };
 
+template <int V, typename T> using vec_t = typename VecOf<V, T>::type;
+
 template <int V, typename T>
 __device__ __forceinline__ void ldv(float* d, const T* __restrict__ p) {
   if constexpr (V == 1) {
@@ -73,12 +75,32 @@ __device__ __forceinline__ float k_max(float a, float b) { return a > b ? a : b;
 __device__ __forceinline__ float k_min(float a, float b) { return a < b ? a : b; }
 
 // Mish written as x * n / (n + 2) with n = e^x (e^x + 2), which equals
-// x * tanh(log(1 + e^x)) exactly; for large x the quotient is 1 in fp32.
+// x * tanh(log(1 + e^x)) exactly; for x > 20 the quotient is 1 in fp32.
 __device__ __forceinline__ float k_mish(float x) {
   if (x > 20.0f) return x;
-  float ex = __expf(x);
+  float ex = expf(x);
   float n = ex * (ex + 2.0f);
   return x * (n / (n + 2.0f));
+}
+
+// Fast variants for kernels whose results are stored in fp16 / bf16: the
+// hardware exp2 / log2 / reciprocal approximations (a few ulp of fp32),
+// far below the 2^-11 / 2^-8 spacing of the stored values.
+__device__ __forceinline__ float f_exp(float x) { return __expf(x); }
+__device__ __forceinline__ float f_log(float x) { return __logf(x); }
+__device__ __forceinline__ float f_div(float x, float y) { return x * __builtin_amdgcn_rcpf(y); }
+// tanh(x) = 1 - 2 / (e^{2x} + 1): saturates to +-1 when e^{2x} overflows or vanishes.
+__device__ __forceinline__ float f_tanh(float x) { return 1.0f - f_div(2.0f, f_exp(2.0f * x) + 1.0f); }
+__device__ __forceinline__ float f_rsqrt(float x) { return __builtin_amdgcn_rsqf(x); }
+__device__ __forceinline__ float f_gelu_tanh(float x) {
+  const float c = 0.7978845608028654f;
+  return 0.5f * x * (1.0f + f_tanh(c * (x + 0.044715f * x * x * x)));
+}
+__device__ __forceinline__ float f_mish(float x) {
+  if (x > 20.0f) return x;
+  float ex = f_exp(x);
+  float n = ex * (ex + 2.0f);
+  return x * f_div(n, n + 2.0f);
 }
 
 // ---- reductions across a group of G lanes of a wavefront (G power of two <= 64)

@@ -245,11 +245,11 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = group_max<16>(mx[i]);\n";
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = 0.0f;\n";
   s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
-  s << "    sc[f][i] = expf(sc[f][i] - mx[i]);\n    sm[i] += sc[f][i];\n  }\n";
+  s << "    sc[f][i] = " << unary_expr(KORCH_EXP, "(sc[f][i] - mx[i])") << ";\n    sm[i] += sc[f][i];\n  }\n";
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = group_sum<16>(sm[i]);\n";
   s << "  " << T << "* Pw = Ps + wave * " << 16 * NKP << ";\n";
   s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) Pw[((l >> 4) * 4 + i) * "
-    << NKP << " + f * 16 + (l & 15)] = fromf<" << T << ">(sc[f][i] / sm[i]);\n";
+    << NKP << " + f * 16 + (l & 15)] = fromf<" << T << ">(" << binary_expr(KORCH_DIV, "sc[f][i]", "sm[i]") << ");\n";
   s << "  __syncthreads();\n";
   // O = P V
   s << "  f32x4 oc[" << OF << "];\n";

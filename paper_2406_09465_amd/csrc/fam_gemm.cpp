@@ -260,10 +260,109 @@ void choose_tiles(GemmSpec& sp, bool split) {
   sp.LDC = sp.BN + 4;
 }
 
+// Raw staging of an operand that is a plain materialized tensor (no prologue):
+// the bytes go to LDS unchanged.  A k-contiguous operand ([.., rows, K]) moves
+// as 16-byte vectors; a row-contiguous one ([.., K, rows], e.g. a weight
+// [K, N]) is read as 4-wide row vectors from KB consecutive k and transposed in
+// registers, so every LDS write is a 16-byte vector of KB consecutive k.
+// Returns "" when the operand does not qualify.
+static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot) {
+  const Graph& g = ki.g;
+  if (sp.conv && isA) return "";
+  if (!sp.conv && (!isA && sp.Bs.size() != 1)) return "";
+  int node = isA ? sp.A : sp.Bs[0];
+  if (ki.in.count(node)) return "";
+  bool f32 = sp.mtype == KORCH_F32;
+  std::string T = ctype(sp.mtype);
+  int rows = isA ? sp.BM : sp.BN;
+  int64_t R = isA ? sp.M : sp.N;
+  std::string X = isA ? "A" : "B";
+  std::string lds = isA ? "As" : "Bs";
+  std::string base = isA ? "m0" : "n0";
+  std::string P = "((const " + T + "*)a.p[" + std::to_string(slot.at(node)) + "])";
+  // batch offset of the operand (broadcast batch dims read index 0)
+  std::string boff = "0";
+  if (!sp.conv) {
+    const Shape& sh = g.nodes[node].shape;
+    Shape ob(sp.OUT.begin(), sp.OUT.begin() + sp.nb);
+    Shape nbsh(sh.begin(), sh.end() - 2);
+    std::vector<Ix> zc;
+    for (int d = 0; d < sp.nb; ++d) zc.push_back(Ix::var("z" + std::to_string(d)));
+    auto bi = broadcast_index(nbsh, ob, zc);
+    auto st = strides_of(sh);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], st[d], 1));
+    boff = off.at();
+  }
+  std::ostringstream s;
+  if (isA) {
+    // A: [.., M, K], k contiguous
+    int V = sp.VA;
+    if (sp.K % V) return "";
+    int kper = sp.BK / V;
+    int nslots = rows * kper;
+    int per = (nslots + 255) / 256;
+    s << "  uint4 r" << X << "[2][" << per << "];\n";
+    s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+    s << "    const int sl = tid + i * 256;\n";
+    if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+    s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
+    s << "    const i64 rg = " << base << " + rl, kg = k0 + kl;\n";
+    s << "    if (rg < " << R << "LL && kg + " << V << " <= " << sp.K << "LL) r" << X << "[st][i] = *(const uint4*)(" << P
+      << " + " << boff << " + rg * " << sp.K << "LL + kg);\n";
+    s << "    else {\n      " << T << " t_[" << V << "];\n#pragma unroll\n      for (int e = 0; e < " << V
+      << "; ++e) t_[e] = (rg < " << R << "LL && kg + e < " << sp.K << "LL) ? " << P << "[" << boff << " + rg * "
+      << sp.K << "LL + kg + e] : fromf<" << T << ">(0.0f);\n      __builtin_memcpy(&r" << X << "[st][i], t_, 16);\n    }\n";
+    s << "  }\n  };\n";
+    s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+    s << "    const int sl = tid + i * 256;\n";
+    if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+    s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
+    s << "    *(uint4*)(" << lds << " + buf * " << rows * sp.BKP << " + rl * " << sp.BKP << " + kl) = r" << X << "[st][i];\n";
+    s << "  }\n  };\n";
+    return s.str();
+  }
+  // B: [.., K, N] (or conv weights [KH, KW, Cin, Cout] = [K, N]), n contiguous
+  const int VT = 4;
+  int KB = f32 ? 4 : 8;
+  if (sp.N % VT) return "";
+  int nper = rows / VT;
+  int nblocks = (sp.BK / KB) * nper;
+  int per = (nblocks + 255) / 256;
+  std::string T4 = "vec_t<4, " + T + ">";
+  std::string TK = "vec_t<" + std::to_string(KB) + ", " + T + ">";
+  s << "  " << T4 << " r" << X << "[2][" << per << "][" << KB << "];\n";
+  s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+  s << "    const int b_ = tid + i * 256;\n";
+  if (nblocks % 256) s << "    if (b_ >= " << nblocks << ") break;\n";
+  s << "    const int kb = b_ / " << nper << ", nb = b_ % " << nper << ";\n";
+  s << "    const i64 kg = k0 + kb * " << KB << ", ng = " << base << " + nb * " << VT << ";\n";
+  s << "#pragma unroll\n    for (int kk = 0; kk < " << KB << "; ++kk) {\n";
+  s << "      const i64 k = kg + kk;\n";
+  s << "      if (k < " << sp.K << "LL && ng + " << VT << " <= " << sp.N << "LL) r" << X << "[st][i][kk] = *(const " << T4
+    << "*)(" << P << " + " << boff << " + k * " << sp.N << "LL + ng);\n";
+  s << "      else {\n#pragma unroll\n        for (int j = 0; j < " << VT << "; ++j) r" << X
+    << "[st][i][kk][j] = (k < " << sp.K << "LL && ng + j < " << sp.N << "LL) ? " << P << "[" << boff << " + k * " << sp.N
+    << "LL + ng + j] : fromf<" << T << ">(0.0f);\n      }\n    }\n  }\n  };\n";
+  s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+  s << "    const int b_ = tid + i * 256;\n";
+  if (nblocks % 256) s << "    if (b_ >= " << nblocks << ") break;\n";
+  s << "    const int kb = b_ / " << nper << ", nb = b_ % " << nper << ";\n";
+  s << "#pragma unroll\n    for (int j = 0; j < " << VT << "; ++j) {\n      " << TK << " col;\n";
+  s << "#pragma unroll\n      for (int kk = 0; kk < " << KB << "; ++kk) col[kk] = r" << X << "[st][i][kk][j];\n";
+  s << "      *(" << TK << "*)(" << lds << " + buf * " << rows * sp.BKP << " + (nb * " << VT << " + j) * " << sp.BKP
+    << " + kb * " << KB << ") = col;\n    }\n  }\n  };\n";
+  return s.str();
+}
+
 // Emits a lambda `fetchX(k0)` that evaluates the operand (with its prologue)
 // for this thread's slots of a BM x BK (A) or BN x BK (B) tile into registers,
 // and `stashX(buf)` that converts and writes them to LDS in [row][k] layout.
 std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot) {
+  {
+    std::string raw = raw_loader(ki, sp, isA, slot);
+    if (!raw.empty()) return raw;
+  }
   const Graph& g = ki.g;
   int V = isA ? sp.VA : sp.VB;
   int rows = isA ? sp.BM : sp.BN;
@@ -349,8 +448,8 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   int kper = axis_k ? sp.BK / V : sp.BK;
   // slot s -> (row, k): axis_k: row = s / (BK/V), kk = (s % (BK/V)) * V
   //                     axis_row: kk = s / (rows/V), row = (s % (rows/V)) * V
-  s << "  float r" << X << "[" << per << "][" << V << "];\n";
-  s << "  auto fetch" << X << " = [&](const i64 k0) {\n";
+  s << "  float r" << X << "[2][" << per << "][" << V << "];\n";
+  s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
   s << "    const int sl = tid + i * 256;\n";
   if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
@@ -360,14 +459,15 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
     s << "    const int kl = sl / " << rows / V << ", rl = (sl % " << rows / V << ") * " << V << ";\n";
   std::string base = isA ? "m0" : "n0";
   s << "    const i64 rg = " << base << " + rl, kg = k0 + kl;\n";
-  s << "    float* dst = r" << X << "[i];\n";
+  s << "    float* dst = r" << X << "[st][i];\n";
   if (sp.conv && isA) {
-    // implicit GEMM: row = output pixel, k = (ky, kx, ci)
+    // implicit GEMM: row = output pixel, k = (ky, kx, ci); 32-bit index math
+    // (pixel counts and per-image sizes are far below 2^31)
     bool vecok = sp.Cin % V == 0;
-    s << "    {\n      const i64 oy = rg / " << sp.Wo << ", ox = rg % " << sp.Wo << ";\n";
-    s << "      const i64 tap = kg / " << sp.Cin << ", ci = kg % " << sp.Cin << ";\n";
-    s << "      const i64 iy = oy * " << sp.stride << " + tap / " << sp.KW << " - " << sp.pad << ";\n";
-    s << "      const i64 ix = ox * " << sp.stride << " + tap % " << sp.KW << " - " << sp.pad << ";\n";
+    s << "    {\n      const int oy = (int)rg / " << sp.Wo << ", ox = (int)rg % " << sp.Wo << ";\n";
+    s << "      const int tap = (int)kg / " << sp.Cin << ", ci = (int)kg % " << sp.Cin << ";\n";
+    s << "      const int iy = oy * " << sp.stride << " + tap / " << sp.KW << " - " << sp.pad << ";\n";
+    s << "      const int ix = ox * " << sp.stride << " + tap % " << sp.KW << " - " << sp.pad << ";\n";
     std::string P = "((const " + T + "*)a.p[" + std::to_string(slot.at(sp.A)) + "])";
     std::string bofs = sp.nb ? "z0 * " + std::to_string(sp.H * sp.W * sp.Cin) + "LL + " : "";
     s << "      const bool ok = rg < " << sp.M << "LL && kg < " << sp.K << "LL && iy >= 0 && iy < " << sp.H
@@ -419,18 +519,18 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   }
   s << "  }\n  };\n";
   // stash: fp32 registers -> LDS [row][k] of the MFMA operand type
-  s << "  auto stash" << X << " = [&](const int buf) {\n";
+  s << "  auto stash" << X << " = [&](const int buf, const int st) {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
   s << "    const int sl = tid + i * 256;\n";
   if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
   if (axis_k) {
     s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
     s << "    stv<" << V << ">(" << lds << " + buf * " << rows * sp.BKP << " + rl * " << sp.BKP << " + kl, r" << X
-      << "[i]);\n";
+      << "[st][i]);\n";
   } else {
     s << "    const int kl = sl / " << rows / V << ", rl = (sl % " << rows / V << ") * " << V << ";\n";
     s << "#pragma unroll\n    for (int e = 0; e < " << V << "; ++e) " << lds << "[buf * " << rows * sp.BKP
-      << " + (rl + e) * " << sp.BKP << " + kl] = fromf<" << T << ">(r" << X << "[i][e]);\n";
+      << " + (rl + e) * " << sp.BKP << " + kl] = fromf<" << T << ">(r" << X << "[st][i][e]);\n";
   }
   s << "  }\n  };\n";
   return s.str();
@@ -469,17 +569,32 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
       << sp.FN << "; ++j) acc[i][j] = " << fn << "(af[i], bf[j], acc[i][j], 0, 0, 0);\n";
   }
   s << "    }\n  };\n";
-  s << "  fetchA((i64)kt0 * " << sp.BK << "); fetchB((i64)kt0 * " << sp.BK << ");\n";
-  s << "  stashA(0); stashB(0);\n  __syncthreads();\n";
-  s << "  for (int kt = kt0; kt < kt1; ++kt) {\n";
-  s << "    const int cur = (kt - kt0) & 1;\n";
-  s << "    if (kt + 1 < kt1) { fetchA((i64)(kt + 1) * " << sp.BK << "); fetchB((i64)(kt + 1) * " << sp.BK << "); }\n";
+  // Two-deep pipeline: while tile t is multiplied from LDS buffer t%2, the
+  // registers of stage (t+1)%2 already hold tile t+1 (loaded one iteration
+  // earlier) and the loads of tile t+2 are in flight into stage t%2.  The loop
+  // is unrolled by two so every register stage index is a constant.
   int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
   std::string wguard = nw < 4 ? "if (wave < " + std::to_string(nw) + ") " : "";
-  s << "    " << wguard << "compute(cur);\n";
-  if (!hook.empty()) s << "    {\n      const " << T << "* Ab = As + cur * " << sp.BM * sp.BKP << ";\n" << hook << "    }\n";
-  s << "    if (kt + 1 < kt1) { stashA(cur ^ 1); stashB(cur ^ 1); }\n";
-  s << "    __syncthreads();\n  }\n";
+  auto ktile = [&](const std::string& t) { return "(i64)(" + t + ") * " + std::to_string(sp.BK); };
+  auto step = [&](int b, const std::string& kt) {
+    std::ostringstream o;
+    o << "    if (" << kt << " + 2 < kt1) { fetchA(" << ktile(kt + " + 2") << ", " << b << "); fetchB(" << ktile(kt + " + 2")
+      << ", " << b << "); }\n";
+    o << "    " << wguard << "compute(" << b << ");\n";
+    if (!hook.empty()) o << "    {\n      const " << T << "* Ab = As + " << b * sp.BM * sp.BKP << ";\n" << hook << "    }\n";
+    o << "    if (" << kt << " + 1 < kt1) { stashA(" << 1 - b << ", " << 1 - b << "); stashB(" << 1 - b << ", " << 1 - b
+      << "); }\n";
+    o << "    __syncthreads();\n";
+    return o.str();
+  };
+  s << "  fetchA(" << ktile("kt0") << ", 0); fetchB(" << ktile("kt0") << ", 0);\n";
+  s << "  if (kt0 + 1 < kt1) { fetchA(" << ktile("kt0 + 1") << ", 1); fetchB(" << ktile("kt0 + 1") << ", 1); }\n";
+  s << "  stashA(0, 0); stashB(0, 0);\n  __syncthreads();\n";
+  s << "  for (int kt = kt0; kt < kt1; kt += 2) {\n";
+  s << step(0, "kt");
+  s << "    if (kt + 1 >= kt1) break;\n";
+  s << step(1, "(kt + 1)");
+  s << "  }\n";
   // accumulators -> LDS C tile (fp32)
   s << "  float* Cs = (float*)smem;\n";
   s << "  " << wguard << "{\n#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN

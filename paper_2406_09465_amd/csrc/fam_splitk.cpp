@@ -11,6 +11,7 @@
 // accumulated from the operand tiles as they pass through LDS.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 
 #include "gemm_common.h"
 
@@ -244,7 +245,11 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   int64_t mtiles = (sp.M + sp.BM - 1) / sp.BM;
   int64_t KT = (sp.K + sp.BK - 1) / sp.BK;
   int64_t base = mtiles * sp.batch;
-  int64_t S = std::max<int64_t>(1, std::min<int64_t>((512 + base - 1) / base, std::max<int64_t>(1, KT / 2)));
+  // about KORCH_SPLITK_WGS workgroups in total (default 256, one per compute
+  // unit), each with at least 4 k-tiles
+  int64_t target = 256;
+  if (const char* e = getenv("KORCH_SPLITK_WGS")) target = std::max(1, atoi(e));
+  int64_t S = std::max<int64_t>(1, std::min<int64_t>((target + base - 1) / base, std::max<int64_t>(1, KT / 4)));
   int64_t ktper = (KT + S - 1) / S;
   S = (KT + ktper - 1) / ktper;
   int64_t tile = (int64_t)sp.BM * sp.BN;
@@ -289,11 +294,16 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "  for (int i = tid; i < " << tile << "; i += 256) part[(tix * " << S << " + split) * " << tile
     << "LL + i] = Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "];\n";
   if (nside) s << "  if (tid < " << sp.BM << ") sidep[(tix * " << S << " + split) * " << sp.BM << " + tid] = side_acc;\n";
-  s << "  __threadfence();\n  __syncthreads();\n";
-  s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
+  // Every wave's partial stores precede the barrier; one device-scope release
+  // by thread 0 then publishes the workgroup's partials before the counter
+  // increment, and the last workgroup's acquire makes all partials visible.
+  s << "  __syncthreads();\n";
+  s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n    __threadfence();\n";
   s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);\n";
-  s << "    last_ = (old == " << S - 1 << ");\n    if (last_) __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
-  s << "  __syncthreads();\n  if (!last_) return;\n  __threadfence();\n";
+  s << "    last_ = (old == " << S - 1 << ");\n";
+  s << "    if (last_) {\n      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n"
+    << "      __threadfence();\n    }\n  }\n";
+  s << "  __syncthreads();\n  if (!last_) return;\n";
   // deterministic sum of the partials, split 0 first
   s << "  for (int i = tid; i < " << tile << "; i += 256) {\n    float acc_ = 0.0f;\n";
   s << "    for (int p = 0; p < " << S << "; ++p) acc_ += part[(tix * " << S << " + p) * " << tile << "LL + i];\n";

@@ -630,6 +630,10 @@ GenKernel generate_kernel(const Graph& g, const KernelDesc& k, int index) {
   std::string why;
   int fam = match_family(g, k, &why);
   KInfo ki(g, k);
+  bool half_outputs = true;
+  for (int o : k.outs)
+    if (g.nodes[o].dtype == KORCH_F32) half_outputs = false;
+  set_fast_math(half_outputs);
   switch (fam) {
     case KORCH_FAM_POINTWISE: return gen_pointwise(ki, index);
     case KORCH_FAM_ROW: return gen_row(ki, index);

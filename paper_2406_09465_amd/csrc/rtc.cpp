@@ -3,6 +3,7 @@
 #include <hip/hiprtc.h>
 #include <sys/stat.h>
 #include <unistd.h>
+#include <utime.h>
 
 #include <cstdio>
 #include <cstdlib>
@@ -62,7 +63,10 @@ std::vector<char> rtc_compile(const std::string& src, const std::string& name) {
     std::ifstream f(path, std::ios::binary);
     if (f) {
       std::vector<char> code((std::istreambuf_iterator<char>(f)), std::istreambuf_iterator<char>());
-      if (!code.empty()) return code;
+      if (!code.empty()) {
+        utime(path.c_str(), nullptr);  // mark as recently used (cache pruning keeps it)
+        return code;
+      }
     }
   }
   hiprtcProgram prog;

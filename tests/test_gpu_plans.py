@@ -1,0 +1,64 @@
+"""GPU parity of seeded random orchestration plans, and the kernel profiler.
+
+Every valid plan -- any grouping of primitives into supported convex kernels,
+with redundant execution and pruning -- must reproduce the unfused float64
+oracle within the dtype tolerance (fusion changes cost, not the result).
+"""
+
+import math
+
+import pytest
+
+from oracle import configs as OC
+from oracle.graph import run_unfused
+from tests.helpers import TOL, close, inputs_f64
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SIZES = {
+    "attention": dict(n=96, d=32),
+    "mlp": dict(m=256, d=128, h=192),
+    "sra": dict(hh=32, ww=32, c=32, r=8),
+    "conv": dict(hh=24, ww=20, cin=16, cout=32),
+    "linattn": dict(heads=4, n=512, d=16),
+}
+N_PLANS = 6
+SEED = 7
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.mark.parametrize("workload", list(SIZES))
+def test_sampled_plans(workload):
+    from paper_2406_09465_amd import graphs, search
+    from paper_2406_09465_amd.runner import PlanRunner
+    sizes = SIZES[workload]
+    w = graphs.build(workload, **sizes)
+    raw, x64 = inputs_f64(workload, **sizes)
+    ref = run_unfused(OC.build(workload, **sizes), x64)
+    plans = search.sampled_plans(w.graph, N_PLANS, SEED)
+    tol = TOL[w.dtype]
+    for i, ks in enumerate(plans):
+        print(f"\n[case] {workload} sampled plan {i}: {len(ks)} kernels", flush=True)
+        out = PlanRunner(w, kernels=ks).run(raw)
+        for name in w.output_names:
+            ok, mx, rel = close(out[name], ref[name], tol)
+            assert ok, f"{workload} plan {i} {ks}: max err {mx:.3e} rel {rel:.3e}"
+
+
+def test_profiler_times_candidates():
+    from paper_2406_09465_amd import graphs
+    w = graphs.mlp(**SIZES["mlp"])
+    print("\n[case] profiler", flush=True)
+    for prims, outs in w.kernels("fused"):
+        us = w.graph.profile(prims, outs, warmup=3, reps=10, flush_bytes=64 << 20)
+        assert us is not None and math.isfinite(us) and 0.5 < us < 5000.0
+    ids = w.ids
+    # a kernel no family implements costs infinity (None)
+    assert w.graph.profile([ids["var"], ids["ve"], ids["r"], ids["Xh"], ids["Yg"], ids["Y"], ids["H0"]],
+                           [ids["H0"]], warmup=1, reps=1) is None
