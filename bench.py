@@ -91,7 +91,7 @@ def traffic_from_profiles(kernel_name, source_hash):
         return None
     try:
         data = json.load(open(path))
-        rec = data["kernels"].get(kernel_name)
+        rec = data["kernels"].get(kernel_name)  # "<workload>/<kernel name>"
         if not rec or rec.get("source_hash") != source_hash:
             return None
         return rec["hbm_bytes_per_launch"]
@@ -121,11 +121,14 @@ def main():
     stream = torch.cuda.current_stream()
 
     if args.calib_copy_mib:
+        # A plain streaming kernel of known traffic for the byte counters:
+        # dst = src + 1 reads and writes exactly n bytes each (uint8).
         n = args.calib_copy_mib << 20
-        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
+        torch.cuda.synchronize()
         for _ in range(3):
-            dst.copy_(src)
+            torch.add(src, 1, out=dst)
         torch.cuda.synchronize()
         del src, dst
 
@@ -176,7 +179,7 @@ def main():
         achieved = abytes / (dom_us * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK["hbm_GBs"], "unit": "GB/s",
                 "frac": round(achieved / PEAK["hbm_GBs"], 4)}
-    roof["traffic"] = traffic_from_profiles(name, src_hash)
+    roof["traffic"] = traffic_from_profiles(f"{args.workload}/{name}", src_hash)
     roof["kernel"] = name
     roof["kernel_us"] = round(dom_us, 3)
     roof["alg_bytes"] = abytes

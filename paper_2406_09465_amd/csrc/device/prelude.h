@@ -12,9 +12,24 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
 struct KArgs {
   void* p[KORCH_NARGS];
 };
+
+// Half-precision MFMA B-operand fragment from an LDS tile stored [k][n] (n
+// contiguous, row pitch `pitch` elements).  Each lane passes the address of
+// row k0 + (lane%16)/4, column n0 + 4*(lane%4); the transposing read returns
+// to lane i of every 16-lane group the 4 elements (k0..k0+3, n0 + i); a second
+// read 4 rows below completes the 8 consecutive k of the fragment.
+__device__ __forceinline__ s16x8 lds_tr_k8(const void* p, int pitch) {
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+  s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)((const short*)p + 4 * pitch));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
 
 // ---- scalar conversions ----------------------------------------------------
 __device__ __forceinline__ float tof(float x) { return x; }

@@ -9,6 +9,8 @@
 // before the single store (epilogue).  Several products that share their left
 // operand may run as one kernel, their right operands side by side in the tile.
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 
 #include "families.h"
 #include "gemm_common.h"
@@ -250,6 +252,22 @@ void choose_tiles(GemmSpec& sp, bool split) {
     }
   }
   if (sp.BM / sp.WM < 16) sp.WM = std::max(1, sp.BM / 16);
+  sp.NT = 256;
+  // Explicit tile override "BM,BN,BK,WM,WN" (tile-configuration sweeps of the
+  // profiler); ignored unless it is consistent.
+  if (const char* e = getenv("KORCH_GEMM_CFG")) {
+    int bm, bn, bk, wm, wn;
+    if (!split && sscanf(e, "%d,%d,%d,%d,%d", &bm, &bn, &bk, &wm, &wn) == 5 && (wm * wn == 4 || wm * wn == 8) &&
+        bm % (16 * wm) == 0 && bn % (16 * wn) == 0 && bk % sp.kstep == 0 && bk >= sp.kstep &&
+        (sp.mms.size() == 1 || bn >= sp.Ntot)) {
+      sp.BM = bm;
+      sp.BN = bn;
+      sp.BK = bk;
+      sp.WM = wm;
+      sp.WN = wn;
+      sp.NT = 64 * wm * wn;
+    }
+  }
   sp.WTM = sp.BM / sp.WM;
   sp.WTN = sp.BN / sp.WN;
   sp.FM = sp.WTM / 16;
@@ -258,6 +276,13 @@ void choose_tiles(GemmSpec& sp, bool split) {
   sp.VB = sp.VA;
   sp.BKP = sp.BK + (f32 ? 4 : 8);
   sp.LDC = sp.BN + 4;
+}
+
+void plan_operands(const KInfo& ki, GemmSpec& sp) {
+  int C = 16 / dtype_bytes(sp.mtype);
+  sp.b_kn = sp.Bs.size() == 1 && !ki.in.count(sp.Bs[0]) && sp.N % C == 0;
+  // row pitch: 32 extra bytes keep the four rows of one transposing read in distinct banks
+  sp.BNP = sp.BN + (sp.mtype == KORCH_F32 ? 4 : 16);
 }
 
 // Raw staging of an operand that is a plain materialized tensor (no prologue):
@@ -301,11 +326,11 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
     if (sp.K % V) return "";
     int kper = sp.BK / V;
     int nslots = rows * kper;
-    int per = (nslots + 255) / 256;
+    int per = (nslots + sp.NT - 1) / sp.NT;
     s << "  uint4 r" << X << "[2][" << per << "];\n";
     s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
-    s << "    const int sl = tid + i * 256;\n";
-    if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+    s << "    const int sl = tid + i * " << sp.NT << ";\n";
+    if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
     s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
     s << "    const i64 rg = " << base << " + rl, kg = k0 + kl;\n";
     s << "    if (rg < " << R << "LL && kg + " << V << " <= " << sp.K << "LL) r" << X << "[st][i] = *(const uint4*)(" << P
@@ -315,26 +340,55 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
       << sp.K << "LL + kg + e] : fromf<" << T << ">(0.0f);\n      __builtin_memcpy(&r" << X << "[st][i], t_, 16);\n    }\n";
     s << "  }\n  };\n";
     s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
-    s << "    const int sl = tid + i * 256;\n";
-    if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+    s << "    const int sl = tid + i * " << sp.NT << ";\n";
+    if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
     s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
     s << "    *(uint4*)(" << lds << " + buf * " << rows * sp.BKP << " + rl * " << sp.BKP << " + kl) = r" << X << "[st][i];\n";
     s << "  }\n  };\n";
     return s.str();
   }
   // B: [.., K, N] (or conv weights [KH, KW, Cin, Cout] = [K, N]), n contiguous
+  if (sp.b_kn) {
+    // copied unchanged into LDS as [k][n]; the MFMA reads transpose it
+    int C = 16 / dtype_bytes(sp.mtype);
+    int cpr = sp.BN / C;
+    int nslots = sp.BK * cpr;
+    int per = (nslots + sp.NT - 1) / sp.NT;
+    s << "  uint4 r" << X << "[2][" << per << "];\n";
+    s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
+      << "; ++i) {\n";
+    s << "    const int sl = tid + i * " << sp.NT << ";\n";
+    if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
+    s << "    const int kl = sl / " << cpr << ", nl = (sl % " << cpr << ") * " << C << ";\n";
+    s << "    const i64 kg = k0 + kl, ng = " << base << " + nl;\n";
+    s << "    if (kg < " << sp.K << "LL && ng + " << C << " <= " << sp.N << "LL) r" << X << "[st][i] = *(const uint4*)(" << P
+      << " + " << boff << " + kg * " << sp.N << "LL + ng);\n";
+    s << "    else {\n      " << T << " t_[" << C << "];\n#pragma unroll\n      for (int e = 0; e < " << C
+      << "; ++e) t_[e] = (kg < " << sp.K << "LL && ng + e < " << sp.N << "LL) ? " << P << "[" << boff << " + kg * "
+      << sp.N << "LL + ng + e] : fromf<" << T << ">(0.0f);\n      __builtin_memcpy(&r" << X << "[st][i], t_, 16);\n    }\n";
+    s << "  }\n  };\n";
+    s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
+      << "; ++i) {\n";
+    s << "    const int sl = tid + i * " << sp.NT << ";\n";
+    if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
+    s << "    const int kl = sl / " << cpr << ", nl = (sl % " << cpr << ") * " << C << ";\n";
+    s << "    *(uint4*)(" << lds << " + buf * " << sp.BK * sp.BNP << " + kl * " << sp.BNP << " + nl) = r" << X
+      << "[st][i];\n";
+    s << "  }\n  };\n";
+    return s.str();
+  }
   const int VT = 4;
   int KB = f32 ? 4 : 8;
   if (sp.N % VT) return "";
   int nper = rows / VT;
   int nblocks = (sp.BK / KB) * nper;
-  int per = (nblocks + 255) / 256;
+  int per = (nblocks + sp.NT - 1) / sp.NT;
   std::string T4 = "vec_t<4, " + T + ">";
   std::string TK = "vec_t<" + std::to_string(KB) + ", " + T + ">";
   s << "  " << T4 << " r" << X << "[2][" << per << "][" << KB << "];\n";
   s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
-  s << "    const int b_ = tid + i * 256;\n";
-  if (nblocks % 256) s << "    if (b_ >= " << nblocks << ") break;\n";
+  s << "    const int b_ = tid + i * " << sp.NT << ";\n";
+  if (nblocks % sp.NT) s << "    if (b_ >= " << nblocks << ") break;\n";
   s << "    const int kb = b_ / " << nper << ", nb = b_ % " << nper << ";\n";
   s << "    const i64 kg = k0 + kb * " << KB << ", ng = " << base << " + nb * " << VT << ";\n";
   s << "#pragma unroll\n    for (int kk = 0; kk < " << KB << "; ++kk) {\n";
@@ -345,8 +399,8 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
     << "[st][i][kk][j] = (k < " << sp.K << "LL && ng + j < " << sp.N << "LL) ? " << P << "[" << boff << " + k * " << sp.N
     << "LL + ng + j] : fromf<" << T << ">(0.0f);\n      }\n    }\n  }\n  };\n";
   s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
-  s << "    const int b_ = tid + i * 256;\n";
-  if (nblocks % 256) s << "    if (b_ >= " << nblocks << ") break;\n";
+  s << "    const int b_ = tid + i * " << sp.NT << ";\n";
+  if (nblocks % sp.NT) s << "    if (b_ >= " << nblocks << ") break;\n";
   s << "    const int kb = b_ / " << nper << ", nb = b_ % " << nper << ";\n";
   s << "#pragma unroll\n    for (int j = 0; j < " << VT << "; ++j) {\n      " << TK << " col;\n";
   s << "#pragma unroll\n      for (int kk = 0; kk < " << KB << "; ++kk) col[kk] = r" << X << "[st][i][kk][j];\n";
@@ -355,10 +409,134 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
   return s.str();
 }
 
+// Branch-free staging of plain materialized operands with buffer loads: each
+// 16-byte vector's byte offset is replaced by an out-of-range sentinel when the
+// vector lies outside the tensor, and the hardware then returns zeros.  With
+// no divergent control flow the loads of later k-tiles stay in flight while
+// the current tile is multiplied.  Handles the left operand ([.., M, K], k
+// contiguous), the implicit-GEMM convolution input, and the right operand
+// staged [k][n].  Returns "" when the operand does not qualify (needs
+// 16-byte-divisible rows and a tensor below 2 GiB).
+static std::string buffer_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot) {
+  const Graph& g = ki.g;
+  int node = isA ? sp.A : sp.Bs[0];
+  if (!isA && (sp.Bs.size() != 1 || !sp.b_kn)) return "";
+  if (ki.in.count(node)) return "";
+  int eb = dtype_bytes(sp.mtype);
+  int C = 16 / eb;  // elements per 16-byte vector
+  double bytes = (double)numel(g.nodes[node].shape) * eb;
+  if (bytes >= 2147483648.0) return "";
+  std::string T = ctype(sp.mtype);
+  std::string X = isA ? "A" : "B";
+  std::string lds = isA ? "As" : "Bs";
+  std::string P = "a.p[" + std::to_string(slot.at(node)) + "]";
+  std::string boff = "0";
+  if (!sp.conv) {
+    const Shape& sh = g.nodes[node].shape;
+    Shape ob(sp.OUT.begin(), sp.OUT.begin() + sp.nb);
+    Shape nbsh(sh.begin(), sh.end() - 2);
+    std::vector<Ix> zc;
+    for (int d = 0; d < sp.nb; ++d) zc.push_back(Ix::var("z" + std::to_string(d)));
+    auto bi = broadcast_index(nbsh, ob, zc);
+    auto st = strides_of(sh);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], st[d], 1));
+    boff = off.at();
+  } else if (sp.nb && isA) {
+    boff = "z0 * " + std::to_string(sp.H * sp.W * sp.Cin);
+  }
+  std::ostringstream s;
+  int rows, kper, nslots;
+  if (isA) {
+    if (sp.K % C) return "";
+    if (sp.conv && sp.Cin % C) return "";
+    kper = sp.BK / C;
+    rows = sp.BM;
+    nslots = rows * kper;
+  } else {
+    if (sp.N % C) return "";
+    kper = sp.BN / C;  // vectors per k row
+    rows = sp.BK;
+    nslots = rows * kper;
+  }
+  int per = (nslots + sp.NT - 1) / sp.NT;
+  s << "  const __amdgpu_buffer_rsrc_t rs" << X << " = __builtin_amdgcn_make_buffer_rsrc(" << P << ", 0, "
+    << (long long)bytes << ", 0x00020000);\n";
+  s << "  uint4 r" << X << "[2][" << per << "];\n";
+  // per-slot constants
+  s << "  int o" << X << "[" << per << "];  // element offset of the slot's vector at k-tile 0\n";
+  s << "  bool v" << X << "[" << per << "];  // slot lies inside the tile rows / columns\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+  s << "    const int sl = tid + i * " << sp.NT << ";\n";
+  if (isA) {
+    s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << C << ";\n";
+    s << "    const i64 rg = m0 + rl;\n";
+    if (sp.conv) {
+      s << "    o" << X << "[i] = (int)rg;  // output pixel\n";
+      s << "    v" << X << "[i] = sl < " << nslots << " && rg < " << sp.M << "LL;\n";
+    } else {
+      s << "    o" << X << "[i] = (int)(" << boff << " + rg * " << sp.K << "LL + kl);\n";
+      s << "    v" << X << "[i] = sl < " << nslots << " && rg < " << sp.M << "LL;\n";
+    }
+  } else {
+    s << "    const int kl = sl / " << kper << ", nl = (sl % " << kper << ") * " << C << ";\n";
+    s << "    const i64 ng = n0 + nl;\n";
+    s << "    o" << X << "[i] = (int)(" << boff << " + (i64)kl * " << sp.N << "LL + ng);\n";
+    s << "    v" << X << "[i] = sl < " << nslots << " && ng < " << sp.N << "LL;\n";
+  }
+  s << "  }\n";
+  s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
+    << "; ++i) {\n";
+  s << "    const int sl = tid + i * " << sp.NT << ";\n";
+  if (isA) {
+    s << "    const int kl = (sl % " << kper << ") * " << C << ";\n";
+    s << "    const int kg = (int)k0 + kl;\n";
+    if (sp.conv) {
+      s << "    const int p_ = o" << X << "[i];\n";
+      s << "    const int oy = p_ / " << sp.Wo << ", ox = p_ % " << sp.Wo << ";\n";
+      s << "    const int tap = kg / " << sp.Cin << ", ci = kg % " << sp.Cin << ";\n";
+      s << "    const int iy = oy * " << sp.stride << " + tap / " << sp.KW << " - " << sp.pad << ";\n";
+      s << "    const int ix = ox * " << sp.stride << " + tap % " << sp.KW << " - " << sp.pad << ";\n";
+      s << "    const bool ok = v" << X << "[i] && kg < " << sp.K << " && iy >= 0 && iy < " << sp.H << " && ix >= 0 && ix < "
+        << sp.W << ";\n";
+      s << "    const int e_ = (int)(" << boff << ") + (iy * " << sp.W << " + ix) * " << sp.Cin << " + ci;\n";
+    } else {
+      s << "    const bool ok = v" << X << "[i] && kg < " << sp.K << ";\n";
+      s << "    const int e_ = o" << X << "[i] + (int)k0;\n";
+    }
+  } else {
+    s << "    const int kl = sl / " << kper << ";\n";
+    s << "    const bool ok = v" << X << "[i] && (int)k0 + kl < " << sp.K << ";\n";
+    s << "    const int e_ = o" << X << "[i] + (int)k0 * " << sp.N << ";\n";
+  }
+  s << "    const unsigned off = ok ? (unsigned)e_ * " << eb << "u : 0x80000000u;\n";
+  s << "    r" << X << "[st][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs" << X
+    << ", off, 0, 0));\n";
+  s << "  }\n  };\n";
+  s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
+    << "; ++i) {\n";
+  s << "    const int sl = tid + i * " << sp.NT << ";\n";
+  if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
+  if (isA) {
+    s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << C << ";\n";
+    s << "    *(uint4*)(" << lds << " + buf * " << sp.BM * sp.BKP << " + rl * " << sp.BKP << " + kl) = r" << X << "[st][i];\n";
+  } else {
+    s << "    const int kl = sl / " << kper << ", nl = (sl % " << kper << ") * " << C << ";\n";
+    s << "    *(uint4*)(" << lds << " + buf * " << sp.BK * sp.BNP << " + kl * " << sp.BNP << " + nl) = r" << X
+      << "[st][i];\n";
+  }
+  s << "  }\n  };\n";
+  return s.str();
+}
+
 // Emits a lambda `fetchX(k0)` that evaluates the operand (with its prologue)
 // for this thread's slots of a BM x BK (A) or BN x BK (B) tile into registers,
 // and `stashX(buf)` that converts and writes them to LDS in [row][k] layout.
 std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot) {
+  {
+    std::string buf = buffer_loader(ki, sp, isA, slot);
+    if (!buf.empty()) return buf;
+  }
   {
     std::string raw = raw_loader(ki, sp, isA, slot);
     if (!raw.empty()) return raw;
@@ -367,7 +545,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   int V = isA ? sp.VA : sp.VB;
   int rows = isA ? sp.BM : sp.BN;
   int nslots = rows * sp.BK / V;
-  int per = (nslots + 255) / 256;
+  int per = (nslots + sp.NT - 1) / sp.NT;
   std::string X = isA ? "A" : "B";
   std::string T = ctype(sp.mtype);
   std::string lds = isA ? "As" : "Bs";
@@ -451,8 +629,8 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   s << "  float r" << X << "[2][" << per << "][" << V << "];\n";
   s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
-  s << "    const int sl = tid + i * 256;\n";
-  if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+  s << "    const int sl = tid + i * " << sp.NT << ";\n";
+  if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
   if (axis_k)
     s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
   else
@@ -510,9 +688,15 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
                                        std::to_string(sp.K) + "LL)"
                                  : "(rg + " + std::to_string(V) + " <= " + lim + "LL && kg < " +
                                        std::to_string(sp.K) + "LL)";
-      s << "      if " << fastc << " {\n"
-        << emit_operand(nodes[j], axis_k, false, rowv, "kg", lim + "LL", lo) << "      } else {\n"
-        << emit_operand(nodes[j], axis_k, true, rowv, "kg", lim + "LL", lo) << "      }\n    }\n";
+      // a tile-aligned problem never needs the guarded per-element path
+      int64_t R = isA ? sp.M : sp.N;
+      bool aligned = nodes.size() == 1 && R % rows == 0 && sp.K % sp.BK == 0;
+      if (aligned)
+        s << "      {\n" << emit_operand(nodes[j], axis_k, false, rowv, "kg", lim + "LL", lo) << "      }\n    }\n";
+      else
+        s << "      if " << fastc << " {\n"
+          << emit_operand(nodes[j], axis_k, false, rowv, "kg", lim + "LL", lo) << "      } else {\n"
+          << emit_operand(nodes[j], axis_k, true, rowv, "kg", lim + "LL", lo) << "      }\n    }\n";
     }
     if (nodes.size() > 1)
       s << "    else {\n#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) dst[e] = 0.0f;\n    }\n";
@@ -521,8 +705,8 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   // stash: fp32 registers -> LDS [row][k] of the MFMA operand type
   s << "  auto stash" << X << " = [&](const int buf, const int st) {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
-  s << "    const int sl = tid + i * 256;\n";
-  if (nslots % 256) s << "    if (sl >= " << nslots << ") break;\n";
+  s << "    const int sl = tid + i * " << sp.NT << ";\n";
+  if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
   if (axis_k) {
     s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
     s << "    stv<" << V << ">(" << lds << " + buf * " << rows * sp.BKP << " + rl * " << sp.BKP << " + kl, r" << X
@@ -546,14 +730,19 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
     << "; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
   s << "  auto compute = [&](const int buf) {\n";
   s << "    const " << T << "* Ab = As + buf * " << sp.BM * sp.BKP << ";\n";
-  s << "    const " << T << "* Bb = Bs + buf * " << sp.BN * sp.BKP << ";\n";
+  int bbuf = sp.b_kn ? sp.BK * sp.BNP : sp.BN * sp.BKP;
+  s << "    const " << T << "* Bb = Bs + buf * " << bbuf << ";\n";
   s << "#pragma unroll\n    for (int kk = 0; kk < " << sp.BK / sp.kstep << "; ++kk) {\n";
   if (f32) {
     s << "      float af[" << sp.FM << "], bf[" << sp.FN << "];\n";
     s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i) af[i] = Ab[(wm * " << sp.WTM
       << " + i * 16 + (l & 15)) * " << sp.BKP << " + kk * 4 + (l >> 4)];\n";
-    s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = Bb[(wn * " << sp.WTN
-      << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 4 + (l >> 4)];\n";
+    if (sp.b_kn)
+      s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = Bb[(kk * 4 + (l >> 4)) * " << sp.BNP
+        << " + wn * " << sp.WTN << " + j * 16 + (l & 15)];\n";
+    else
+      s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = Bb[(wn * " << sp.WTN
+        << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 4 + (l >> 4)];\n";
     s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n      for (int j = 0; j < "
       << sp.FN << "; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i], bf[j], acc[i][j], 0, 0, 0);\n";
   } else {
@@ -563,8 +752,13 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
     s << "      " << V8 << " af[" << sp.FM << "], bf[" << sp.FN << "];\n";
     s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i) af[i] = *(const " << V8 << "*)(Ab + (wm * "
       << sp.WTM << " + i * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
-    s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = *(const " << V8 << "*)(Bb + (wn * "
-      << sp.WTN << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
+    if (sp.b_kn)
+      s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = __builtin_bit_cast(" << V8
+        << ", lds_tr_k8(Bb + (kk * 32 + (l >> 4) * 8 + ((l & 15) >> 2)) * " << sp.BNP << " + wn * " << sp.WTN
+        << " + j * 16 + 4 * (l & 3), " << sp.BNP << "));\n";
+    else
+      s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = *(const " << V8 << "*)(Bb + (wn * "
+        << sp.WTN << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
     s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n      for (int j = 0; j < "
       << sp.FN << "; ++j) acc[i][j] = " << fn << "(af[i], bf[j], acc[i][j], 0, 0, 0);\n";
   }
@@ -574,7 +768,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
   // earlier) and the loads of tile t+2 are in flight into stage t%2.  The loop
   // is unrolled by two so every register stage index is a constant.
   int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
-  std::string wguard = nw < 4 ? "if (wave < " + std::to_string(nw) + ") " : "";
+  std::string wguard = nw < sp.NT / 64 ? "if (wave < " + std::to_string(nw) + ") " : "";
   auto ktile = [&](const std::string& t) { return "(i64)(" + t + ") * " + std::to_string(sp.BK); };
   auto step = [&](int b, const std::string& kt) {
     std::ostringstream o;
@@ -605,7 +799,8 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
 }
 
 size_t gemm_smem_bytes(const GemmSpec& sp) {
-  size_t ab = (size_t)2 * (sp.BM + sp.BN) * sp.BKP * dtype_bytes(sp.mtype);
+  size_t bbuf = sp.b_kn ? (size_t)sp.BK * sp.BNP : (size_t)sp.BN * sp.BKP;
+  size_t ab = (size_t)2 * ((size_t)sp.BM * sp.BKP + bbuf) * dtype_bytes(sp.mtype);
   size_t c = (size_t)sp.BM * sp.LDC * 4;
   return std::max(ab, c);
 }
@@ -682,7 +877,7 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
     }
   }
   std::ostringstream s;
-  s << "  for (int s_ = tid; s_ < " << sp.BM * (cols / VE) << "; s_ += 256) {\n";
+  s << "  for (int s_ = tid; s_ < " << sp.BM * (cols / VE) << "; s_ += " << sp.NT << ") {\n";
   s << "    const int ml = s_ / " << cols / VE << ", nl = (s_ % " << cols / VE << ") * " << VE << ";\n";
   s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
   s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n";
@@ -710,6 +905,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   std::string why;
   if (!analyze_gemm(ki, sp, &why, false)) fail(KORCH_E_UNSUPPORTED, why);
   choose_tiles(sp, false);
+  plan_operands(ki, sp);
   GenKernel gk;
   gk.family = sp.conv ? KORCH_FAM_CONV : KORCH_FAM_GEMM;
   gk.name = kernel_name(index, sp.conv ? "conv" : "gemm");
@@ -720,10 +916,22 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   int64_t KT = (sp.K + sp.BK - 1) / sp.BK;
   std::ostringstream s;
   s << source_header((int)gk.args.size());
-  s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
+  s << "extern \"C\" __global__ void __launch_bounds__(" << sp.NT << ") " << gk.name << "(KArgs a) {\n";
   s << gemm_prologue_common(sp);
-  s << "  const i64 n0 = (i64)blockIdx.x * " << sp.BN << ", m0 = (i64)blockIdx.y * " << sp.BM << ";\n";
-  s << "  i64 q_ = blockIdx.z;\n";
+  // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
+  // L2.  Renumber them so every XCD owns a contiguous range of tiles, and order
+  // tiles in groups of GM row-tiles so the tiles running together on one XCD
+  // share their A row-panels and B column-panels in that XCD's L2.
+  int64_t total = ntn * ntm * sp.batch;
+  int64_t GM = std::min<int64_t>(8, ntm);
+  s << "  const int wg = blockIdx.x, xcd = wg % 8, jx = wg / 8;\n";
+  s << "  const int q = xcd * " << total / 8 << " + (xcd < " << total % 8 << " ? xcd : " << total % 8 << ") + jx;\n";
+  s << "  const int bz_ = q / " << ntm * ntn << ", r_ = q % " << ntm * ntn << ";\n";
+  s << "  const int grp = r_ / " << GM * ntn << ", first = grp * " << GM << ";\n";
+  s << "  const int gs = " << ntm << " - first < " << GM << " ? " << ntm << " - first : " << GM << ";\n";
+  s << "  const int tm = first + (r_ % " << GM * ntn << ") % gs, tn = (r_ % " << GM * ntn << ") / gs;\n";
+  s << "  const i64 n0 = (i64)tn * " << sp.BN << ", m0 = (i64)tm * " << sp.BM << ";\n";
+  s << "  i64 q_ = bz_;\n";
   for (int d = sp.nb - 1; d >= 0; --d)
     s << "  const i64 z" << d << " = q_ % " << sp.OUT[d] << "LL; q_ /= " << sp.OUT[d] << "LL;\n";
   s << "  const int kt0 = 0, kt1 = " << KT << ";\n";
@@ -733,10 +941,10 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   s << gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(sp.LDC));
   s << "}\n";
   gk.source = s.str();
-  gk.grid[0] = (int)ntn;
-  gk.grid[1] = (int)ntm;
-  gk.grid[2] = (int)sp.batch;
+  gk.grid[0] = (int)total;
+  gk.block[0] = sp.NT;
   gk.lds_bytes = (int)gemm_smem_bytes(sp);
+  if (gk.lds_bytes > 160 * 1024) fail(KORCH_E_UNSUPPORTED, "gemm: tiles need more than 160 KiB of LDS");
   ki.fill_cost(gk);
   return gk;
 }

@@ -237,6 +237,7 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   std::string why;
   if (!analyze_splitk(ki, sp, si, &why)) fail(KORCH_E_UNSUPPORTED, why);
   choose_tiles(sp, true);
+  plan_operands(ki, sp);
   GenKernel gk;
   gk.family = KORCH_FAM_SPLITK;
   gk.name = kernel_name(index, "splitk");

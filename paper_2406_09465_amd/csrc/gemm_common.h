@@ -30,7 +30,16 @@ struct GemmSpec {
   // tiling
   int BM = 128, BN = 128, BK = 32, BKP = 40, kstep = 32, WM = 2, WN = 2, WTM = 64, WTN = 64, FM = 4, FN = 4;
   int VA = 8, VB = 8, LDC = 132;
+  int NT = 256;  // threads per workgroup (64 per wave)
+  // Right operand staged raw in LDS as [k][n] (n contiguous, pitch BNP) and
+  // read into MFMA fragments with transposing LDS reads (half precision) or
+  // plain reads (fp32); otherwise staged as [n][k] with pitch BKP.
+  bool b_kn = false;
+  int BNP = 0;
 };
+
+// Decides operand staging layouts once the tiles are chosen.
+void plan_operands(const KInfo& ki, GemmSpec& sp);
 
 bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_reduce);
 void choose_tiles(GemmSpec& sp, bool split);

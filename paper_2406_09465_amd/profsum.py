@@ -1,0 +1,111 @@
+"""Summarizes rocprofv3 outputs into the short text files kept under profiles/.
+
+  python -m paper_2406_09465_amd.profsum stats <rocprof dir> <out.md> --cmd "<command>"
+      kernel-trace statistics (*_kernel_stats.csv) as a markdown table.
+
+  python -m paper_2406_09465_amd.profsum pmc --workload mlp --fetch <dir> --write <dir>
+         --calib-mib 256 --out profiles/pmc_traffic.json --cmd-fetch "..." --cmd-write "..."
+      FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of every kernel of the
+      workload's fused plan, each scaled by the ratio between the known bytes of
+      a plain streaming kernel (dst = src + 1 over calib-mib MiB, uint8) and
+      what the same counter reads for it; records the generated source's hash
+      so a stale figure is never reported for a changed kernel.
+"""
+
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import statistics
+
+
+def _rows(d, pattern):
+    out = []
+    for f in glob.glob(os.path.join(d, "**", pattern), recursive=True):
+        out.extend(csv.DictReader(open(f)))
+    return out
+
+
+def stats(args):
+    rows = _rows(args.dir, "*_kernel_stats.csv")
+    lines = [f"# {args.title or os.path.basename(args.out)}", "", "Command:", "", "```", args.cmd, "```", "",
+             "| kernel | calls | average (us) | min (us) | max (us) | share |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['Name']} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                     f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f}% |")
+    open(args.out, "w").write("\n".join(lines) + "\n")
+
+
+def _counter(d, name):
+    per = {}
+    for r in _rows(d, "*counter_collection.csv"):
+        if r.get("Counter_Name") != name:
+            continue
+        per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return {k: statistics.median(v) for k, v in per.items()}
+
+
+def pmc(args):
+    from . import graphs
+    fetch = _counter(args.fetch, "FETCH_SIZE")
+    write = _counter(args.write, "WRITE_SIZE")
+    calib = [k for k in fetch if "elementwise" in k and fetch[k] > 1000]
+    if not calib:
+        raise SystemExit("no calibration kernel found")
+    ck = max(calib, key=lambda k: fetch[k])
+    known_kib = args.calib_mib * 1024.0
+    f_fetch = known_kib / fetch[ck]
+    f_write = known_kib / write[ck]
+    w = graphs.build(args.workload)
+    p = w.plan(args.plan)
+    p.compile()
+    res = {"workload": args.workload, "plan": args.plan, "calibration_kernel": ck[:80],
+           "fetch_factor": f_fetch, "write_factor": f_write, "cmd_fetch": args.cmd_fetch, "cmd_write": args.cmd_write,
+           "kernels": {}}
+    old = {}
+    if os.path.exists(args.out):
+        old = json.load(open(args.out)).get("kernels", {})
+    for k in range(p.num_kernels()):
+        name = p.kernel_name(k)
+        if name not in fetch or name not in write:
+            continue
+        fam, ab, af = p.kernel_info(k)
+        h = hashlib.sha256(p.kernel_source(k).encode()).hexdigest()[:16]
+        hbm = (fetch[name] * f_fetch + write[name] * f_write) * 1024.0
+        res["kernels"][f"{args.workload}/{name}"] = {
+            "workload": args.workload, "family": fam, "source_hash": h, "fetch_kib": fetch[name],
+            "write_kib": write[name], "hbm_bytes_per_launch": hbm, "alg_bytes": ab,
+            "traffic_over_alg": hbm / ab if ab else None}
+    for k, v in old.items():  # keep other workloads' records
+        if v.get("workload") != args.workload:
+            res["kernels"].setdefault(k, v)
+    json.dump(res, open(args.out, "w"), indent=1)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="mode", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("dir")
+    s.add_argument("out")
+    s.add_argument("--cmd", required=True)
+    s.add_argument("--title", default="")
+    p = sub.add_parser("pmc")
+    p.add_argument("--workload", default="mlp")
+    p.add_argument("--plan", default="fused")
+    p.add_argument("--fetch", required=True)
+    p.add_argument("--write", required=True)
+    p.add_argument("--calib-mib", type=int, default=256)
+    p.add_argument("--out", required=True)
+    p.add_argument("--cmd-fetch", default="")
+    p.add_argument("--cmd-write", default="")
+    a = ap.parse_args()
+    stats(a) if a.mode == "stats" else pmc(a)
+
+
+if __name__ == "__main__":
+    main()
