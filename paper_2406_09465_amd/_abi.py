@@ -19,6 +19,14 @@ os.environ.setdefault("KORCH_CACHE_DIR", os.path.join(PKG, "_kcache"))
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2406_09465_amd.build`")
+# A process must hold one HIP runtime.  PyTorch ships its own copy; loading it
+# first lets the library's HIP dependencies resolve to that copy by soname.
+# Loaded the other way round, the process would hold two HIP runtimes and the
+# second to start would see no device.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
 lib = C.CDLL(LIB_PATH)
 
 MAX_RANK = 8

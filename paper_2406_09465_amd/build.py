@@ -70,7 +70,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
                 print(r.stdout, r.stderr, file=sys.stderr)
     objs = [c[-1] for c in jobs_list]
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, f"-L{ROCM}/lib", "-lhiprtc",
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, f"-L{ROCM}/lib", "-ldl",
           f"-Wl,-rpath,{ROCM}/lib", "-o", tmp])
     os.replace(tmp, LIB)
     return LIB

@@ -84,6 +84,19 @@ def pmc(args):
         if v.get("workload") != args.workload:
             res["kernels"].setdefault(k, v)
     json.dump(res, open(args.out, "w"), indent=1)
+    md = os.path.splitext(args.out)[0] + ".md"
+    lines = ["# HBM traffic per launch (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
+             f"Calibration: `{res['calibration_kernel'][:60]}` over {args.calib_mib} MiB (uint8, dst = src + 1) reads "
+             f"FETCH_SIZE x {f_fetch:.3f} and WRITE_SIZE x {f_write:.3f} of the known bytes; every figure below "
+             "is scaled by those factors.", "", "Commands (run once per workload `<w>`):", "", "```",
+             args.cmd_fetch, args.cmd_write, "```", "",
+             "| kernel | family | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes | algorithmic bytes | ratio | source hash |",
+             "|---|---|---|---|---|---|---|---|"]
+    for k, v in sorted(res["kernels"].items()):
+        lines.append(f"| {k} | {v['family']} | {v['fetch_kib']:.0f} | {v['write_kib']:.0f} | "
+                     f"{v['hbm_bytes_per_launch']:.0f} | {v['alg_bytes']:.0f} | {v['traffic_over_alg']:.3f} | "
+                     f"{v['source_hash']} |")
+    open(md, "w").write("\n".join(lines) + "\n")
 
 
 def main():
