@@ -99,6 +99,14 @@ struct Emitter {
   int guard_depth = 0;
   int n_gather = 0, n_vector = 0, n_uniform = 0;
   std::vector<std::map<std::string, std::string>> memo{1};
+  // Staged loads: a hoisted (uniform or vector) load becomes an assignment into
+  // an array of the tensor's own type, declared in `stage_decl` with
+  // [stages][slots] extents and indexed by the generated variables `st` and
+  // `i`; the value is read back (converted to float) where it is used.  The
+  // loads can then be issued one pipeline stage ahead of the arithmetic.
+  bool staged = false;
+  int stages = 2, slots = 1;
+  std::ostringstream stage_decl;
 
   Emitter(const Graph& gg) : g(gg) {}
   std::string value(int node, const std::vector<Ix>& idx);

@@ -312,6 +312,20 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
   std::string T = ctype(n.dtype);
   std::string P = "((const " + T + "*)a.p[" + std::to_string(it->second) + "])";
   bool hoist = guard_depth == 0 && !force_gather;
+  if (staged && hoist && off.affine && off.c == 0) {
+    ++n_uniform;
+    std::string v = fresh("su");
+    stage_decl << "  " << T << " " << v << "[" << stages << "][" << slots << "];\n";
+    pre << "    " << v << "[st][i] = " << P << "[" << off.b << "];\n";
+    return "tof(" + v + "[st][i])";
+  }
+  if (staged && hoist && off.affine && off.c == 1 && vec > 1 && off.al % vec == 0) {
+    ++n_vector;
+    std::string v = fresh("sx");
+    stage_decl << "  vec_t<" << vec << ", " << T << "> " << v << "[" << stages << "][" << slots << "];\n";
+    pre << "    " << v << "[st][i] = *(const vec_t<" << vec << ", " << T << ">*)(" << P << " + " << off.b << ");\n";
+    return "tof(" + v + "[st][i][e])";
+  }
   if (hoist && off.affine && off.c == 0) {
     ++n_uniform;
     std::string v = fresh("u");

@@ -339,7 +339,7 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
       << "; ++e) t_[e] = (rg < " << R << "LL && kg + e < " << sp.K << "LL) ? " << P << "[" << boff << " + rg * "
       << sp.K << "LL + kg + e] : fromf<" << T << ">(0.0f);\n      __builtin_memcpy(&r" << X << "[st][i], t_, 16);\n    }\n";
     s << "  }\n  };\n";
-    s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+    s << "  auto stash" << X << " = [&](const int buf, const int st, const i64 k0_) {\n  (void)k0_;\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
     s << "    const int sl = tid + i * " << sp.NT << ";\n";
     if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
     s << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
@@ -367,7 +367,7 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
       << "; ++e) t_[e] = (kg < " << sp.K << "LL && ng + e < " << sp.N << "LL) ? " << P << "[" << boff << " + kg * "
       << sp.N << "LL + ng + e] : fromf<" << T << ">(0.0f);\n      __builtin_memcpy(&r" << X << "[st][i], t_, 16);\n    }\n";
     s << "  }\n  };\n";
-    s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
+    s << "  auto stash" << X << " = [&](const int buf, const int st, const i64 k0_) {\n  (void)k0_;\n#pragma unroll\n  for (int i = 0; i < " << per
       << "; ++i) {\n";
     s << "    const int sl = tid + i * " << sp.NT << ";\n";
     if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
@@ -398,7 +398,7 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
   s << "      else {\n#pragma unroll\n        for (int j = 0; j < " << VT << "; ++j) r" << X
     << "[st][i][kk][j] = (k < " << sp.K << "LL && ng + j < " << sp.N << "LL) ? " << P << "[" << boff << " + k * " << sp.N
     << "LL + ng + j] : fromf<" << T << ">(0.0f);\n      }\n    }\n  }\n  };\n";
-  s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
+  s << "  auto stash" << X << " = [&](const int buf, const int st, const i64 k0_) {\n  (void)k0_;\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
   s << "    const int b_ = tid + i * " << sp.NT << ";\n";
   if (nblocks % sp.NT) s << "    if (b_ >= " << nblocks << ") break;\n";
   s << "    const int kb = b_ / " << nper << ", nb = b_ % " << nper << ";\n";
@@ -513,7 +513,7 @@ static std::string buffer_loader(const KInfo& ki, const GemmSpec& sp, bool isA, 
   s << "    r" << X << "[st][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs" << X
     << ", off, 0, 0));\n";
   s << "  }\n  };\n";
-  s << "  auto stash" << X << " = [&](const int buf, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
+  s << "  auto stash" << X << " = [&](const int buf, const int st, const i64 k0_) {\n  (void)k0_;\n#pragma unroll\n  for (int i = 0; i < " << per
     << "; ++i) {\n";
   s << "    const int sl = tid + i * " << sp.NT << ";\n";
   if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
@@ -624,6 +624,74 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
     axis_k = isA ? true : false;  // X: channels contiguous; W as [K, N]: N contiguous
   }
   int kper = axis_k ? sp.BK / V : sp.BK;
+  // Staged prologue: fetchX only issues the loads of the operand's inputs
+  // (uniform and vector loads, into per-stage registers of their own type, at
+  // indices clamped into the tensors); stashX evaluates the prologue once the
+  // data has arrived, zeroes elements outside the problem and writes LDS.  The
+  // loads of a tile then stay in flight while earlier tiles are multiplied.
+  if (!sp.conv && nodes.size() == 1) {
+    const int64_t R = isA ? sp.M : sp.N;
+    if (axis_k ? sp.K % V == 0 : R % V == 0) {
+      Emitter em(g);
+      em.inset = sp.pro;
+      em.argslot = slot;
+      em.vec = V;
+      em.staged = true;
+      em.stages = 2;
+      em.slots = per;
+      em.tmp = isA ? 0 : 500;  // keep the two operands' register names apart
+      std::vector<Ix> idx = batch_idx(nodes[0]);
+      Ix r = axis_k ? Ix::var("rg", 0, 1) : Ix::var("rg", 1, V);
+      Ix k = axis_k ? Ix::var("kg", 1, V) : Ix::var("kg", 0, 1);
+      if (isA) {
+        idx.push_back(r);
+        idx.push_back(k);
+      } else {
+        idx.push_back(k);
+        idx.push_back(r);
+      }
+      std::string val = em.value(nodes[0], idx);
+      if (em.n_gather == 0) {
+        std::string base = isA ? "m0" : "n0";
+        auto slot_coords = [&]() {
+          std::ostringstream o;
+          o << "    const int sl = tid + i * " << sp.NT << ";\n";
+          if (nslots % sp.NT) o << "    if (sl >= " << nslots << ") break;\n";
+          if (axis_k)
+            o << "    const int rl = sl / " << kper << ", kl = (sl % " << kper << ") * " << V << ";\n";
+          else
+            o << "    const int kl = sl / " << rows / V << ", rl = (sl % " << rows / V << ") * " << V << ";\n";
+          return o.str();
+        };
+        s << em.stage_decl.str();
+        s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
+          << "; ++i) {\n";
+        s << slot_coords();
+        s << "    const i64 rg = " << base << " + rl < " << R - (axis_k ? 1 : V) << "LL ? " << base << " + rl : "
+          << R - (axis_k ? 1 : V) << "LL;\n";
+        s << "    const i64 kg = k0 + kl < " << sp.K - (axis_k ? V : 1) << "LL ? k0 + kl : " << sp.K - (axis_k ? V : 1)
+          << "LL;\n";
+        s << em.pre.str() << "  }\n  };\n";
+        s << "  auto stash" << X << " = [&](const int buf, const int st, const i64 k0) {\n#pragma unroll\n  for (int i = 0; i < "
+          << per << "; ++i) {\n";
+        s << slot_coords();
+        s << "    const i64 rg = " << base << " + rl, kg = k0 + kl;\n";
+        s << "    float dst[" << V << "];\n";
+        std::string cond = axis_k ? "(rg < " + std::to_string(R) + "LL && kg + e < " + std::to_string(sp.K) + "LL)"
+                                  : "(rg + e < " + std::to_string(R) + "LL && kg < " + std::to_string(sp.K) + "LL)";
+        s << "#pragma unroll\n    for (int e = 0; e < " << V << "; ++e) {\n" << em.body.str() << "      dst[e] = " << cond
+          << " ? (float)(" << val << ") : 0.0f;\n    }\n";
+        if (axis_k) {
+          s << "    stv<" << V << ">(" << lds << " + buf * " << rows * sp.BKP << " + rl * " << sp.BKP << " + kl, dst);\n";
+        } else {
+          s << "#pragma unroll\n    for (int e = 0; e < " << V << "; ++e) " << lds << "[buf * " << rows * sp.BKP
+            << " + (rl + e) * " << sp.BKP << " + kl] = fromf<" << T << ">(dst[e]);\n";
+        }
+        s << "  }\n  };\n";
+        return s.str();
+      }
+    }
+  }
   // slot s -> (row, k): axis_k: row = s / (BK/V), kk = (s % (BK/V)) * V
   //                     axis_row: kk = s / (rows/V), row = (s % (rows/V)) * V
   s << "  float r" << X << "[2][" << per << "][" << V << "];\n";
@@ -703,7 +771,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   }
   s << "  }\n  };\n";
   // stash: fp32 registers -> LDS [row][k] of the MFMA operand type
-  s << "  auto stash" << X << " = [&](const int buf, const int st) {\n";
+  s << "  auto stash" << X << " = [&](const int buf, const int st, const i64 k0_) {\n  (void)k0_;\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
   s << "    const int sl = tid + i * " << sp.NT << ";\n";
   if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
@@ -721,7 +789,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
 }
 
 // The MFMA main loop over k-tiles [kt0, kt1) of the contraction.
-std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
+std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t kconst) {
   std::ostringstream s;
   bool f32 = sp.mtype == KORCH_F32;
   std::string T = ctype(sp.mtype);
@@ -765,30 +833,40 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook) {
   s << "    }\n  };\n";
   // Two-deep pipeline: while tile t is multiplied from LDS buffer t%2, the
   // registers of stage (t+1)%2 already hold tile t+1 (loaded one iteration
-  // earlier) and the loads of tile t+2 are in flight into stage t%2.  The loop
-  // is unrolled by two so every register stage index is a constant.
+  // earlier) and the loads of tile t+2 are in flight into stage t%2.  Fetches
+  // are unconditional (tile indices clamped to the last tile) so the compiler
+  // counts outstanding loads exactly; with a compile-time tile count the loop
+  // is unrolled completely.
   int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
   std::string wguard = nw < sp.NT / 64 ? "if (wave < " + std::to_string(nw) + ") " : "";
-  auto ktile = [&](const std::string& t) { return "(i64)(" + t + ") * " + std::to_string(sp.BK); };
-  auto step = [&](int b, const std::string& kt) {
+  auto clampk = [&](const std::string& t) {
+    return "(i64)((" + t + ") < kt1 ? (" + t + ") : kt1 - 1) * " + std::to_string(sp.BK);
+  };
+  auto step = [&](const std::string& b, const std::string& kt) {
     std::ostringstream o;
-    o << "    if (" << kt << " + 2 < kt1) { fetchA(" << ktile(kt + " + 2") << ", " << b << "); fetchB(" << ktile(kt + " + 2")
-      << ", " << b << "); }\n";
+    o << "    fetchA(" << clampk(kt + " + 2") << ", " << b << "); fetchB(" << clampk(kt + " + 2") << ", " << b << ");\n";
     o << "    " << wguard << "compute(" << b << ");\n";
-    if (!hook.empty()) o << "    {\n      const " << T << "* Ab = As + " << b * sp.BM * sp.BKP << ";\n" << hook << "    }\n";
-    o << "    if (" << kt << " + 1 < kt1) { stashA(" << 1 - b << ", " << 1 - b << "); stashB(" << 1 - b << ", " << 1 - b
-      << "); }\n";
+    if (!hook.empty()) o << "    {\n      const " << T << "* Ab = As + (" << b << ") * " << sp.BM * sp.BKP << ";\n" << hook << "    }\n";
+    o << "    stashA(1 - (" << b << "), 1 - (" << b << "), " << clampk(kt + " + 1") << "); stashB(1 - (" << b << "), 1 - ("
+      << b << "), " << clampk(kt + " + 1") << ");\n";
     o << "    __syncthreads();\n";
     return o.str();
   };
-  s << "  fetchA(" << ktile("kt0") << ", 0); fetchB(" << ktile("kt0") << ", 0);\n";
-  s << "  if (kt0 + 1 < kt1) { fetchA(" << ktile("kt0 + 1") << ", 1); fetchB(" << ktile("kt0 + 1") << ", 1); }\n";
-  s << "  stashA(0, 0); stashB(0, 0);\n  __syncthreads();\n";
-  s << "  for (int kt = kt0; kt < kt1; kt += 2) {\n";
-  s << step(0, "kt");
-  s << "    if (kt + 1 >= kt1) break;\n";
-  s << step(1, "(kt + 1)");
-  s << "  }\n";
+  s << "  fetchA(" << clampk("kt0") << ", 0); fetchB(" << clampk("kt0") << ", 0);\n";
+  s << "  fetchA(" << clampk("kt0 + 1") << ", 1); fetchB(" << clampk("kt0 + 1") << ", 1);\n";
+  s << "  stashA(0, 0, " << clampk("kt0") << "); stashB(0, 0, " << clampk("kt0") << ");\n  __syncthreads();\n";
+  if (kconst > 0 && kconst <= 128) {
+    s << "#pragma unroll\n  for (int kt = kt0; kt < kt0 + " << kconst << "; ++kt) {\n";
+    s << "    const int b_ = (kt - kt0) & 1;\n";
+    s << step("b_", "kt");
+    s << "  }\n";
+  } else {
+    s << "  for (int kt = kt0; kt < kt1; kt += 2) {\n";
+    s << step("0", "kt");
+    s << "    if (kt + 1 >= kt1) break;\n";
+    s << step("1", "(kt + 1)");
+    s << "  }\n";
+  }
   // accumulators -> LDS C tile (fp32)
   s << "  float* Cs = (float*)smem;\n";
   s << "  " << wguard << "{\n#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
@@ -937,7 +1015,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   s << "  const int kt0 = 0, kt1 = " << KT << ";\n";
   s << operand_loader(ki, sp, true, slot);
   s << operand_loader(ki, sp, false, slot);
-  s << mfma_mainloop(sp);
+  s << mfma_mainloop(sp, "", KT);
   s << gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(sp.LDC));
   s << "}\n";
   gk.source = s.str();

@@ -44,7 +44,9 @@ void plan_operands(const KInfo& ki, GemmSpec& sp);
 bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_reduce);
 void choose_tiles(GemmSpec& sp, bool split);
 std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot);
-std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "");
+// kconst: number of k-tiles when it is a compile-time constant (the loop is then
+// unrolled completely), else 0.
+std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "", int64_t kconst = 0);
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
                           const std::string& cs_row, const std::set<int>& skip = {});
 std::string gemm_prologue_common(const GemmSpec& sp);

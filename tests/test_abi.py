@@ -265,3 +265,12 @@ def test_unsupported_kernel_reports_infinite_cost():
     assert w.graph.family(prims, [ids["O"]]) == "none"
     p = K.Plan(w.graph, [([ids["KT"], ids["S0"], ids["S"]], [ids["S"]]), (prims, [ids["O"]])])
     assert code(p.compile) == -20
+
+
+def test_sampled_and_sized_plans_compile():
+    """Every plan that the GPU tests execute (workload plans at the test sizes and
+    the seeded random plans) generates kernels that hipRTC compiles for gfx950."""
+    from paper_2406_09465_amd import warm
+
+    failures = warm.warm_cache(prune_stale=False)
+    assert not failures, failures[:3]
