@@ -45,7 +45,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="mlp", choices=list(DESCR))
-    ap.add_argument("--plan", default="fused")
+    ap.add_argument("--plan", default="fused",
+                    help="fused | layered | unfused | korch (profile every candidate kernel and run the cheapest plan)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work for the oracle sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -115,7 +116,20 @@ def main():
 
     torch.cuda.set_device(0)
     w = graphs.build(args.workload)
-    r = PlanRunner(w, args.plan)
+    chosen = None
+    if args.plan == "korch":
+        from paper_2406_09465_amd import chooser
+        from paper_2406_09465_amd.warm import CHOOSER_LIMITS
+        t0 = time.time()
+        hand = [k for name in ("fused", "layered") for k in w.kernels(name)]
+        ch = chooser.korch_plan(w.graph, warmup=10, reps=50, extra=hand, **CHOOSER_LIMITS)
+        names = {v: k for k, v in w.ids.items()}
+        chosen = {"kernels": [[[names[v] for v in p], [names[v] for v in o]] for p, o in ch.kernels],
+                  "predicted_us": round(ch.cost_us, 3), "candidates": ch.candidates,
+                  "search_states": ch.states, "choose_seconds": round(time.time() - t0, 1)}
+        r = PlanRunner(w, kernels=ch.kernels)
+    else:
+        r = PlanRunner(w, args.plan)
     r.set_inputs(W.inputs(args.workload))
     nk = r.plan.num_kernels()
     stream = torch.cuda.current_stream()
@@ -208,6 +222,8 @@ def main():
         "roofline": roof,
         "kernels": kernels,
     }
+    if chosen:
+        out["chosen_plan"] = chosen
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
     print(json.dumps(out), flush=True)

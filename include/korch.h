@@ -211,8 +211,14 @@ int korch_plan_kernel_name(const korch_plan* p, int32_t k, char* buf, size_t cap
 int korch_plan_kernel_launch(const korch_plan* p, int32_t k, int32_t grid[3], int32_t block[3], int32_t* lds_bytes);
 
 /* ---- profiler (Section 5.2, kernel profiler; Algorithm 1's Profiling) --- */
+/* Generates and compiles (hipRTC, gfx950, code-object cache) the single kernel
+   (P', O) exactly as korch_profile_candidate does, without touching a GPU, so
+   that profiling on a device finds it compiled.  Returns KORCH_E_UNSUPPORTED
+   when no family implements it, KORCH_E_COMPILE when hipRTC rejects it. */
+int korch_compile_candidate(const korch_graph* g, const korch_kernel_desc* k);
+
 /* Times the single kernel (P', O) in isolation: compiles it, fills its inputs
-   with seeded N(0,1) values in device buffers the profiler allocates, runs
+   with seeded uniform values in [0.5, 1.5) in device buffers the profiler allocates, runs
    `warmup` untimed launches, then `reps` launches each preceded by a write of
    `flush_bytes` to a scratch buffer (to evict L2 and the Infinity Cache) and
    bracketed by HIP events on `stream`; *median_us is the median.  Returns

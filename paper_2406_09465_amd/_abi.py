@@ -102,6 +102,7 @@ _SIGS = {
     "korch_plan_kernel_source": ([_P, _I, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_kernel_name": ([_P, _I, C.c_char_p, C.c_size_t], C.c_int),
     "korch_plan_kernel_launch": ([_P, _I, C.POINTER(_I), C.POINTER(_I), C.POINTER(_I)], C.c_int),
+    "korch_compile_candidate": ([_P, C.POINTER(korch_kernel_desc)], C.c_int),
     "korch_profile_candidate": ([_P, C.POINTER(korch_kernel_desc), _I, _I, C.c_size_t, _P, C.POINTER(C.c_float)],
                                 C.c_int),
 }
@@ -146,7 +147,7 @@ class Graph:
         check(lib.korch_graph_create(C.byref(self.h)))
 
     def __del__(self):
-        if getattr(self, "h", None):
+        if getattr(self, "h", None) and lib is not None:
             lib.korch_graph_destroy(self.h)
             self.h = None
 
@@ -262,6 +263,15 @@ class Graph:
         check(lib.korch_kernel_family(self.h, C.byref(d), C.byref(fam)))
         return FAMILIES[fam.value]
 
+    def compile_candidate(self, prims, outs):
+        """Compiles the single kernel (prims, outs) as the profiler will; False when unsupported."""
+        d, keep = kernel_desc(prims, outs)
+        rc = lib.korch_compile_candidate(self.h, C.byref(d))
+        if rc == E_UNSUPPORTED:
+            return False
+        check(rc)
+        return True
+
     def profile(self, prims, outs, warmup=20, reps=100, flush_bytes=512 << 20, stream=0):
         """Median latency (us) of the single kernel (prims, outs); None when unsupported (infinite cost)."""
         d, keep = kernel_desc(prims, outs)
@@ -292,7 +302,7 @@ class Plan:
             check(lib.korch_plan_create(graph.h, len(kernels), descs, C.byref(self.h)))
 
     def __del__(self):
-        if getattr(self, "h", None):
+        if getattr(self, "h", None) and lib is not None:
             lib.korch_plan_destroy(self.h)
             self.h = None
 

@@ -25,6 +25,7 @@ void load_plan(Plan& p);
 void destroy_plan_device(Plan& p);
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
                   hipStream_t stream, int first, int count);
+void compile_candidate(const Graph& g, const KernelDesc& kd);
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream);
 }  // namespace korch
@@ -444,6 +445,18 @@ int korch_plan_kernel_launch(const korch_plan* p, int32_t k, int32_t grid[3], in
       if (block) block[i] = gk.block[i];
     }
     if (lds_bytes) *lds_bytes = gk.lds_bytes;
+  });
+}
+
+int korch_compile_candidate(const korch_graph* g, const korch_kernel_desc* k) {
+  return guard([&] {
+    NEED(g);
+    NEED(k);
+    if (!g->g.finalized) fail(KORCH_E_STATE, "graph is not finalized");
+    KernelDesc kd = to_desc(*k);
+    std::string why;
+    if (match_family(g->g, kd, &why) == KORCH_FAM_NONE) fail(KORCH_E_UNSUPPORTED, why);
+    compile_candidate(g->g, kd);
   });
 }
 

@@ -107,6 +107,10 @@ struct Emitter {
   bool staged = false;
   int stages = 2, slots = 1;
   std::ostringstream stage_decl;
+  // When set, the only index variable that differs between the slots of one
+  // thread: a staged load whose offset does not use it is issued once per stage
+  // (slot 0) and shared by all slots.
+  std::string slot_var;
 
   Emitter(const Graph& gg) : g(gg) {}
   std::string value(int node, const std::vector<Ix>& idx);

@@ -1,6 +1,7 @@
 // Shared code-generation machinery: affine index expressions, elementwise
 // expression strings and the per-element emitter that folds broadcast and
 // layout primitives (Korch, Section 3: O[x] = I[L(x)]) into load addresses.
+#include <cctype>
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
@@ -302,6 +303,17 @@ static std::vector<Ix> reshape_index(const Shape& out, const Shape& in, const st
   return res;
 }
 
+// True if identifier `v` occurs in expression `e` as a whole word.
+static bool uses_var(const std::string& e, const std::string& v) {
+  auto word = [](char c) { return std::isalnum((unsigned char)c) || c == '_'; };
+  for (size_t p = e.find(v); p != std::string::npos; p = e.find(v, p + 1)) {
+    bool lo = p == 0 || !word(e[p - 1]);
+    bool hi = p + v.size() >= e.size() || !word(e[p + v.size()]);
+    if (lo && hi) return true;
+  }
+  return false;
+}
+
 std::string Emitter::load(int node, const std::vector<Ix>& idx) {
   auto it = argslot.find(node);
   if (it == argslot.end()) fail(KORCH_E_UNSUPPORTED, "emitter: node " + std::to_string(node) + " is not available");
@@ -312,19 +324,21 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
   std::string T = ctype(n.dtype);
   std::string P = "((const " + T + "*)a.p[" + std::to_string(it->second) + "])";
   bool hoist = guard_depth == 0 && !force_gather;
-  if (staged && hoist && off.affine && off.c == 0) {
-    ++n_uniform;
-    std::string v = fresh("su");
-    stage_decl << "  " << T << " " << v << "[" << stages << "][" << slots << "];\n";
-    pre << "    " << v << "[st][i] = " << P << "[" << off.b << "];\n";
-    return "tof(" + v + "[st][i])";
-  }
-  if (staged && hoist && off.affine && off.c == 1 && vec > 1 && off.al % vec == 0) {
+  if (staged && hoist && off.affine && (off.c == 0 || (off.c == 1 && vec > 1 && off.al % vec == 0))) {
+    bool shared = !slot_var.empty() && !uses_var(off.b, slot_var);
+    std::string v = fresh(off.c == 0 ? "su" : "sx");
+    std::string ty = off.c == 0 ? T : "vec_t<" + std::to_string(vec) + ", " + T + ">";
+    std::string at = shared ? "[st][0]" : "[st][i]";
+    stage_decl << "  " << ty << " " << v << "[" << stages << "][" << (shared ? 1 : slots) << "];\n";
+    pre << "    " << (shared ? "if (i == 0) " : "") << v << at << " = ";
+    if (off.c == 0) {
+      ++n_uniform;
+      pre << P << "[" << off.b << "];\n";
+      return "tof(" + v + at + ")";
+    }
     ++n_vector;
-    std::string v = fresh("sx");
-    stage_decl << "  vec_t<" << vec << ", " << T << "> " << v << "[" << stages << "][" << slots << "];\n";
-    pre << "    " << v << "[st][i] = *(const vec_t<" << vec << ", " << T << ">*)(" << P << " + " << off.b << ");\n";
-    return "tof(" + v + "[st][i][e])";
+    pre << "*(const " << ty << "*)(" << P << " + " << off.b << ");\n";
+    return "tof(" + v + at + "[e])";
   }
   if (hoist && off.affine && off.c == 0) {
     ++n_uniform;

@@ -160,6 +160,19 @@ Graph extract_subgraph(const Graph& g, const KernelDesc& kd) {
   return s;
 }
 
+void compile_candidate(const Graph& g, const KernelDesc& kd) {
+  Plan p;
+  p.g = extract_subgraph(g, kd);
+  KernelDesc one;
+  for (size_t i = 0; i < p.g.nodes.size(); ++i)
+    if (p.g.is_prim((int)i)) one.prims.push_back((int)i);
+  one.outs = p.g.outputs;
+  std::sort(one.outs.begin(), one.outs.end());
+  p.kernels = {one};
+  validate_plan(p.g, p.kernels, false);
+  compile_plan(p);
+}
+
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream) {
   Plan p;

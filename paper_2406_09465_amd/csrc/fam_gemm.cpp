@@ -640,6 +640,10 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
       em.stages = 2;
       em.slots = per;
       em.tmp = isA ? 0 : 500;  // keep the two operands' register names apart
+      // the slots of one thread differ only in their row (axis_k) or only in
+      // their k (vector along rows) when the thread count is a multiple of the
+      // vectors per row / per k
+      if (axis_k ? sp.NT % kper == 0 : sp.NT % (rows / V) == 0) em.slot_var = axis_k ? "rg" : "kg";
       std::vector<Ix> idx = batch_idx(nodes[0]);
       Ix r = axis_k ? Ix::var("rg", 0, 1) : Ix::var("rg", 1, V);
       Ix k = axis_k ? Ix::var("kg", 1, V) : Ix::var("kg", 0, 1);
@@ -677,8 +681,11 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
         s << slot_coords();
         s << "    const i64 rg = " << base << " + rl, kg = k0 + kl;\n";
         s << "    float dst[" << V << "];\n";
-        std::string cond = axis_k ? "(rg < " + std::to_string(R) + "LL && kg + e < " + std::to_string(sp.K) + "LL)"
-                                  : "(rg + e < " + std::to_string(R) + "LL && kg < " + std::to_string(sp.K) + "LL)";
+        // a tile-aligned problem has no element outside it
+        const bool aligned = R % rows == 0 && sp.K % sp.BK == 0;
+        std::string cond = aligned ? "true"
+                           : axis_k ? "(rg < " + std::to_string(R) + "LL && kg + e < " + std::to_string(sp.K) + "LL)"
+                                    : "(rg + e < " + std::to_string(R) + "LL && kg < " + std::to_string(sp.K) + "LL)";
         s << "#pragma unroll\n    for (int e = 0; e < " << V << "; ++e) {\n" << em.body.str() << "      dst[e] = " << cond
           << " ? (float)(" << val << ") : 0.0f;\n    }\n";
         if (axis_k) {

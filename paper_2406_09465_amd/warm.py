@@ -1,6 +1,7 @@
 """Pre-compiles (hipRTC, gfx950, no GPU needed) the kernels of the standard plans
-of every workload, and of the seeded sampled plans the GPU tests run, so a GPU
-run finds them in the code-object cache."""
+of every workload, of the seeded sampled plans the GPU tests run, and every
+supported candidate kernel the measured-cost chooser profiles, so a GPU run
+finds them in the code-object cache."""
 
 from __future__ import annotations
 
@@ -26,6 +27,56 @@ SAMPLED = {
     "linattn": (dict(heads=4, n=512, d=16), 6, 7),
 }
 
+# Sizes at which the chooser profiles every supported candidate (bench.py's
+# measured-cost plan at full size; the chooser GPU test at the sampled sizes).
+CHOOSER = {w: [{}, SAMPLED[w][0]] for w in SAMPLED}
+CHOOSER_LIMITS = dict(max_prims=64, max_outs=3)
+
+
+def _jobs():
+    """Independent compile jobs: (kind, workload, sizes, extra)."""
+    jobs = []
+    for w, sizes in SIZES.items():
+        for sz in sizes:
+            jobs.append(("plans", w, sz, None))
+    for w, (sz, n, seed) in SAMPLED.items():
+        jobs.append(("sampled", w, sz, (n, seed)))
+    for w, sizes in CHOOSER.items():
+        for sz in sizes:
+            jobs.append(("candidates", w, sz, None))
+    return jobs
+
+
+def _run_job(job, part=0, parts=1):
+    """Compiles this process's share of one job; returns the failures."""
+    kind, w, sz, extra = job
+    wl = graphs.build(w, **sz)
+    failures = []
+    if kind == "plans":
+        for pn in ("unfused", "layered", "fused"):
+            try:
+                wl.plan(pn).compile()
+            except KorchError as e:
+                failures.append((w, sz, pn, str(e)[:200]))
+    elif kind == "sampled":
+        for i, ks in enumerate(search.sampled_plans(wl.graph, *extra)):
+            try:
+                graphs.Plan(wl.graph, ks).compile()
+            except KorchError as e:
+                failures.append((w, sz, f"sampled {i}", str(e)[:200]))
+    else:
+        cands = wl.graph.candidates(only_supported=True, **CHOOSER_LIMITS)
+        for c in cands[part::parts]:
+            try:
+                wl.graph.compile_candidate(*c)
+            except KorchError as e:
+                failures.append((w, sz, f"candidate {c}", str(e)[:200]))
+    return failures
+
+
+def _worker(args):
+    return _run_job(*args)
+
 
 def prune(before):
     """Delete cached code objects not used since ``before`` (a time.time())."""
@@ -42,24 +93,26 @@ def prune(before):
     return n
 
 
-def warm_cache(verbose=False, prune_stale=True):
+def warm_cache(verbose=False, prune_stale=True, processes=None):
+    """Compiles every job; hipRTC serializes compiles within one process, so the
+    jobs are spread over worker processes (spawned, each loading the library)."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    import os
     t0 = time.time()
+    procs = processes or min(8, os.cpu_count() or 1)
+    tasks = []
+    for job in _jobs():
+        parts = procs if job[0] == "candidates" else 1
+        tasks.extend((job, i, parts) for i in range(parts))
     failures = []
-    for w, sizes in SIZES.items():
-        for sz in sizes:
-            wl = graphs.build(w, **sz)
-            for pn in ("unfused", "layered", "fused"):
-                try:
-                    wl.plan(pn).compile()
-                except KorchError as e:
-                    failures.append((w, sz, pn, str(e)[:200]))
-    for w, (sz, n, seed) in SAMPLED.items():
-        wl = graphs.build(w, **sz)
-        for i, ks in enumerate(search.sampled_plans(wl.graph, n, seed)):
-            try:
-                graphs.Plan(wl.graph, ks).compile()
-            except KorchError as e:
-                failures.append((w, sz, f"sampled {i}", str(e)[:200]))
+    if procs <= 1:
+        for t in tasks:
+            failures.extend(_worker(t))
+    else:
+        with cf.ProcessPoolExecutor(max_workers=procs, mp_context=mp.get_context("spawn")) as ex:
+            for f in ex.map(_worker, tasks):
+                failures.extend(f)
     removed = prune(t0) if prune_stale and not failures else 0
     if verbose:
         print(f"warm_cache: {time.time() - t0:.1f}s, {len(failures)} plans not compiled, {removed} stale removed")
