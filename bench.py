@@ -45,8 +45,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="mlp", choices=list(DESCR))
-    ap.add_argument("--plan", default="fused",
-                    help="fused | layered | unfused | korch (profile every candidate kernel and run the cheapest plan)")
+    ap.add_argument("--plan", default="korch",
+                    help="korch (profile every candidate kernel on this GPU and run the cheapest valid plan; the "
+                         "default) | fused | layered | unfused (hand-written plans)")
+    ap.add_argument("--kernels-json", default="",
+                    help="run the plan recorded (chosen_plan) in an earlier bench.py output line instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work for the oracle sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -117,7 +120,12 @@ def main():
     torch.cuda.set_device(0)
     w = graphs.build(args.workload)
     chosen = None
-    if args.plan == "korch":
+    if args.kernels_json:
+        d = json.loads(open(args.kernels_json).read().strip().splitlines()[-1])
+        chosen = d["chosen_plan"]
+        ks = [([w.ids[n] for n in pr], [w.ids[n] for n in ou]) for pr, ou in chosen["kernels"]]
+        r = PlanRunner(w, kernels=ks)
+    elif args.plan == "korch":
         from paper_2406_09465_amd import chooser
         from paper_2406_09465_amd.warm import CHOOSER_LIMITS
         t0 = time.time()
@@ -218,7 +226,8 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": DESCR[args.workload], "plan": args.plan, "kernels": nk},
+        "config": {"workload": DESCR[args.workload], "plan": "recorded" if args.kernels_json else args.plan,
+                   "kernels": nk},
         "roofline": roof,
         "kernels": kernels,
     }

@@ -7,6 +7,7 @@
 #include <cstdlib>
 #include <thread>
 
+#include "families.h"
 #include "plan.h"
 
 namespace korch {
@@ -24,10 +25,17 @@ hipError_t launch_fill(void* p, size_t n, int dtype, uint64_t seed, hipStream_t 
 void generate_plan(Plan& p) {
   if (!p.ck.empty()) return;
   std::vector<CompiledKernel> ck(p.kernels.size());
-  for (size_t k = 0; k < p.kernels.size(); ++k) {
-    ck[k].desc = p.kernels[k];
-    ck[k].gen = generate_kernel(p.g, ck[k].desc, (int)k);
+  set_kernel_prefix(p.name_prefix);
+  try {
+    for (size_t k = 0; k < p.kernels.size(); ++k) {
+      ck[k].desc = p.kernels[k];
+      ck[k].gen = generate_kernel(p.g, ck[k].desc, (int)k);
+    }
+  } catch (...) {
+    set_kernel_prefix("korch_k");
+    throw;
   }
+  set_kernel_prefix("korch_k");
   p.ck = std::move(ck);
   plan_workspace(p);
 }
@@ -162,6 +170,7 @@ Graph extract_subgraph(const Graph& g, const KernelDesc& kd) {
 
 void compile_candidate(const Graph& g, const KernelDesc& kd) {
   Plan p;
+  p.name_prefix = "korch_cand";
   p.g = extract_subgraph(g, kd);
   KernelDesc one;
   for (size_t i = 0; i < p.g.nodes.size(); ++i)
@@ -176,6 +185,7 @@ void compile_candidate(const Graph& g, const KernelDesc& kd) {
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream) {
   Plan p;
+  p.name_prefix = "korch_cand";
   p.g = extract_subgraph(g, kd);
   KernelDesc one;
   for (size_t i = 0; i < p.g.nodes.size(); ++i)

@@ -239,7 +239,7 @@ void choose_tiles(GemmSpec& sp, bool split) {
   sp.BM = 128;
   int64_t tiles = (sp.M + 127) / 128 * ((sp.N + sp.BN - 1) / sp.BN) * sp.batch;
   if (!split && tiles < 240 && sp.M > 64) sp.BM = 64;
-  if (split) sp.BM = sp.M <= 16 ? 16 : (sp.M <= 32 ? 32 : 64);
+  if (split) sp.BM = sp.M <= 16 ? 16 : 32;
   sp.WN = sp.BN >= 64 ? 2 : 1;
   sp.WM = 4 / sp.WN;
   while (sp.BM / sp.WM < 16) {
@@ -253,6 +253,8 @@ void choose_tiles(GemmSpec& sp, bool split) {
   }
   if (sp.BM / sp.WM < 16) sp.WM = std::max(1, sp.BM / 16);
   sp.NT = 256;
+  sp.NS = 2;
+  if (const char* e = getenv("KORCH_GEMM_NS")) sp.NS = std::max(2, std::min(8, atoi(e)));
   // Explicit tile override "BM,BN,BK,WM,WN" (tile-configuration sweeps of the
   // profiler); ignored unless it is consistent.
   if (const char* e = getenv("KORCH_GEMM_CFG")) {
@@ -327,7 +329,7 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
     int kper = sp.BK / V;
     int nslots = rows * kper;
     int per = (nslots + sp.NT - 1) / sp.NT;
-    s << "  uint4 r" << X << "[2][" << per << "];\n";
+    s << "  uint4 r" << X << "[" << sp.NS << "][" << per << "];\n";
     s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
     s << "    const int sl = tid + i * " << sp.NT << ";\n";
     if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
@@ -354,7 +356,7 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
     int cpr = sp.BN / C;
     int nslots = sp.BK * cpr;
     int per = (nslots + sp.NT - 1) / sp.NT;
-    s << "  uint4 r" << X << "[2][" << per << "];\n";
+    s << "  uint4 r" << X << "[" << sp.NS << "][" << per << "];\n";
     s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per
       << "; ++i) {\n";
     s << "    const int sl = tid + i * " << sp.NT << ";\n";
@@ -385,7 +387,7 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
   int per = (nblocks + sp.NT - 1) / sp.NT;
   std::string T4 = "vec_t<4, " + T + ">";
   std::string TK = "vec_t<" + std::to_string(KB) + ", " + T + ">";
-  s << "  " << T4 << " r" << X << "[2][" << per << "][" << KB << "];\n";
+  s << "  " << T4 << " r" << X << "[" << sp.NS << "][" << per << "][" << KB << "];\n";
   s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
   s << "    const int b_ = tid + i * " << sp.NT << ";\n";
   if (nblocks % sp.NT) s << "    if (b_ >= " << nblocks << ") break;\n";
@@ -462,7 +464,7 @@ static std::string buffer_loader(const KInfo& ki, const GemmSpec& sp, bool isA, 
   int per = (nslots + sp.NT - 1) / sp.NT;
   s << "  const __amdgpu_buffer_rsrc_t rs" << X << " = __builtin_amdgcn_make_buffer_rsrc(" << P << ", 0, "
     << (long long)bytes << ", 0x00020000);\n";
-  s << "  uint4 r" << X << "[2][" << per << "];\n";
+  s << "  uint4 r" << X << "[" << sp.NS << "][" << per << "];\n";
   // per-slot constants
   s << "  int o" << X << "[" << per << "];  // element offset of the slot's vector at k-tile 0\n";
   s << "  bool v" << X << "[" << per << "];  // slot lies inside the tile rows / columns\n";
@@ -637,7 +639,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
       em.argslot = slot;
       em.vec = V;
       em.staged = true;
-      em.stages = 2;
+      em.stages = sp.NS;
       em.slots = per;
       em.tmp = isA ? 0 : 500;  // keep the two operands' register names apart
       // the slots of one thread differ only in their row (axis_k) or only in
@@ -701,7 +703,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   }
   // slot s -> (row, k): axis_k: row = s / (BK/V), kk = (s % (BK/V)) * V
   //                     axis_row: kk = s / (rows/V), row = (s % (rows/V)) * V
-  s << "  float r" << X << "[2][" << per << "][" << V << "];\n";
+  s << "  float r" << X << "[" << sp.NS << "][" << per << "][" << V << "];\n";
   s << "  auto fetch" << X << " = [&](const i64 k0, const int st) {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << per << "; ++i) {\n";
   s << "    const int sl = tid + i * " << sp.NT << ";\n";
@@ -796,7 +798,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
 }
 
 // The MFMA main loop over k-tiles [kt0, kt1) of the contraction.
-std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t kconst) {
+std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t kconst, bool kconst_exact) {
   std::ostringstream s;
   bool f32 = sp.mtype == KORCH_F32;
   std::string T = ctype(sp.mtype);
@@ -838,36 +840,50 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
       << sp.FN << "; ++j) acc[i][j] = " << fn << "(af[i], bf[j], acc[i][j], 0, 0, 0);\n";
   }
   s << "    }\n  };\n";
-  // Two-deep pipeline: while tile t is multiplied from LDS buffer t%2, the
-  // registers of stage (t+1)%2 already hold tile t+1 (loaded one iteration
-  // earlier) and the loads of tile t+2 are in flight into stage t%2.  Fetches
-  // are unconditional (tile indices clamped to the last tile) so the compiler
-  // counts outstanding loads exactly; with a compile-time tile count the loop
-  // is unrolled completely.
+  // Register pipeline of NS stages over two LDS buffers: while tile t is
+  // multiplied from LDS buffer t%2, tiles t+1 .. t+NS-1 are in registers or in
+  // flight, and the loads of tile t+NS are issued into the stage tile t
+  // occupied (it was staged to LDS before tile t's products).  Fetches are
+  // unconditional (tile indices clamped to the last tile) so the compiler counts
+  // outstanding loads exactly; with a compile-time tile count the loop is
+  // unrolled completely (stage and buffer indices are then constants).
   int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
   std::string wguard = nw < sp.NT / 64 ? "if (wave < " + std::to_string(nw) + ") " : "";
   auto clampk = [&](const std::string& t) {
     return "(i64)((" + t + ") < kt1 ? (" + t + ") : kt1 - 1) * " + std::to_string(sp.BK);
   };
-  auto step = [&](const std::string& b, const std::string& kt) {
-    std::ostringstream o;
-    o << "    fetchA(" << clampk(kt + " + 2") << ", " << b << "); fetchB(" << clampk(kt + " + 2") << ", " << b << ");\n";
-    o << "    " << wguard << "compute(" << b << ");\n";
-    if (!hook.empty()) o << "    {\n      const " << T << "* Ab = As + (" << b << ") * " << sp.BM * sp.BKP << ";\n" << hook << "    }\n";
-    o << "    stashA(1 - (" << b << "), 1 - (" << b << "), " << clampk(kt + " + 1") << "); stashB(1 - (" << b << "), 1 - ("
-      << b << "), " << clampk(kt + " + 1") << ");\n";
-    o << "    __syncthreads();\n";
-    return o.str();
+  auto hookat = [&](const std::string& b) {
+    if (hook.empty()) return std::string();
+    return "    {\n      const " + T + "* Ab = As + (" + b + ") * " + std::to_string(sp.BM * sp.BKP) + ";\n" + hook + "    }\n";
   };
-  s << "  fetchA(" << clampk("kt0") << ", 0); fetchB(" << clampk("kt0") << ", 0);\n";
-  s << "  fetchA(" << clampk("kt0 + 1") << ", 1); fetchB(" << clampk("kt0 + 1") << ", 1);\n";
+  const bool unrolled = kconst > 0 && kconst <= 128;
+  const int NS = unrolled ? sp.NS : 2;
+  for (int st = 0; st < NS; ++st)
+    s << "  fetchA(" << clampk("kt0 + " + std::to_string(st)) << ", " << st << "); fetchB("
+      << clampk("kt0 + " + std::to_string(st)) << ", " << st << ");\n";
   s << "  stashA(0, 0, " << clampk("kt0") << "); stashB(0, 0, " << clampk("kt0") << ");\n  __syncthreads();\n";
-  if (kconst > 0 && kconst <= 128) {
-    s << "#pragma unroll\n  for (int kt = kt0; kt < kt0 + " << kconst << "; ++kt) {\n";
-    s << "    const int b_ = (kt - kt0) & 1;\n";
-    s << step("b_", "kt");
-    s << "  }\n";
+  if (unrolled) {
+    // a split shorter than kconst skips the products of its missing tiles
+    std::string live = kconst_exact ? "" : "if (kt < kt1) ";
+    s << "#pragma unroll\n  for (int j = 0; j < " << kconst << "; ++j) {\n";
+    s << "    const int kt = kt0 + j, b_ = j & 1, s_ = j % " << NS << ", sn_ = (j + 1) % " << NS << ";\n";
+    s << "    fetchA(" << clampk("kt + " + std::to_string(NS)) << ", s_); fetchB(" << clampk("kt + " + std::to_string(NS))
+      << ", s_);\n";
+    s << "    " << live << wguard << "compute(b_);\n";
+    if (!hook.empty()) s << "    " << live << "{\n" << hookat("b_") << "    }\n";
+    s << "    stashA(1 - b_, sn_, " << clampk("kt + 1") << "); stashB(1 - b_, sn_, " << clampk("kt + 1") << ");\n";
+    s << "    __syncthreads();\n  }\n";
   } else {
+    auto step = [&](const std::string& b, const std::string& kt) {
+      std::ostringstream o;
+      o << "    fetchA(" << clampk(kt + " + 2") << ", " << b << "); fetchB(" << clampk(kt + " + 2") << ", " << b << ");\n";
+      o << "    " << wguard << "compute(" << b << ");\n";
+      o << hookat(b);
+      o << "    stashA(1 - (" << b << "), 1 - (" << b << "), " << clampk(kt + " + 1") << "); stashB(1 - (" << b << "), 1 - ("
+        << b << "), " << clampk(kt + " + 1") << ");\n";
+      o << "    __syncthreads();\n";
+      return o.str();
+    };
     s << "  for (int kt = kt0; kt < kt1; kt += 2) {\n";
     s << step("0", "kt");
     s << "    if (kt + 1 >= kt1) break;\n";
@@ -991,6 +1007,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   if (!analyze_gemm(ki, sp, &why, false)) fail(KORCH_E_UNSUPPORTED, why);
   choose_tiles(sp, false);
   plan_operands(ki, sp);
+  if ((sp.K + sp.BK - 1) / sp.BK > 128) sp.NS = 2;  // long contractions use the rolled loop
   GenKernel gk;
   gk.family = sp.conv ? KORCH_FAM_CONV : KORCH_FAM_GEMM;
   gk.name = kernel_name(index, sp.conv ? "conv" : "gemm");

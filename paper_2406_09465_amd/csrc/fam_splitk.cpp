@@ -246,13 +246,23 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   int64_t mtiles = (sp.M + sp.BM - 1) / sp.BM;
   int64_t KT = (sp.K + sp.BK - 1) / sp.BK;
   int64_t base = mtiles * sp.batch;
-  // about KORCH_SPLITK_WGS workgroups in total (default 256, one per compute
-  // unit), each with at least 4 k-tiles
+  // About KORCH_SPLITK_WGS workgroups in total (default 256, one per compute
+  // unit) and at most 16 splits per output tile, so that the last workgroup of
+  // a tile sums few partial tiles.  A split count that divides the tile count
+  // is preferred (every split then runs the same unrolled loop); each split
+  // keeps up to four k-tiles of loads in flight.
   int64_t target = 256;
   if (const char* e = getenv("KORCH_SPLITK_WGS")) target = std::max(1, atoi(e));
-  int64_t S = std::max<int64_t>(1, std::min<int64_t>((target + base - 1) / base, std::max<int64_t>(1, KT / 4)));
+  int64_t S = std::max<int64_t>(1, std::min<int64_t>({(target + base - 1) / base, 16, KT}));
+  for (int64_t d = S; d >= std::max<int64_t>(1, S / 2); --d)
+    if (KT % d == 0) {
+      S = d;
+      break;
+    }
   int64_t ktper = (KT + S - 1) / S;
   S = (KT + ktper - 1) / ktper;
+  const bool exact = KT % ktper == 0;
+  sp.NS = (int)std::max<int64_t>(2, std::min<int64_t>(4, ktper));
   int64_t tile = (int64_t)sp.BM * sp.BN;
   int nside = (int)sp.side.size();
   // scratch: partial tiles, then side partials; counters: one per output tile
@@ -287,7 +297,7 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "  float side_acc = 0.0f;\n";
   s << operand_loader(ki, sp, true, slot);
   s << operand_loader(ki, sp, false, slot);
-  s << mfma_mainloop(sp, hook.str());
+  s << mfma_mainloop(sp, hook.str(), ktper <= 128 ? ktper : 0, exact);
   // partial tile -> scratch
   s << "  const i64 tix = bz * " << mtiles << " + mt;\n";
   s << "  float* part = (float*)a.p[" << scr_slot << "];\n";

@@ -64,7 +64,9 @@ void KInfo::fill_cost(GenKernel& gk) const {
   gk.alg_flops = flops;
 }
 
-std::string kernel_name(int index, const char* fam) { return "korch_k" + std::to_string(index) + "_" + fam; }
+static thread_local std::string g_kernel_prefix = "korch_k";
+void set_kernel_prefix(const std::string& prefix) { g_kernel_prefix = prefix; }
+std::string kernel_name(int index, const char* fam) { return g_kernel_prefix + std::to_string(index) + "_" + fam; }
 
 static int64_t pow2ceil(int64_t x) {
   int64_t p = 1;

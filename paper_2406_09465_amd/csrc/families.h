@@ -26,6 +26,8 @@ struct KInfo {
 };
 
 std::string kernel_name(int index, const char* fam);
+// Prefix of the kernel symbols generated on this thread ("korch_k" for plans).
+void set_kernel_prefix(const std::string& prefix);
 void choose_row_geometry(int64_t L, int elem_bytes, int& G, int& VEC, int& NC);
 
 bool match_pointwise(const KInfo& ki, std::string* why);

@@ -31,6 +31,7 @@ struct GemmSpec {
   int BM = 128, BN = 128, BK = 32, BKP = 40, kstep = 32, WM = 2, WN = 2, WTM = 64, WTN = 64, FM = 4, FN = 4;
   int VA = 8, VB = 8, LDC = 132;
   int NT = 256;  // threads per workgroup (64 per wave)
+  int NS = 2;    // register pipeline stages (tiles loaded ahead of the one multiplied)
   // Right operand staged raw in LDS as [k][n] (n contiguous, pitch BNP) and
   // read into MFMA fragments with transposing LDS reads (half precision) or
   // plain reads (fp32); otherwise staged as [n][k] with pitch BKP.
@@ -45,8 +46,11 @@ bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_re
 void choose_tiles(GemmSpec& sp, bool split);
 std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const std::map<int, int>& slot);
 // kconst: number of k-tiles when it is a compile-time constant (the loop is then
-// unrolled completely), else 0.
-std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "", int64_t kconst = 0);
+// unrolled completely and uses sp.NS register stages), else 0; kconst_exact:
+// every workgroup runs exactly kconst tiles (else tiles at or past kt1 are
+// skipped).
+std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "", int64_t kconst = 0,
+                          bool kconst_exact = true);
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
                           const std::string& cs_row, const std::set<int>& skip = {});
 std::string gemm_prologue_common(const GemmSpec& sp);

@@ -38,6 +38,7 @@ struct Plan {
   void* counters = nullptr;      // device buffer owned by the plan
   int counter_device = -1;
   std::map<int, size_t> ws_offset;  // workspace-resident materialized node -> offset
+  std::string name_prefix = "korch_k";  // kernel symbols: <prefix><index>_<family>
 };
 
 // Checks a plan against Definitions 1 and 3 and the ordered dependency /

@@ -61,7 +61,13 @@ def pmc(args):
     f_fetch = known_kib / fetch[ck]
     f_write = known_kib / write[ck]
     w = graphs.build(args.workload)
-    p = w.plan(args.plan)
+    if args.bench_json:
+        # the plan bench.py ran (e.g. the measured-cost choice), by node names
+        d = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
+        ks = [([w.ids[n] for n in pr], [w.ids[n] for n in ou]) for pr, ou in d["chosen_plan"]["kernels"]]
+        p = graphs.Plan(w.graph, ks)
+    else:
+        p = w.plan(args.plan)
     p.compile()
     res = {"workload": args.workload, "plan": args.plan, "calibration_kernel": ck[:80],
            "fetch_factor": f_fetch, "write_factor": f_write, "cmd_fetch": args.cmd_fetch, "cmd_write": args.cmd_write,
@@ -116,6 +122,7 @@ def main():
     p.add_argument("--out", required=True)
     p.add_argument("--cmd-fetch", default="")
     p.add_argument("--cmd-write", default="")
+    p.add_argument("--bench-json", default="", help="bench.py output line whose chosen_plan to use")
     a = ap.parse_args()
     stats(a) if a.mode == "stats" else pmc(a)
 
