@@ -237,8 +237,28 @@ void choose_tiles(GemmSpec& sp, bool split) {
   else
     sp.BN = 128;
   sp.BM = 128;
-  int64_t tiles = (sp.M + 127) / 128 * ((sp.N + sp.BN - 1) / sp.BN) * sp.batch;
-  if (!split && tiles < 240 && sp.M > 64) sp.BM = 64;
+  if (!split && nt > 64 && sp.mms.size() == 1) {
+    // Tile shape by a throughput model of 256 compute units: tiles run in
+    // rounds of 256, each round costs its tile area, and every tile pays for
+    // re-reading its operand panels (proportional to 1/BM + 1/BN).
+    double best = 1e300;
+    for (int bm : {128, 64}) {
+      for (int bn : {128, 96, 64}) {
+        if (bn == 96 && sp.N % 96 != 0) continue;
+        int64_t tiles = (sp.M + bm - 1) / bm * ((sp.N + bn - 1) / bn) * sp.batch;
+        double rounds = (double)((tiles + 255) / 256);
+        double cost = rounds * bm * bn * (1.0 + 24.0 * (1.0 / bm + 1.0 / bn));
+        if (cost < best * (1.0 - 1e-9)) {
+          best = cost;
+          sp.BM = bm;
+          sp.BN = bn;
+        }
+      }
+    }
+  } else if (!split) {
+    int64_t tiles = (sp.M + 127) / 128 * ((sp.N + sp.BN - 1) / sp.BN) * sp.batch;
+    if (tiles < 240 && sp.M > 64) sp.BM = 64;
+  }
   if (split) sp.BM = sp.M <= 16 ? 16 : 32;
   sp.WN = sp.BN >= 64 ? 2 : 1;
   sp.WM = 4 / sp.WN;
