@@ -305,6 +305,37 @@ void plan_operands(const KInfo& ki, GemmSpec& sp) {
   sp.b_kn = sp.Bs.size() == 1 && !ki.in.count(sp.Bs[0]) && sp.N % C == 0;
   // row pitch: 32 extra bytes keep the four rows of one transposing read in distinct banks
   sp.BNP = sp.BN + (sp.mtype == KORCH_F32 ? 4 : 16);
+  sp.BSH = 0;
+  const char* shift_env = getenv("KORCH_LDS_BANK_SHIFT");  // "0" disables the row shift
+  if (sp.b_kn && sp.mtype != KORCH_F32 && !(shift_env && atoi(shift_env) == 0)) {
+    // smallest shift (a multiple of 16 bytes) that makes the 32-byte windows of
+    // rows {0,1,2,3,8,9,10,11} disjoint modulo the 256 bytes of the 64 banks
+    const int P = sp.BNP * 2;
+    for (int S = 0; S < 256; S += 16) {
+      int w[8], n = 0;
+      for (int r : {0, 1, 2, 3, 8, 9, 10, 11}) w[n++] = (r * P + (r >> 3) * S) % 256;
+      bool ok = true;
+      for (int a = 0; a < 8 && ok; ++a)
+        for (int b = a + 1; b < 8 && ok; ++b) {
+          int d = (w[b] - w[a] + 256) % 256;
+          if (d < 32 || d > 224) ok = false;
+        }
+      if (ok) {
+        sp.BSH = S / 2;
+        break;
+      }
+    }
+  }
+}
+
+std::string b_row_off(const GemmSpec& sp, const std::string& k) {
+  std::string r = "(" + k + ") * " + std::to_string(sp.BNP);
+  if (sp.BSH) r += " + ((" + k + ") >> 3) * " + std::to_string(sp.BSH);
+  return r;
+}
+
+int64_t b_buf_elems(const GemmSpec& sp) {
+  return sp.b_kn ? (int64_t)sp.BK * sp.BNP + (int64_t)((sp.BK + 7) / 8) * sp.BSH : (int64_t)sp.BN * sp.BKP;
 }
 
 // Raw staging of an operand that is a plain materialized tensor (no prologue):
@@ -394,7 +425,7 @@ static std::string raw_loader(const KInfo& ki, const GemmSpec& sp, bool isA, con
     s << "    const int sl = tid + i * " << sp.NT << ";\n";
     if (nslots % sp.NT) s << "    if (sl >= " << nslots << ") break;\n";
     s << "    const int kl = sl / " << cpr << ", nl = (sl % " << cpr << ") * " << C << ";\n";
-    s << "    *(uint4*)(" << lds << " + buf * " << sp.BK * sp.BNP << " + kl * " << sp.BNP << " + nl) = r" << X
+    s << "    *(uint4*)(" << lds << " + buf * " << b_buf_elems(sp) << " + " << b_row_off(sp, "kl") << " + nl) = r" << X
       << "[st][i];\n";
     s << "  }\n  };\n";
     return s.str();
@@ -544,7 +575,7 @@ static std::string buffer_loader(const KInfo& ki, const GemmSpec& sp, bool isA, 
     s << "    *(uint4*)(" << lds << " + buf * " << sp.BM * sp.BKP << " + rl * " << sp.BKP << " + kl) = r" << X << "[st][i];\n";
   } else {
     s << "    const int kl = sl / " << kper << ", nl = (sl % " << kper << ") * " << C << ";\n";
-    s << "    *(uint4*)(" << lds << " + buf * " << sp.BK * sp.BNP << " + kl * " << sp.BNP << " + nl) = r" << X
+    s << "    *(uint4*)(" << lds << " + buf * " << b_buf_elems(sp) << " + " << b_row_off(sp, "kl") << " + nl) = r" << X
       << "[st][i];\n";
   }
   s << "  }\n  };\n";
@@ -827,7 +858,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
     << "; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
   s << "  auto compute = [&](const int buf) {\n";
   s << "    const " << T << "* Ab = As + buf * " << sp.BM * sp.BKP << ";\n";
-  int bbuf = sp.b_kn ? sp.BK * sp.BNP : sp.BN * sp.BKP;
+  int64_t bbuf = b_buf_elems(sp);
   s << "    const " << T << "* Bb = Bs + buf * " << bbuf << ";\n";
   s << "#pragma unroll\n    for (int kk = 0; kk < " << sp.BK / sp.kstep << "; ++kk) {\n";
   if (f32) {
@@ -851,7 +882,8 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
       << sp.WTM << " + i * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
     if (sp.b_kn)
       s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = __builtin_bit_cast(" << V8
-        << ", lds_tr_k8(Bb + (kk * 32 + (l >> 4) * 8 + ((l & 15) >> 2)) * " << sp.BNP << " + wn * " << sp.WTN
+        << ", lds_tr_k8(Bb + (kk * 32 + (l >> 4) * 8 + ((l & 15) >> 2)) * " << sp.BNP
+        << (sp.BSH ? " + (kk * 4 + (l >> 4)) * " + std::to_string(sp.BSH) : std::string()) << " + wn * " << sp.WTN
         << " + j * 16 + 4 * (l & 3), " << sp.BNP << "));\n";
     else
       s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = *(const " << V8 << "*)(Bb + (wn * "
@@ -920,7 +952,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
 }
 
 size_t gemm_smem_bytes(const GemmSpec& sp) {
-  size_t bbuf = sp.b_kn ? (size_t)sp.BK * sp.BNP : (size_t)sp.BN * sp.BKP;
+  size_t bbuf = (size_t)b_buf_elems(sp);
   size_t ab = (size_t)2 * ((size_t)sp.BM * sp.BKP + bbuf) * dtype_bytes(sp.mtype);
   size_t c = (size_t)sp.BM * sp.LDC * 4;
   return std::max(ab, c);

@@ -37,7 +37,17 @@ struct GemmSpec {
   // plain reads (fp32); otherwise staged as [n][k] with pitch BKP.
   bool b_kn = false;
   int BNP = 0;
+  // Each block of 8 rows starts BSH elements after the previous block ends
+  // (row k at k * BNP + (k / 8) * BSH): one half-wave of transposing reads
+  // covers rows {0..3, 8..11} (+ 16 j), and the relative shift of the second
+  // block puts those eight 32-byte windows on distinct LDS banks.
+  int BSH = 0;
 };
+
+// LDS element offset of row k of the [k][n] right-operand tile.
+std::string b_row_off(const GemmSpec& sp, const std::string& k);
+// Elements of one LDS buffer of the right operand.
+int64_t b_buf_elems(const GemmSpec& sp);
 
 // Decides operand staging layouts once the tiles are chosen.
 void plan_operands(const KInfo& ki, GemmSpec& sp);
