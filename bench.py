@@ -50,6 +50,8 @@ def parse():
                          "default) | fused | layered | unfused (hand-written plans)")
     ap.add_argument("--kernels-json", default="",
                     help="run the plan recorded (chosen_plan) in an earlier bench.py output line instead")
+    ap.add_argument("--no-rewrite", action="store_true",
+                    help="korch plan: do not consider the transformed primitive graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work for the oracle sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -123,19 +125,30 @@ def main():
     if args.kernels_json:
         d = json.loads(open(args.kernels_json).read().strip().splitlines()[-1])
         chosen = d["chosen_plan"]
-        ks = [([w.ids[n] for n in pr], [w.ids[n] for n in ou]) for pr, ou in chosen["kernels"]]
+        w, ks = graphs.plan_from_record(w, chosen)
         r = PlanRunner(w, kernels=ks)
     elif args.plan == "korch":
+        # Orchestration over the primitive graph and over its transformed
+        # version (Section 3 rewrites); the cheaper measured plan runs.
         from paper_2406_09465_amd import chooser
+        from paper_2406_09465_amd._abi import RW_ALL
         from paper_2406_09465_amd.warm import CHOOSER_LIMITS
         t0 = time.time()
         hand = [k for name in ("fused", "layered") for k in w.kernels(name)]
         ch = chooser.korch_plan(w.graph, warmup=10, reps=50, extra=hand, **CHOOSER_LIMITS)
-        names = {v: k for k, v in w.ids.items()}
-        chosen = {"kernels": [[[names[v] for v in p], [names[v] for v in o]] for p, o in ch.kernels],
-                  "predicted_us": round(ch.cost_us, 3), "candidates": ch.candidates,
-                  "search_states": ch.states, "choose_seconds": round(time.time() - t0, 1)}
-        r = PlanRunner(w, kernels=ch.kernels)
+        best, rules, alt = ch, 0, None
+        if not args.no_rewrite:
+            w2, napp = graphs.rewritten(w, RW_ALL)
+            if napp:
+                alt = chooser.korch_plan(w2.graph, warmup=10, reps=50, **CHOOSER_LIMITS)
+                if alt.cost_us < ch.cost_us:
+                    best, rules, w = alt, RW_ALL, w2
+        chosen = graphs.plan_record(w, best.kernels, rules)
+        chosen.update({"predicted_us": round(best.cost_us, 3), "candidates": best.candidates,
+                       "search_states": best.states, "original_graph_us": round(ch.cost_us, 3),
+                       "rewritten_graph_us": round(alt.cost_us, 3) if alt else None,
+                       "choose_seconds": round(time.time() - t0, 1)})
+        r = PlanRunner(w, kernels=best.kernels)
     else:
         r = PlanRunner(w, args.plan)
     r.set_inputs(W.inputs(args.workload))

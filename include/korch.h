@@ -84,6 +84,9 @@ typedef enum {
   KORCH_SLICE,           /* [attrs.begin, attrs.end) per dim, unit step     */
   KORCH_PAD,             /* attrs.begin = low pads, attrs.end = high pads, value attrs.pad_value */
   KORCH_CONCAT,          /* along attrs.axis, n_in >= 2                     */
+  KORCH_FILL,            /* no operands: a constant tensor of shape attrs.shape (attrs.rank dims)
+                            whose every element is attrs.scalar (the ones tensor of the
+                            reduction-as-product transformation, Section 3)              */
   /* linear */
   KORCH_MATMUL = 128,    /* [..., M, K] x [..., K, N] -> [..., M, N], batch dims broadcast */
   KORCH_CONV2D           /* NHWC x HWIO cross-correlation, zero pad attrs.pad, stride attrs.stride */
@@ -147,6 +150,9 @@ int korch_graph_num_nodes(const korch_graph* g, int32_t* n);
 /* Shape / dtype / op of a node; shape must hold KORCH_MAX_RANK entries. */
 int korch_graph_node_info(const korch_graph* g, int32_t node, int32_t* op, int32_t* dtype, int32_t* rank,
                           int64_t* shape);
+/* Attributes of a node as given at creation (axis normalized for reduce and
+   concat nodes). */
+int korch_graph_node_attrs(const korch_graph* g, int32_t node, korch_attrs* attrs);
 /* The producers a node reads, in operand order: *n receives the count and at
    most `cap` ids are written to `ids` (which may be NULL when cap is 0). */
 int korch_graph_node_inputs(const korch_graph* g, int32_t node, int32_t* ids, int32_t cap, int32_t* n);
@@ -154,6 +160,21 @@ int korch_graph_num_inputs(const korch_graph* g, int32_t* n);
 int korch_graph_num_outputs(const korch_graph* g, int32_t* n);
 int korch_graph_input_node(const korch_graph* g, int32_t i, int32_t* node);
 int korch_graph_output_node(const korch_graph* g, int32_t i, int32_t* node);
+
+/* ---- primitive-graph transformations (Section 3) ------------------------ */
+typedef enum {
+  KORCH_RW_DEFER_DIV = 1,          /* (E / s) . V -> (E . V) / s, s constant along the contraction axis */
+  KORCH_RW_REDUCE_AS_PRODUCT = 2,  /* sum over an axis -> product with a ones tensor, where a product
+                                      on the same operand exists to merge with                      */
+  KORCH_RW_MERGE_PRODUCTS = 4,     /* A . B1, A . B2 -> column slices of A . concat(B1, B2)          */
+  KORCH_RW_ALL = 7
+} korch_rewrite_rule;
+/* Applies the selected rules until none applies and returns a new finalized
+   graph in *out (the caller destroys it) whose inputs and outputs correspond,
+   in order, to those of g; every output has the same value in exact
+   arithmetic.  *applied (may be NULL) receives the number of applications.
+   Node ids of *out are unrelated to those of g. */
+int korch_graph_rewrite(const korch_graph* g, uint32_t rules, korch_graph** out, int32_t* applied);
 
 /* ---- orchestration analysis (Section 4.1) ------------------------------ */
 /* Definition 1 on an arbitrary node set; *convex = 1 or 0. */

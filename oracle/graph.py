@@ -112,6 +112,8 @@ class Graph:
             return tuple(int(e) - int(b) for b, e in zip(a["begin"], a["end"]))
         if op == "pad":
             return tuple(s + int(l) + int(h) for s, l, h in zip(sh[0], a["lo"], a["hi"]))
+        if op == "fill":
+            return tuple(int(d) for d in a["shape"])
         if op == "concat":
             ax = a["axis"]
             out = list(sh[0])
@@ -172,6 +174,8 @@ def evaluate_node(g: Graph, i: int, args):
         return prim.pad(args[0], a["lo"], a["hi"], a.get("value", 0.0))
     if op == "concat":
         return prim.concat(args, a["axis"])
+    if op == "fill":
+        return prim.fill(a["shape"], a["value"])
     if op == "matmul":
         return prim.matmul(args[0], args[1])
     if op == "conv2d":

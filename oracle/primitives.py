@@ -134,6 +134,12 @@ def concat(xs, axis):
     return np.concatenate([np.asarray(x, dtype=np.float64) for x in xs], axis=axis)
 
 
+def fill(shape, value):
+    """A constant tensor (no operands): the ones tensor of the transformation that
+    writes a sum over an axis as a product (Section 3)."""
+    return np.full(tuple(int(d) for d in shape), np.float64(value))
+
+
 # ----------------------------------------------------------------------------
 # Linear transformation primitives (Section 3, "Linear transformation")
 # ----------------------------------------------------------------------------

@@ -41,9 +41,12 @@ OPS = {
     "add": 32, "sub": 33, "mul": 34, "div": 35, "max": 36, "min": 37,
     "reduce_sum": 64, "reduce_mean": 65, "reduce_max": 66, "broadcast": 67,
     "transpose": 96, "reshape": 97, "slice": 98, "pad": 99, "concat": 100,
+    "fill": 101,
     "matmul": 128, "conv2d": 129,
 }
 OP_NAMES = {v: k for k, v in OPS.items()}
+# primitive-graph transformation rules (korch_rewrite_rule)
+RW_DEFER_DIV, RW_REDUCE_AS_PRODUCT, RW_MERGE_PRODUCTS, RW_ALL = 1, 2, 4, 7
 FAMILIES = {0: "none", 1: "pointwise", 2: "row", 3: "colreduce", 4: "gemm", 5: "conv", 6: "attention", 7: "splitk"}
 
 E_UNSUPPORTED = -20
@@ -102,6 +105,8 @@ _SIGS = {
     "korch_plan_kernel_source": ([_P, _I, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_kernel_name": ([_P, _I, C.c_char_p, C.c_size_t], C.c_int),
     "korch_plan_kernel_launch": ([_P, _I, C.POINTER(_I), C.POINTER(_I), C.POINTER(_I)], C.c_int),
+    "korch_graph_node_attrs": ([_P, _I, C.POINTER(korch_attrs)], C.c_int),
+    "korch_graph_rewrite": ([_P, C.c_uint32, C.POINTER(_P), C.POINTER(_I)], C.c_int),
     "korch_compile_candidate": ([_P, C.POINTER(korch_kernel_desc)], C.c_int),
     "korch_profile_candidate": ([_P, C.POINTER(korch_kernel_desc), _I, _I, C.c_size_t, _P, C.POINTER(C.c_float)],
                                 C.c_int),
@@ -193,6 +198,24 @@ class Graph:
         n = _I()
         check(lib.korch_graph_num_nodes(self.h, C.byref(n)))
         return n.value
+
+    def node_attrs(self, node):
+        """Attributes of a node (as a dict; the reduce / concat axis normalized)."""
+        a = korch_attrs()
+        check(lib.korch_graph_node_attrs(self.h, int(node), C.byref(a)))
+        r = a.rank
+        return dict(axis=a.axis, keepdim=bool(a.keepdim), perm=tuple(a.perm[i] for i in range(r)),
+                    shape=tuple(a.shape[i] for i in range(r)), begin=tuple(a.begin[i] for i in range(r)),
+                    end=tuple(a.end[i] for i in range(r)), scalar=a.scalar if a.has_scalar else None,
+                    value=a.scalar, stride=a.stride, pad=a.pad, pad_value=a.pad_value)
+
+    def rewrite(self, rules=RW_ALL):
+        """New graph after the primitive-graph transformations; (graph, applications)."""
+        h, n = _P(), _I()
+        check(lib.korch_graph_rewrite(self.h, int(rules), C.byref(h), C.byref(n)))
+        g = Graph.__new__(Graph)
+        g.h = h
+        return g, n.value
 
     def node_info(self, node):
         op, dt, rank = _I(), _I(), _I()

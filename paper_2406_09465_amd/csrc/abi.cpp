@@ -19,6 +19,7 @@ struct korch_plan {
 };
 
 namespace korch {
+Graph rewrite_graph(const Graph& g, uint32_t rules, int* applied);
 void compile_plan(Plan& p);
 void generate_plan(Plan& p);
 void load_plan(Plan& p);
@@ -151,6 +152,35 @@ int korch_graph_num_nodes(const korch_graph* g, int32_t* n) {
     NEED(g);
     NEED(n);
     *n = (int32_t)g->g.nodes.size();
+  });
+}
+
+int korch_graph_node_attrs(const korch_graph* g, int32_t node, korch_attrs* attrs) {
+  return guard([&] {
+    NEED(g);
+    NEED(attrs);
+    if (node < 0 || node >= (int)g->g.nodes.size()) fail(KORCH_E_ARG, "node id out of range");
+    const Node& n = g->g.nodes[node];
+    *attrs = n.attrs;
+    if (op_kind(n.op) == Kind::Reduce || n.op == KORCH_CONCAT) attrs->axis = n.axis;
+  });
+}
+
+int korch_graph_rewrite(const korch_graph* g, uint32_t rules, korch_graph** out, int32_t* applied) {
+  return guard([&] {
+    NEED(g);
+    NEED(out);
+    if (!g->g.finalized) fail(KORCH_E_STATE, "graph is not finalized");
+    int n = 0;
+    korch_graph* r = new korch_graph();
+    try {
+      r->g = rewrite_graph(g->g, rules, &n);
+    } catch (...) {
+      delete r;
+      throw;
+    }
+    *out = r;
+    if (applied) *applied = n;
   });
 }
 

@@ -409,7 +409,9 @@ std::string Emitter::value(int node, const std::vector<Ix>& idx) {
       out = value(n.in[0], broadcast_index(in_shape(0), n.shape, idx));
       break;
     case Kind::Layout: {
-      if (n.op == KORCH_TRANSPOSE) {
+      if (n.op == KORCH_FILL) {
+        out = flit(n.attrs.scalar);
+      } else if (n.op == KORCH_TRANSPOSE) {
         std::vector<Ix> src(idx.size());
         for (size_t d = 0; d < idx.size(); ++d) src[n.attrs.perm[d]] = idx[d];
         out = value(n.in[0], src);

@@ -609,6 +609,11 @@ int match_family(const Graph& g, const KernelDesc& k, std::string* why) {
   if (!why) why = &w;
   try {
     KInfo ki(g, k);
+    // A constant tensor is evaluated inline by the pointwise emitter and by
+    // product prologues; the row programs take only computed operands.
+    bool has_fill = false;
+    for (int v : k.prims)
+      if (g.nodes[v].op == KORCH_FILL) has_fill = true;
     if (!ki.linear.empty()) {
       if (match_attention(ki, why)) return KORCH_FAM_ATTENTION;
       if (match_conv(ki, why)) return KORCH_FAM_CONV;
@@ -617,6 +622,10 @@ int match_family(const Graph& g, const KernelDesc& k, std::string* why) {
       return KORCH_FAM_NONE;
     }
     if (!ki.reduces.empty()) {
+      if (has_fill) {
+        *why = "row programs do not evaluate constant tensors";
+        return KORCH_FAM_NONE;
+      }
       if (match_row(ki, why)) return KORCH_FAM_ROW;
       if (match_colreduce(ki, why)) return KORCH_FAM_COLREDUCE;
       return KORCH_FAM_NONE;

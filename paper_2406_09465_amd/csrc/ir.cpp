@@ -39,7 +39,7 @@ Kind op_kind(int op) {
   if (op >= KORCH_ADD && op <= KORCH_MIN) return Kind::Binary;
   if (op >= KORCH_REDUCE_SUM && op <= KORCH_REDUCE_MAX) return Kind::Reduce;
   if (op == KORCH_BROADCAST) return Kind::Broadcast;
-  if (op >= KORCH_TRANSPOSE && op <= KORCH_CONCAT) return Kind::Layout;
+  if (op >= KORCH_TRANSPOSE && op <= KORCH_FILL) return Kind::Layout;
   if (op == KORCH_MATMUL || op == KORCH_CONV2D) return Kind::Linear;
   fail(KORCH_E_ARG, "unknown op code " + std::to_string(op));
 }
@@ -79,6 +79,7 @@ const char* op_name(int op) {
     case KORCH_SLICE: return "slice";
     case KORCH_PAD: return "pad";
     case KORCH_CONCAT: return "concat";
+    case KORCH_FILL: return "fill";
     case KORCH_MATMUL: return "matmul";
     case KORCH_CONV2D: return "conv2d";
   }
@@ -170,6 +171,14 @@ int Graph::add_op(int op, const std::vector<int>& in, const korch_attrs* attrs, 
       break;
     }
     case Kind::Layout: {
+      if (op == KORCH_FILL) {
+        need(0);
+        if (a.rank < 0 || a.rank > KORCH_MAX_RANK) fail(KORCH_E_SHAPE, "bad rank");
+        n.shape.assign(a.shape, a.shape + a.rank);
+        for (auto d : n.shape)
+          if (d <= 0) fail(KORCH_E_SHAPE, "fill dims must be positive");
+        break;
+      }
       if (op == KORCH_CONCAT) {
         if (in.size() < 2) fail(KORCH_E_ARG, "concat takes >= 2 inputs");
         int r = (int)sh(0).size();

@@ -230,5 +230,32 @@ def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6):
 BUILDERS = {"attention": attention, "mlp": mlp, "sra": sra, "conv": conv, "linattn": linattn}
 
 
+def rewritten(w: Workload, rules=None):
+    """The workload's graph after the primitive-graph transformations
+    (korch_graph_rewrite), with the same input and output names; returns
+    (workload, number of rule applications).  It has no hand-written plans."""
+    from ._abi import RW_ALL
+    g2, n = w.graph.rewrite(RW_ALL if rules is None else rules)
+    ids = dict(zip(w.input_names, g2.inputs()))
+    ids.update(zip(w.output_names, g2.outputs()))
+    return Workload(w.name, w.dtype, g2, ids, list(w.input_names), list(w.output_names), sizes=dict(w.sizes)), n
+
+
+def plan_record(w: Workload, kernels, rules=0):
+    """JSON-able record of a plan of ``w`` (or of its rewritten graph when
+    ``rules`` is non-zero): node ids, plus names where the workload names them."""
+    names = {v: k for k, v in w.ids.items()} if not rules else {}
+    return {"graph": "rewritten" if rules else "original", "rules": int(rules),
+            "kernel_ids": [[list(map(int, p)), list(map(int, o))] for p, o in kernels],
+            "kernels": [[[names.get(v, f"#{v}") for v in p], [names.get(v, f"#{v}") for v in o]] for p, o in kernels]}
+
+
+def plan_from_record(w: Workload, rec):
+    """(workload, kernels) of a record written by plan_record."""
+    if rec.get("rules"):
+        w, _ = rewritten(w, rec["rules"])
+    return w, [(list(p), list(o)) for p, o in rec["kernel_ids"]]
+
+
 def build(workload: str, **sizes) -> Workload:
     return BUILDERS[workload](**sizes)

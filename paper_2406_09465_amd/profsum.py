@@ -64,7 +64,7 @@ def pmc(args):
     if args.bench_json:
         # the plan bench.py ran (e.g. the measured-cost choice), by node names
         d = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
-        ks = [([w.ids[n] for n in pr], [w.ids[n] for n in ou]) for pr, ou in d["chosen_plan"]["kernels"]]
+        w, ks = graphs.plan_from_record(w, d["chosen_plan"])
         p = graphs.Plan(w.graph, ks)
     else:
         p = w.plan(args.plan)

@@ -44,6 +44,7 @@ def _jobs():
     for w, sizes in CHOOSER.items():
         for sz in sizes:
             jobs.append(("candidates", w, sz, None))
+            jobs.append(("candidates", w, sz, "rewritten"))
     return jobs
 
 
@@ -65,6 +66,10 @@ def _run_job(job, part=0, parts=1):
             except KorchError as e:
                 failures.append((w, sz, f"sampled {i}", str(e)[:200]))
     else:
+        if extra == "rewritten":
+            wl, n = graphs.rewritten(wl)
+            if n == 0:
+                return failures
         cands = wl.graph.candidates(only_supported=True, **CHOOSER_LIMITS)
         for c in cands[part::parts]:
             try:

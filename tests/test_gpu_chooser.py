@@ -49,3 +49,25 @@ def test_chosen_plan(workload):
     for name in w.output_names:
         ok, mx, rel = close(out[name], ref[name], TOL[w.dtype])
         assert ok, f"{workload} chosen plan {ch.kernels}: max err {mx:.3e} rel {rel:.3e}"
+
+
+@pytest.mark.parametrize("workload", ["attention", "sra", "linattn"])
+def test_chosen_plan_of_transformed_graph(workload):
+    """Orchestration of the rewritten primitive graph (Section 3 transformations):
+    the chosen plan must reproduce the oracle of the original graph."""
+    from paper_2406_09465_amd import chooser, graphs
+    from paper_2406_09465_amd.runner import PlanRunner
+    from paper_2406_09465_amd.warm import CHOOSER_LIMITS
+    sizes = SIZES[workload]
+    w, napp = graphs.rewritten(graphs.build(workload, **sizes))
+    assert napp > 0
+    print(f"\n[case] {workload} transformed graph at {sizes}", flush=True)
+    ch = chooser.korch_plan(w.graph, warmup=3, reps=10, flush_bytes=64 << 20, **CHOOSER_LIMITS)
+    print(f"[case] {workload}: {ch.candidates} candidates, chosen {len(ch.kernels)} kernels, {ch.cost_us:.1f} us",
+          flush=True)
+    raw, x64 = inputs_f64(workload, **sizes)
+    ref = run_unfused(OC.build(workload, **sizes), x64)
+    out = PlanRunner(w, kernels=ch.kernels).run(raw)
+    for name in w.output_names:
+        ok, mx, rel = close(out[name], ref[name], TOL[w.dtype])
+        assert ok, f"{workload} transformed plan {ch.kernels}: max err {mx:.3e} rel {rel:.3e}"

@@ -1,0 +1,151 @@
+"""Primitive-graph transformations (Section 3): every rewritten graph computes
+the same outputs as the original in float64 (the oracle executes both), the
+rules produce the intended structure, and they never create cycles."""
+
+import numpy as np
+import pytest
+
+from oracle import configs as OC
+from oracle import primitives as prim
+from oracle.graph import Graph as OGraph
+from oracle.graph import run_unfused
+from paper_2406_09465_amd import _abi as K
+from paper_2406_09465_amd import graphs
+from synthetic import storage_to_f64
+from synthetic import workloads as W
+
+SMALL = {
+    "attention": dict(n=40, d=24),
+    "mlp": dict(m=48, d=32, h=40),
+    "sra": dict(hh=16, ww=16, c=8, r=4),
+    "conv": dict(hh=9, ww=7, cin=8, cout=16),
+    "linattn": dict(heads=3, n=50, d=8),
+}
+RULESETS = [K.RW_DEFER_DIV, K.RW_REDUCE_AS_PRODUCT, K.RW_MERGE_PRODUCTS,
+            K.RW_REDUCE_AS_PRODUCT | K.RW_MERGE_PRODUCTS, K.RW_ALL]
+
+
+def to_oracle(g):
+    """The oracle's copy of a library graph (ops, operands and attributes read
+    back through the C ABI); inputs are named in0, in1, ..."""
+    og = OGraph()
+    names = {}
+    for k, v in enumerate(g.inputs()):
+        names[v] = k
+    for v in range(g.num_nodes()):
+        op, dt, shape = g.node_info(v)
+        if op == "input":
+            og.input(f"in{names[v]}", shape, dtype=dt)
+            continue
+        a = g.node_attrs(v)
+        at = {"dtype": dt}
+        if op in ("reduce_sum", "reduce_mean", "reduce_max"):
+            at.update(axis=a["axis"], keepdim=a["keepdim"])
+        elif op in ("broadcast", "reshape"):
+            at.update(shape=a["shape"])
+        elif op == "transpose":
+            at.update(perm=a["perm"])
+        elif op == "slice":
+            at.update(begin=a["begin"], end=a["end"])
+        elif op == "pad":
+            at.update(lo=a["begin"], hi=a["end"], value=a["pad_value"])
+        elif op == "concat":
+            at.update(axis=a["axis"])
+        elif op == "fill":
+            at.update(shape=a["shape"], value=a["value"])
+        elif op == "conv2d":
+            at.update(stride=a["stride"], pad=a["pad"])
+        elif a["scalar"] is not None:
+            at.update(scalar=a["scalar"])
+        og.op(op, g.node_inputs(v), **at)
+        assert og.nodes[-1].shape == shape, (v, op)
+    for o in g.outputs():
+        og.output(o)
+    return og
+
+
+def outputs_by_position(og, x64_by_position):
+    vals = run_unfused(og, {f"in{k}": x for k, x in enumerate(x64_by_position)})
+    return [vals[og.nodes[o].name] for o in og.outputs]
+
+
+def test_fill_as_ones_column_gives_row_sums():
+    """Pin of the oracle's constant tensor: X . ones = the row sums of X."""
+    x = np.random.default_rng(0).normal(size=(5, 7, 9))
+    assert np.allclose(prim.matmul(x, prim.fill((9, 1), 1.0))[..., 0], x.sum(axis=-1), rtol=1e-14, atol=1e-13)
+    assert prim.fill((2, 3), 2.5).shape == (2, 3) and np.all(prim.fill((2, 3), 2.5) == 2.5)
+
+
+@pytest.mark.parametrize("rules", RULESETS)
+@pytest.mark.parametrize("workload", list(SMALL))
+def test_rewrite_preserves_outputs(workload, rules):
+    sz = SMALL[workload]
+    w = graphs.build(workload, **sz)
+    g2, n = w.graph.rewrite(rules)
+    assert len(g2.inputs()) == len(w.graph.inputs()) and len(g2.outputs()) == len(w.graph.outputs())
+    raw = W.inputs(workload, **sz)
+    x64 = [storage_to_f64(raw[name], w.dtype) for name in w.input_names]
+    ref = run_unfused(OC.build(workload, **sz), dict(zip(w.input_names, x64)))
+    got = outputs_by_position(to_oracle(g2), x64)
+    for name, y in zip(w.output_names, got):
+        r = ref[name]
+        assert y.shape == r.shape
+        assert np.max(np.abs(y - r)) <= 1e-10 * max(1.0, np.max(np.abs(r))), (workload, rules, n)
+
+
+def kinds(g):
+    return [g.node_info(v)[0] for v in range(g.num_nodes())]
+
+
+def test_linear_attention_becomes_two_products():
+    """K^T [V | 1] gives KV and the key sums in one contraction; the query
+    products then merge as Q [KV | sum K]."""
+    w = graphs.build("linattn", **SMALL["linattn"])
+    g2, n = w.graph.rewrite(K.RW_ALL)
+    ops = kinds(g2)
+    assert n >= 3 and ops.count("matmul") == 2 and "reduce_sum" not in ops
+    first = min(v for v in range(g2.num_nodes()) if g2.node_info(v)[0] == "matmul")
+    a, b = g2.node_inputs(first)
+    assert g2.node_info(a)[0] == "transpose" and g2.node_info(b)[0] == "concat"
+    parts = [g2.node_info(u)[0] for u in g2.node_inputs(b)]
+    assert parts[0] == "input" and parts[1] == "fill"
+
+
+def test_attention_normalizes_after_the_product():
+    w = graphs.build("attention", **SMALL["attention"])
+    g2, _ = w.graph.rewrite(K.RW_DEFER_DIV)
+    out = g2.outputs()[0]
+    assert g2.node_info(out)[0] == "div"
+    assert g2.node_info(g2.node_inputs(out)[0])[0] == "matmul"
+    g3, _ = w.graph.rewrite(K.RW_ALL)
+    assert "reduce_sum" not in kinds(g3) and kinds(g3).count("matmul") == 2
+
+
+def test_merge_refuses_a_cycle():
+    """M2's right operand depends on M1: merging them would need C before M1."""
+    g = K.Graph()
+    a = g.input("f32", (8, 4))
+    b1 = g.input("f32", (4, 4))
+    m1 = g.op("matmul", [a, b1], "f32")
+    b2 = g.op("transpose", [m1], "f32", perm=(1, 0))
+    b2b = g.op("slice", [b2], "f32", begin=(0, 0), end=(4, 4))
+    m2 = g.op("matmul", [a, b2b], "f32")
+    g.output(m2)
+    g.finalize()
+    g2, n = g.rewrite(K.RW_MERGE_PRODUCTS)
+    assert n == 0 and kinds(g2).count("matmul") == 2
+
+
+@pytest.mark.parametrize("workload", list(SMALL))
+def test_rewrite_is_idempotent(workload):
+    w = graphs.build(workload, **SMALL[workload])
+    g2, _ = w.graph.rewrite(K.RW_ALL)
+    _, n = g2.rewrite(K.RW_ALL)
+    assert n == 0
+
+
+def test_rewritten_workload_keeps_names():
+    w = graphs.build("linattn", **SMALL["linattn"])
+    w2, n = graphs.rewritten(w)
+    assert n > 0 and w2.input_names == w.input_names and w2.output_names == w.output_names
+    assert [w2.ids[k] for k in w2.input_names] == w2.graph.inputs()
