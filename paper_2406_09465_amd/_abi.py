@@ -50,6 +50,7 @@ RW_DEFER_DIV, RW_REDUCE_AS_PRODUCT, RW_MERGE_PRODUCTS, RW_ALL = 1, 2, 4, 7
 FAMILIES = {0: "none", 1: "pointwise", 2: "row", 3: "colreduce", 4: "gemm", 5: "conv", 6: "attention", 7: "splitk"}
 
 E_UNSUPPORTED = -20
+E_COMPILE = -23
 
 
 class korch_attrs(C.Structure):

@@ -33,6 +33,7 @@ class Choice:
     states: int                   # availability states expanded by the search
     candidates: int               # candidates with a finite cost
     costs: dict = field(default_factory=dict)   # (prims, outs) -> us
+    failures: list = field(default_factory=list)  # candidates whose kernel did not compile
 
 
 def _masks(view: GraphView):
@@ -103,13 +104,22 @@ def plan_cost(view: GraphView, kernels, cost_of) -> float:
     return sum(cost_of[(tuple(p), tuple(o))] for p, o in kernels)
 
 
-def profile_candidates(graph, cands, warmup=10, reps=50, flush_bytes=512 << 20, log=None):
+def profile_candidates(graph, cands, warmup=10, reps=50, flush_bytes=512 << 20, log=None, failures=None):
     """Measured latency (us) of every candidate on the current device, None when
-    no family implements it."""
+    no family implements it.  A candidate whose generated kernel fails to
+    compile also costs infinity; it is appended to ``failures`` when given."""
+    from ._abi import E_COMPILE, KorchError
     costs = []
     t0 = time.time()
     for i, (p, o) in enumerate(cands):
-        costs.append(graph.profile(p, o, warmup=warmup, reps=reps, flush_bytes=flush_bytes))
+        try:
+            costs.append(graph.profile(p, o, warmup=warmup, reps=reps, flush_bytes=flush_bytes))
+        except KorchError as e:
+            if e.code != E_COMPILE:
+                raise
+            costs.append(None)
+            if failures is not None:
+                failures.append(((tuple(p), tuple(o)), str(e)[:300]))
         if log and (i + 1) % 50 == 0:
             log(f"profiled {i + 1}/{len(cands)} candidates ({time.time() - t0:.1f} s)")
     return costs
@@ -127,7 +137,9 @@ def korch_plan(graph, max_prims=64, max_outs=3, warmup=10, reps=50, flush_bytes=
         if k not in seen:
             seen.add(k)
             cands.append(k)
-    costs = profile_candidates(graph, cands, warmup, reps, flush_bytes, log)
+    failures = []
+    costs = profile_candidates(graph, cands, warmup, reps, flush_bytes, log, failures)
     ch = choose(GraphView(graph), cands, costs)
     ch.costs = {(tuple(p), tuple(o)): c for (p, o), c in zip(cands, costs) if c is not None}
+    ch.failures = failures
     return ch

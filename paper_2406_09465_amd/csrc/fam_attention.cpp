@@ -139,9 +139,27 @@ static bool analyze_attention(const KInfo& ki, AttnSpec& a, std::string* why) {
   return true;
 }
 
+// LDS bytes of the kernel: all keys, all values and one score tile per wave.
+static size_t attention_lds_bytes(const AttnSpec& a) {
+  bool f32 = a.dtype == KORCH_F32;
+  int kstep = f32 ? 4 : 32;
+  int64_t dpad = (a.d + kstep - 1) / kstep * kstep;
+  int64_t nkp = f32 ? (a.nk + 15) / 16 * 16 : (a.nk + 31) / 32 * 32;
+  int64_t KSP = dpad + (f32 ? 4 : 8), NKP = nkp + (f32 ? 4 : 8);
+  int64_t dvp = (a.dv + 15) / 16 * 16, VP = dvp + 4;
+  size_t ks = (size_t)(nkp * KSP * dtype_bytes(a.dtype));
+  size_t v = f32 ? (size_t)(nkp * VP * 4) : (size_t)(dvp * NKP * 2);
+  return ks + v + (size_t)(4 * 16 * NKP * dtype_bytes(a.dtype));
+}
+
 bool match_attention(const KInfo& ki, std::string* why) {
   AttnSpec a;
-  return analyze_attention(ki, a, why);
+  if (!analyze_attention(ki, a, why)) return false;
+  if (attention_lds_bytes(a) > 160 * 1024) {
+    *why = "attention: keys and values exceed the 160 KiB of LDS";
+    return false;
+  }
+  return true;
 }
 
 GenKernel gen_attention(const KInfo& ki, int index) {
@@ -168,6 +186,8 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   size_t v_bytes = f32 ? (size_t)nkp * VP * 4 : (size_t)dvp * NKP * 2;
   size_t p_bytes = (size_t)4 * 16 * NKP * dtype_bytes(a.dtype);
   size_t smem = ks_bytes + v_bytes + p_bytes;
+  if (smem != attention_lds_bytes(a) || smem > 160 * 1024)
+    fail(KORCH_E_UNSUPPORTED, "attention: keys and values exceed the 160 KiB of LDS");
   std::string Q = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.q)) + "])";
   std::string K = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.kx)) + "])";
   std::string V = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.v)) + "])";

@@ -40,6 +40,7 @@ def test_chosen_plan(workload):
                             extra=[k for ks in hand.values() for k in ks], **CHOOSER_LIMITS)
     print(f"[case] {workload}: {ch.candidates} candidates, chosen {len(ch.kernels)} kernels, "
           f"{ch.cost_us:.1f} us", flush=True)
+    assert not ch.failures, ch.failures[:2]
     for name, ks in hand.items():
         c = sum(ch.costs[(tuple(sorted(p)), tuple(sorted(o)))] for p, o in ks)
         assert ch.cost_us <= c + 1e-6, (name, c)
