@@ -36,6 +36,7 @@ DESCR = {
     "sra": "spatial-reduction attention fp16: 128x128x64 map, 8x8 patch merge 4096->64, LayerNorm, 16384x256 softmax",
     "conv": "conv3x3 NHWC fp16 416x416x32->64 + BatchNorm scale/shift + Mish",
     "linattn": "ReLU linear attention bf16, 16 heads x 4096 tokens x d16",
+    "instnorm": "InstanceNorm + ReLU + zero Pad fp16 NHWC 224x224x32 -> 226x226x32",
 }
 
 

@@ -143,7 +143,34 @@ def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6):
     return g
 
 
-BUILDERS = {"attention": attention, "mlp": mlp, "sra": sra, "conv": conv, "linattn": linattn}
+def instnorm(hh=224, ww=224, c=32, dtype="f16", eps=1e-5):
+    """Candy's InstanceNorm -> ReLU -> Pad pattern (Section 6 case study) in
+    NHWC at batch 1: per-channel statistics over all pixels (mean, subtract,
+    square, mean = biased variance, add eps, reciprocal square root), normalize,
+    per-channel affine, ReLU, then one pixel of zero padding on each side of
+    the two spatial axes for the next 3x3 convolution."""
+    g = Graph(dtype)
+    x = g.input("X", (hh, ww, c))
+    gamma = g.input("gamma", (c,))
+    beta = g.input("beta", (c,))
+    xp = g.op("reshape", [x], name="Xp", shape=(hh * ww, c))
+    mu = g.op("reduce_mean", [xp], name="mu", axis=0, keepdim=True)
+    d = g.op("sub", [xp, mu], name="D")
+    d2 = g.op("square", [d], name="D2")
+    var = g.op("reduce_mean", [d2], name="var", axis=0, keepdim=True)
+    ve = g.op("add", [var], name="ve", scalar=eps)
+    r = g.op("rsqrt", [ve], name="r")
+    xh = g.op("mul", [d, r], name="Xh")
+    yg = g.op("mul", [xh, gamma], name="Yg")
+    y = g.op("add", [yg, beta], name="Y")
+    rl = g.op("relu", [y], name="R")
+    ri = g.op("reshape", [rl], name="Ri", shape=(hh, ww, c))
+    out = g.op("pad", [ri], name="out", lo=(1, 1, 0), hi=(1, 1, 0), value=0.0)
+    g.output(out)
+    return g
+
+
+BUILDERS = {"attention": attention, "mlp": mlp, "sra": sra, "conv": conv, "linattn": linattn, "instnorm": instnorm}
 
 
 def build(workload: str, **shape):

@@ -499,8 +499,8 @@ bool match_colreduce(const KInfo& ki, std::string* why) {
       *why = "colreduce: prologue node shape differs";
       return false;
     }
-    if (pro && std::find(ki.k.outs.begin(), ki.k.outs.end(), v) != ki.k.outs.end()) {
-      *why = "colreduce: prologue node cannot be an output";
+    if (pro && std::find(ki.k.outs.begin(), ki.k.outs.end(), v) != ki.k.outs.end() && g.nodes[v].shape != S) {
+      *why = "colreduce: a prologue output must have the reduced operand's shape";
       return false;
     }
     if (epi && g.nodes[v].shape != rn.shape) {
@@ -511,6 +511,14 @@ bool match_colreduce(const KInfo& ki, std::string* why) {
   return true;
 }
 
+// Column reduction: the reduced operand is [A.., L (axis), B..]; out[a][b] =
+// combine over l of f(x[a][l][b]).  A workgroup of 256 threads is BB lanes
+// along b (VB consecutive b each, vector loads when the innermost dimension
+// allows) by LY rows along l.  When the kept columns alone give few
+// workgroups, l is split over SPLIT workgroups: each writes fp32 partials, and
+// the last to finish (device-scope counter, one release by thread 0, reset by
+// that workgroup) sums them in split order (deterministic) and runs the
+// epilogue.
 GenKernel gen_colreduce(const KInfo& ki, int index) {
   const Graph& g = ki.g;
   std::string why;
@@ -525,11 +533,21 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
   int X = rn.in[0];
   const Shape& S = g.nodes[X].shape;
   int ax = rn.axis;
+  const int R = (int)S.size();
   int64_t A = 1, B = 1, Lr = S[ax];
   for (int d = 0; d < ax; ++d) A *= S[d];
-  for (size_t d = ax + 1; d < S.size(); ++d) B *= S[d];
-  int BB = B >= 64 ? 64 : (int)pow2ceil(B);
+  for (int d = ax + 1; d < R; ++d) B *= S[d];
+  const int64_t Bin = S[R - 1];  // innermost kept dimension (ax < R - 1)
+  int VB = Bin % 8 == 0 ? 8 : (Bin % 4 == 0 ? 4 : (Bin % 2 == 0 ? 2 : 1));
+  const int64_t BV = B / VB;  // vector columns
+  int BB = BV >= 64 ? 64 : (int)pow2ceil(BV);
   int LY = 256 / BB;
+  const int64_t ctiles = (BV + BB - 1) / BB;
+  // split the reduced axis so that about 256 workgroups run, each with at least
+  // 8 rows per thread
+  int64_t SPLIT = std::max<int64_t>(1, std::min<int64_t>((256 + ctiles * A - 1) / (ctiles * A), Lr / (4 * LY)));
+  int64_t chunk = (Lr + SPLIT - 1) / SPLIT;
+  SPLIT = (Lr + chunk - 1) / chunk;
   bool isMax = rn.op == KORCH_REDUCE_MAX;
   std::string ident = isMax ? "-__builtin_huge_valf()" : "0.0f";
   auto comb = [&](const std::string& x, const std::string& y) {
@@ -538,64 +556,130 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
   std::vector<Ix> xi(S.size());
   for (int d = 0; d < ax; ++d) xi[d] = Ix::var("a" + std::to_string(d));
   xi[ax] = Ix::var("l");
-  for (size_t d = ax + 1; d < S.size(); ++d) xi[d] = Ix::var("b" + std::to_string(d));
+  for (int d = ax + 1; d < R; ++d)
+    xi[d] = d == R - 1 ? Ix::var("b" + std::to_string(d), 1, VB) : Ix::var("b" + std::to_string(d));
   Emitter pe(g);
   pe.inset = ki.in;
   pe.argslot = slot;
-  pe.vec = 1;
+  pe.vec = VB;
   std::string xv = pe.value(X, xi);
-  // epilogue
+  // epilogue over the reduced shape
   std::vector<Ix> ri;
   for (int d = 0; d < ax; ++d) ri.push_back(xi[d]);
-  if ((int)rn.shape.size() == (int)S.size()) ri.push_back(Ix::k(0));
-  for (size_t d = ax + 1; d < S.size(); ++d) ri.push_back(xi[d]);
+  if ((int)rn.shape.size() == R) ri.push_back(Ix::k(0));
+  for (int d = ax + 1; d < R; ++d) ri.push_back(xi[d]);
   Emitter ee(g);
   ee.inset = ki.in;
   ee.argslot = slot;
-  ee.vec = 1;
+  ee.vec = VB;
   std::string rkey = Emitter::key(r, ri);
   ee.provide = [&](int node, const std::vector<Ix>& idx, std::string* out) {
     if (node != r) return false;
     if (Emitter::key(node, idx) != rkey) fail(KORCH_E_UNSUPPORTED, "colreduce: reduction read at another index");
-    *out = "s";
+    *out = "s[e]";
     return true;
   };
-  std::ostringstream st;
+  // prologue outputs (same shape as the reduced operand) are stored in the loop
+  std::set<int> pro_out;
+  for (int o : ki.k.outs)
+    if (o != r && ki.ancestor(o, r)) {
+      pro_out.insert(o);
+      std::string v = pe.value(o, xi);
+      auto strd = strides_of(S);
+      Ix off = Ix::k(0);
+      for (int d = 0; d < R; ++d) off = ix_add(off, ix_mulk(xi[d], strd[d], VB));
+      pe.body << "      if (bv) st1((" << ctype(g.nodes[o].dtype) << "*)a.p[" << ki.out_slot(o) << "] + " << off.at()
+              << ", " << v << ");\n";
+    }
   for (int o : ki.k.outs) {
+    if (pro_out.count(o)) continue;
     const Node& on = g.nodes[o];
     auto bi = broadcast_index(on.shape, rn.shape, ri);
     std::string v = ee.value(o, bi);
     auto strd = strides_of(on.shape);
     Ix off = Ix::k(0);
-    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], strd[d], 1));
-    st << "      st1((" << ctype(on.dtype) << "*)a.p[" << ki.out_slot(o) << "] + " << off.at() << ", " << v << ");\n";
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], strd[d], VB));
+    ee.body << "        st1((" << ctype(on.dtype) << "*)a.p[" << ki.out_slot(o) << "] + " << off.at() << ", " << v
+            << ");\n";
+  }
+  int scr_slot = -1, cnt_slot = -1;
+  if (SPLIT > 1) {
+    ArgRef scr;
+    scr.kind = ArgRef::Scratch;
+    scr.bytes = (size_t)(A * SPLIT * B) * 4;
+    scr_slot = (int)gk.args.size();
+    gk.args.push_back(scr);
+    ArgRef cnt;
+    cnt.kind = ArgRef::Counter;
+    cnt.bytes = (size_t)(A * ctiles) * 4;
+    cnt_slot = (int)gk.args.size();
+    gk.args.push_back(cnt);
   }
   std::ostringstream s;
   s << source_header((int)gk.args.size());
   s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
-  s << "  __shared__ float red[256];\n";
-  s << "  const int bl = threadIdx.x % " << BB << ", ly = threadIdx.x / " << BB << ";\n";
-  s << "  const i64 bi0 = (i64)blockIdx.x * " << BB << " + bl;\n";
-  s << "  const bool bv = bi0 < " << B << "LL;\n";
-  s << "  const i64 bi = bv ? bi0 : " << B - 1 << "LL;\n";
-  s << "  i64 q_ = blockIdx.y;\n";
+  s << "  __shared__ float red[256 * " << VB << "];\n";
+  if (SPLIT > 1) s << "  __shared__ int last_;\n";
+  s << "  const int tid = threadIdx.x, bl = tid % " << BB << ", ly = tid / " << BB << ";\n";
+  s << "  const i64 bv0 = (i64)blockIdx.x * " << BB << " + bl;\n";
+  s << "  const bool bv = bv0 < " << BV << "LL;\n";
+  s << "  const i64 bi = (bv ? bv0 : " << BV - 1 << "LL) * " << VB << ";\n";
+  s << "  const i64 ay = blockIdx.y;\n  i64 q_ = ay;\n";
   for (int d = ax - 1; d >= 0; --d) s << "  const i64 a" << d << " = q_ % " << S[d] << "LL; q_ /= " << S[d] << "LL;\n";
   s << "  q_ = bi;\n";
-  for (int d = (int)S.size() - 1; d > ax; --d)
-    s << "  const i64 b" << d << " = q_ % " << S[d] << "LL; q_ /= " << S[d] << "LL;\n";
-  s << "  float acc = " << ident << ";\n";
-  s << "  for (i64 l = ly; l < " << Lr << "LL; l += " << LY << ") {\n  const int e = 0; (void)e;\n"
-    << pe.pre.str() << pe.body.str() << "    acc = " << comb("acc", xv) << ";\n  }\n";
-  s << "  red[threadIdx.x] = acc;\n  __syncthreads();\n";
-  s << "  if (ly == 0) {\n    float s = red[bl];\n";
-  s << "    for (int y = 1; y < " << LY << "; ++y) s = " << comb("s", "red[y * " + std::to_string(BB) + " + bl]")
-    << ";\n";
-  if (rn.op == KORCH_REDUCE_MEAN) s << "    s = s / " << flit((double)Lr) << ";\n";
-  s << "    if (bv) {\n      const i64 l = 0; (void)l; const int e = 0; (void)e;\n"
-    << ee.pre.str() << ee.body.str() << st.str() << "    }\n  }\n}\n";
+  for (int d = R - 1; d > ax; --d) s << "  const i64 b" << d << " = q_ % " << S[d] << "LL; q_ /= " << S[d] << "LL;\n";
+  s << "  const i64 l0 = (i64)blockIdx.z * " << chunk << ", l1 = l0 + " << chunk << " < " << Lr << "LL ? l0 + " << chunk
+    << " : " << Lr << "LL;\n";
+  s << "  float acc[" << VB << "];\n#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) acc[e] = " << ident << ";\n";
+  s << "#pragma unroll 4\n  for (i64 l = l0 + ly; l < l1; l += " << LY << ") {\n" << pe.pre.str() << "#pragma unroll\n    for (int e = 0; e < "
+    << VB << "; ++e) {\n" << pe.body.str() << "      acc[e] = " << comb("acc[e]", xv) << ";\n    }\n  }\n";
+  s << "#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) red[e * 256 + tid] = acc[e];\n  __syncthreads();\n";
+  // fixed-order combine of the LY rows of this workgroup: s[e] for column bi + e
+  s << "  float s[" << VB << "];\n";
+  s << "  if (ly == 0) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n      s[e] = red[e * 256 + bl];\n"
+    << "      for (int y = 1; y < " << LY << "; ++y) s[e] = " << comb("s[e]", "red[e * 256 + y * " + std::to_string(BB) + " + bl]")
+    << ";\n    }\n  }\n";
+  if (SPLIT > 1) {
+    s << "  float* part = (float*)a.p[" << scr_slot << "];\n";
+    s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) part[(ay * " << SPLIT
+      << " + blockIdx.z) * " << B << "LL + bi + e] = s[e];\n  }\n";
+    s << "  __syncthreads();\n";
+    s << "  const i64 tix = ay * " << ctiles << " + blockIdx.x;\n";
+    s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n    __threadfence();\n";
+    s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);\n";
+    s << "    last_ = (old == " << SPLIT - 1 << ");\n";
+    s << "    if (last_) {\n      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n"
+      << "      __threadfence();\n    }\n  }\n";
+    s << "  __syncthreads();\n  if (!last_) return;\n";
+    // every thread of the last workgroup sums a group of splits for one column
+    // of the tile; the groups are then combined in order (deterministic)
+    const int TC = BB * VB;                   // columns of the tile
+    const int G = TC <= 256 ? 256 / TC : 1;   // split groups per column
+    s << "  {\n    const i64 cb = (i64)blockIdx.x * " << TC << ";\n";
+    s << "    for (int c = tid % " << std::min(TC, 256) << "; c < " << TC << "; c += 256) {\n";
+    s << "      const int g = " << (G > 1 ? "tid / " + std::to_string(TC) : std::string("0")) << ";\n";
+    s << "      float t_ = " << ident << ";\n";
+    s << "      if (cb + c < " << B << "LL)\n#pragma unroll 4\n        for (int z = g; z < " << SPLIT << "; z += " << G
+      << ") t_ = " << comb("t_", "part[(ay * " + std::to_string(SPLIT) + " + z) * " + std::to_string(B) + "LL + cb + c]")
+      << ";\n";
+    s << "      red[g * " << TC << " + c] = t_;\n    }\n  }\n  __syncthreads();\n";
+    s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n";
+    s << "      s[e] = red[bl * " << VB << " + e];\n";
+    if (G > 1)
+      s << "      for (int g = 1; g < " << G << "; ++g) s[e] = " << comb("s[e]", "red[g * " + std::to_string(TC) + " + bl * " +
+                                                                                 std::to_string(VB) + " + e]")
+        << ";\n";
+    s << "    }\n  }\n";
+  }
+  s << "  if (ly == 0 && bv) {\n";
+  if (rn.op == KORCH_REDUCE_MEAN)
+    s << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) s[e] = s[e] / " << flit((double)Lr) << ";\n";
+  s << "    const i64 l = 0; (void)l;\n" << ee.pre.str() << "#pragma unroll\n    for (int e = 0; e < " << VB
+    << "; ++e) {\n" << ee.body.str() << "    }\n  }\n}\n";
   gk.source = s.str();
-  gk.grid[0] = (int)((B + BB - 1) / BB);
+  gk.grid[0] = (int)ctiles;
   gk.grid[1] = (int)A;
+  gk.grid[2] = (int)SPLIT;
   ki.fill_cost(gk);
   return gk;
 }

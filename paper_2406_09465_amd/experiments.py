@@ -26,6 +26,7 @@ SWEEPS = {
     "linattn": [dict(heads=16, n=n, d=16) for n in (256, 1024, 4096, 16384)],
     "mlp": [dict(m=m, d=768, h=3072) for m in (128, 512, 2048, 8192)],
     "sra": [dict(hh=h, ww=h, c=64, r=8) for h in (32, 64, 128, 256)],
+    "instnorm": [dict(hh=h, ww=h, c=32) for h in (28, 56, 112, 224, 448)],
 }
 LIMITS = dict(max_prims=64, max_outs=3)
 

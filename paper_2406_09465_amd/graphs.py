@@ -227,7 +227,40 @@ def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6):
     return w
 
 
-BUILDERS = {"attention": attention, "mlp": mlp, "sra": sra, "conv": conv, "linattn": linattn}
+def instnorm(hh=224, ww=224, c=32, dtype="f16", eps=1e-5):
+    b = _B(dtype)
+    b.inp("X", (hh, ww, c))
+    b.inp("gamma", (c,))
+    b.inp("beta", (c,))
+    b.op("Xp", "reshape", ["X"], shape=(hh * ww, c))
+    b.op("mu", "reduce_mean", ["Xp"], axis=0, keepdim=True)
+    b.op("D", "sub", ["Xp", "mu"])
+    b.op("D2", "square", ["D"])
+    b.op("var", "reduce_mean", ["D2"], axis=0, keepdim=True)
+    b.op("ve", "add", ["var"], scalar=eps)
+    b.op("r", "rsqrt", ["ve"])
+    b.op("Xh", "mul", ["D", "r"])
+    b.op("Yg", "mul", ["Xh", "gamma"])
+    b.op("Y", "add", ["Yg", "beta"])
+    b.op("R", "relu", ["Y"])
+    b.op("Ri", "reshape", ["R"], shape=(hh, ww, c))
+    b.op("out", "pad", ["Ri"], begin=(1, 1, 0), end=(1, 1, 0))
+    b.g.output(b.ids["out"])
+    b.g.finalize()
+    w = Workload("instnorm", dtype, b.g, b.ids, b.inputs, ["out"], sizes=dict(hh=hh, ww=ww, c=c))
+    # operator per kernel (InstanceNorm as mean, variance and normalize; ReLU; Pad).
+    # D feeds both the variance and the normalization, and a kernel holding D
+    # and Xh but not the variance chain would not be convex, so the variance
+    # kernel materializes D.
+    w.plans["layered"] = [(["mu"], ["mu"]), (["D", "D2", "var", "ve", "r"], ["D", "r"]),
+                          (["Xh", "Yg", "Y"], ["Y"]), (["R"], ["R"]), (["out"], ["out"])]
+    # norm fission fused into the following ReLU and Pad (Section 6 case study)
+    w.plans["fused"] = [(["mu"], ["mu"]), (["D", "D2", "var", "ve", "r"], ["D", "r"]),
+                        (["Xh", "Yg", "Y", "R", "Ri", "out"], ["out"])]
+    return w
+
+
+BUILDERS = {"attention": attention, "mlp": mlp, "sra": sra, "conv": conv, "linattn": linattn, "instnorm": instnorm}
 
 
 def rewritten(w: Workload, rules=None):

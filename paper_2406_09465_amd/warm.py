@@ -17,6 +17,7 @@ SIZES = {
     "sra": [{}, dict(hh=40, ww=24, c=16, r=8)],
     "conv": [{}, dict(hh=37, ww=29, cin=8, cout=24)],
     "linattn": [{}, dict(heads=3, n=300, d=16)],
+    "instnorm": [{}, dict(hh=13, ww=11, c=24)],
 }
 # (sizes, number of plans, seed) of the sampled-plan GPU tests.
 SAMPLED = {
@@ -25,6 +26,7 @@ SAMPLED = {
     "sra": (dict(hh=32, ww=32, c=32, r=8), 6, 7),
     "conv": (dict(hh=24, ww=20, cin=16, cout=32), 6, 7),
     "linattn": (dict(heads=4, n=512, d=16), 6, 7),
+    "instnorm": (dict(hh=40, ww=36, c=16), 6, 7),
 }
 
 # Sizes at which the chooser profiles every supported candidate (bench.py's

@@ -70,18 +70,28 @@ def linattn_specs(heads=16, n=4096, d=16, dtype="bf16"):
     ]
 
 
+def instnorm_specs(hh=224, ww=224, c=32, dtype="f16"):
+    # activations after a convolution: per-tensor offset and spread
+    return [
+        ("X", 6001, (hh, ww, c), dtype, "normal", 0.3, 1.2),
+        ("gamma", 6002, (c,), dtype, "normal", 1.0, 0.1),
+        ("beta", 6003, (c,), dtype, "normal", 0.0, 0.1),
+    ]
+
+
 SPEC_FNS = {
     "attention": attention_specs,
     "mlp": mlp_specs,
     "sra": sra_specs,
     "conv": conv_specs,
     "linattn": linattn_specs,
+    "instnorm": instnorm_specs,
 }
 
 # Workload names in the order of the five configurations.
-WORKLOADS = ("attention", "mlp", "sra", "conv", "linattn")
+WORKLOADS = ("attention", "mlp", "sra", "conv", "linattn", "instnorm")
 
-DEFAULT_DTYPE = {"attention": "f32", "mlp": "f16", "sra": "f16", "conv": "f16", "linattn": "bf16"}
+DEFAULT_DTYPE = {"attention": "f32", "mlp": "f16", "sra": "f16", "conv": "f16", "linattn": "bf16", "instnorm": "f16"}
 
 
 def specs(workload: str, **shape):

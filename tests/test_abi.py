@@ -206,7 +206,7 @@ def test_every_plan_compiles_for_gfx950(workload):
     w = graphs.build(workload)
     expected = {
         "attention": ["attention"], "mlp": ["row", "gemm", "gemm"], "sra": ["splitk", "attention"],
-        "conv": ["conv"], "linattn": ["splitk", "gemm"],
+        "conv": ["conv"], "linattn": ["splitk", "gemm"], "instnorm": ["colreduce", "colreduce", "pointwise"],
     }[workload]
     for pn in ("unfused", "layered", "fused"):
         p = w.plan(pn)

@@ -112,7 +112,7 @@ def test_chooser_uses_redundancy_when_cheaper():
     assert sum(1 in p for p in covered) >= 2   # `a` is computed by more than one kernel
 
 
-@pytest.mark.parametrize("workload", ["attention", "mlp", "sra", "conv", "linattn"])
+@pytest.mark.parametrize("workload", ["attention", "mlp", "sra", "conv", "linattn", "instnorm"])
 def test_chooser_never_worse_than_hand_plans(workload):
     w = graphs.build(workload)
     g = w.graph

@@ -18,6 +18,7 @@ SIZES = {
     "sra": dict(hh=32, ww=32, c=32, r=8),
     "conv": dict(hh=24, ww=20, cin=16, cout=32),
     "linattn": dict(heads=4, n=512, d=16),
+    "instnorm": dict(hh=40, ww=36, c=16),
 }
 
 

@@ -23,6 +23,7 @@ FULL = {
     "sra": {},
     "conv": {},
     "linattn": {},
+    "instnorm": {},
 }
 RAGGED = {
     "attention": dict(n=50, d=24),
@@ -30,6 +31,7 @@ RAGGED = {
     "sra": dict(hh=40, ww=24, c=16, r=8),
     "conv": dict(hh=37, ww=29, cin=8, cout=24),
     "linattn": dict(heads=3, n=300, d=16),
+    "instnorm": dict(hh=13, ww=11, c=24),
 }
 PLANS = ["unfused", "layered", "fused"]
 

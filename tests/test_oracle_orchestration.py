@@ -181,7 +181,8 @@ def test_all_plans_small_attention_bitwise():
 def test_random_plans_all_workloads_bitwise():
     """T11 on small variants of every workload, including redundant execution."""
     sizes = {"attention": dict(n=8, d=4), "mlp": dict(m=8, d=16, h=8), "sra": dict(hh=8, ww=8, c=4, r=2),
-             "conv": dict(hh=5, ww=6, cin=3, cout=4), "linattn": dict(heads=2, n=16, d=4)}
+             "conv": dict(hh=5, ww=6, cin=3, cout=4), "linattn": dict(heads=2, n=16, d=4),
+             "instnorm": dict(hh=5, ww=4, c=3)}
     rnd = random.Random(12)
     for w, sh in sizes.items():
         g = configs.build(w, **sh)

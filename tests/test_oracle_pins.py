@@ -300,4 +300,46 @@ def test_output_magnitudes():
 def test_workload_graph_sizes():
     """Primitive counts of the five workload graphs."""
     counts = {w: len(configs.build(w).primitives()) for w in configs.BUILDERS}
-    assert counts == {"attention": 9, "mlp": 13, "sra": 23, "conv": 8, "linattn": 10}
+    assert counts == {"attention": 9, "mlp": 13, "sra": 23, "conv": 8, "linattn": 10, "instnorm": 13}
+
+
+def _instnorm(x, gamma, beta, eps=1e-5):
+    hh, ww, c = x.shape
+    g = configs.instnorm(hh=hh, ww=ww, c=c, eps=eps)
+    return run_unfused(g, {"X": x, "gamma": gamma, "beta": beta})["out"]
+
+
+def test_instnorm_closed_forms():
+    """InstanceNorm -> ReLU -> Pad (Candy pattern): a per-channel constant input
+    normalizes to 0, so the interior is relu(beta); a +-1 input (half the pixels
+    each) has mean 0 and biased variance 1, so it becomes
+    relu(+-gamma / sqrt(1 + eps) + beta); the one-pixel border is zero."""
+    rng = np.random.default_rng(3)
+    hh, ww, c, eps = 6, 8, 5, 1e-5
+    gamma = rng.normal(1.0, 0.3, c)
+    beta = rng.normal(0.0, 0.5, c)
+    x = np.broadcast_to(rng.normal(size=c), (hh, ww, c)).copy()
+    out = _instnorm(x, gamma, beta, eps)
+    assert out.shape == (hh + 2, ww + 2, c)
+    assert np.all(out[0] == 0) and np.all(out[-1] == 0) and np.all(out[:, 0] == 0) and np.all(out[:, -1] == 0)
+    # the mean of a constant carries a rounding residue of ~1e-16, which the
+    # reciprocal standard deviation 1/sqrt(eps) ~ 316 amplifies
+    assert np.allclose(out[1:-1, 1:-1], np.maximum(beta, 0.0), rtol=0, atol=1e-12)
+    sign = np.where((np.arange(hh * ww) % 2) == 0, 1.0, -1.0).reshape(hh, ww, 1)
+    x2 = np.broadcast_to(sign, (hh, ww, c)).copy()
+    out2 = _instnorm(x2, gamma, beta, eps)
+    expect = np.maximum(sign * gamma / np.sqrt(1.0 + eps) + beta, 0.0)
+    assert np.allclose(out2[1:-1, 1:-1], expect, rtol=1e-14, atol=1e-14)
+
+
+def test_instnorm_shift_invariance():
+    """Adding a per-channel constant to the input changes nothing (the mean is
+    subtracted); scaling by 2 changes only the eps term."""
+    rng = np.random.default_rng(4)
+    x = rng.normal(size=(7, 5, 6))
+    gamma, beta = rng.normal(1, 0.2, 6), rng.normal(0, 0.2, 6)
+    a = _instnorm(x, gamma, beta)
+    b = _instnorm(x + rng.normal(size=6) * 3.0, gamma, beta)
+    assert np.allclose(a, b, rtol=1e-12, atol=1e-12)
+    c = _instnorm(2.0 * x, gamma, beta, eps=4e-5)
+    assert np.allclose(a, c, rtol=1e-12, atol=1e-12)

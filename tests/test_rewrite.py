@@ -20,6 +20,7 @@ SMALL = {
     "sra": dict(hh=16, ww=16, c=8, r=4),
     "conv": dict(hh=9, ww=7, cin=8, cout=16),
     "linattn": dict(heads=3, n=50, d=8),
+    "instnorm": dict(hh=6, ww=5, c=8),
 }
 RULESETS = [K.RW_DEFER_DIV, K.RW_REDUCE_AS_PRODUCT, K.RW_MERGE_PRODUCTS,
             K.RW_REDUCE_AS_PRODUCT | K.RW_MERGE_PRODUCTS, K.RW_ALL]
