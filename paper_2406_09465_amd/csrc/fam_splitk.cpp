@@ -305,15 +305,18 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "  for (int i = tid; i < " << tile << "; i += 256) part[(tix * " << S << " + split) * " << tile
     << "LL + i] = Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "];\n";
   if (nside) s << "  if (tid < " << sp.BM << ") sidep[(tix * " << S << " + split) * " << sp.BM << " + tid] = side_acc;\n";
-  // Every wave's partial stores precede the barrier; one device-scope release
-  // by thread 0 then publishes the workgroup's partials before the counter
-  // increment, and the last workgroup's acquire makes all partials visible.
+  // Every wave's partial stores precede the barrier; the counter increment by
+  // thread 0 is a device-scope release that publishes the workgroup's
+  // partials, and only the last workgroup performs the device-scope acquire
+  // (each is an L2 write-back or invalidate on this multi-XCD device, so no
+  // other fence is issued).  The reset of the counter is ordered before its
+  // next use by the end of the kernel.
   s << "  __syncthreads();\n";
-  s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n    __threadfence();\n";
-  s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);\n";
+  s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
+  s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);\n";
   s << "    last_ = (old == " << S - 1 << ");\n";
-  s << "    if (last_) {\n      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n"
-    << "      __threadfence();\n    }\n  }\n";
+  s << "    if (last_) {\n      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, \"agent\");\n"
+    << "      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n    }\n  }\n";
   s << "  __syncthreads();\n  if (!last_) return;\n";
   // deterministic sum of the partials, split 0 first
   s << "  for (int i = tid; i < " << tile << "; i += 256) {\n    float acc_ = 0.0f;\n";

@@ -645,11 +645,12 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
       << " + blockIdx.z) * " << B << "LL + bi + e] = s[e];\n  }\n";
     s << "  __syncthreads();\n";
     s << "  const i64 tix = ay * " << ctiles << " + blockIdx.x;\n";
-    s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n    __threadfence();\n";
-    s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);\n";
+    // release by thread 0 with the increment; acquire only in the last workgroup
+    s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
+    s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);\n";
     s << "    last_ = (old == " << SPLIT - 1 << ");\n";
-    s << "    if (last_) {\n      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n"
-      << "      __threadfence();\n    }\n  }\n";
+    s << "    if (last_) {\n      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, \"agent\");\n"
+      << "      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n    }\n  }\n";
     s << "  __syncthreads();\n  if (!last_) return;\n";
     // every thread of the last workgroup sums a group of splits for one column
     // of the tile; the groups are then combined in order (deterministic)
