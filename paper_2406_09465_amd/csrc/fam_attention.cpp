@@ -203,26 +203,52 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   s << "  const i64 bz = blockIdx.y;\n";
   s << "  const i64 qoff = bz * " << a.nq * a.d << "LL, koff = bz * " << a.nk * a.d << "LL, voff = bz * "
     << a.nk * a.dv << "LL, ooff = bz * " << a.nq * a.dv << "LL;\n";
-  // K into LDS as [key][dim] (zero-padded dims)
-  s << "  for (int i = tid; i < " << nkp * dpad << "; i += 256) {\n";
-  s << "    const int key = i / " << dpad << ", dim = i % " << dpad << ";\n";
-  if (a.k_is_kt)
-    s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K << "[koff + (i64)dim * " << a.nk
-      << " + key] : fromf<" << T << ">(0.0f);\n";
-  else
-    s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K << "[koff + (i64)key * " << a.d
-      << " + dim] : fromf<" << T << ">(0.0f);\n";
-  s << "  }\n";
+  // K into LDS as [key][dim] (zero-padded dims); 16-byte vectors along dim
+  // when the rows allow (row pitches are multiples of 16 bytes)
+  const int VL = 16 / dtype_bytes(a.dtype);
+  const std::string VT = "vec_t<" + std::to_string(VL) + ", " + T + ">";
+  if (!a.k_is_kt && a.d % VL == 0 && dpad % VL == 0) {
+    s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dpad / VL << "; i += 256) {\n";
+    s << "    const int key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
+    s << "    " << VT << " x_ = {};\n";
+    s << "    if (dim < " << a.d << " && key < " << a.nk << ") x_ = *(const " << VT << "*)(" << K << " + koff + (i64)key * "
+      << a.d << " + dim);\n";
+    s << "    *(" << VT << "*)(Ks + key * " << KSP << " + dim) = x_;\n  }\n";
+  } else {
+    s << "  for (int i = tid; i < " << nkp * dpad << "; i += 256) {\n";
+    s << "    const int key = i / " << dpad << ", dim = i % " << dpad << ";\n";
+    if (a.k_is_kt)
+      s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K
+        << "[koff + (i64)dim * " << a.nk << " + key] : fromf<" << T << ">(0.0f);\n";
+    else
+      s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K
+        << "[koff + (i64)key * " << a.d << " + dim] : fromf<" << T << ">(0.0f);\n";
+    s << "  }\n";
+  }
   // V into LDS: fp32 natural [key][dim]; half precision transposed [dim][key]
-  s << "  for (int i = tid; i < " << nkp * dvp << "; i += 256) {\n";
-  s << "    const int key = i / " << dvp << ", dim = i % " << dvp << ";\n";
-  s << "    const " << T << " x_ = (key < " << a.nk << " && dim < " << a.dv << ") ? " << V << "[voff + (i64)key * "
-    << a.dv << " + dim] : fromf<" << T << ">(0.0f);\n";
-  if (f32)
-    s << "    Vs[key * " << VP << " + dim] = x_;\n";
-  else
-    s << "    Vs[dim * " << NKP << " + key] = x_;\n";
-  s << "  }\n  __syncthreads();\n";
+  if (a.dv % VL == 0 && dvp % VL == 0) {
+    s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dvp / VL << "; i += 256) {\n";
+    s << "    const int key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
+    s << "    " << VT << " x_ = {};\n";
+    s << "    if (key < " << a.nk << " && dim < " << a.dv << ") x_ = *(const " << VT << "*)(" << V << " + voff + (i64)key * "
+      << a.dv << " + dim);\n";
+    if (f32)
+      s << "    *(" << VT << "*)(Vs + key * " << VP << " + dim) = x_;\n";
+    else
+      s << "#pragma unroll\n    for (int e = 0; e < " << VL << "; ++e) Vs[(dim + e) * " << NKP << " + key] = x_[e];\n";
+    s << "  }\n";
+  } else {
+    s << "  for (int i = tid; i < " << nkp * dvp << "; i += 256) {\n";
+    s << "    const int key = i / " << dvp << ", dim = i % " << dvp << ";\n";
+    s << "    const " << T << " x_ = (key < " << a.nk << " && dim < " << a.dv << ") ? " << V << "[voff + (i64)key * "
+      << a.dv << " + dim] : fromf<" << T << ">(0.0f);\n";
+    if (f32)
+      s << "    Vs[key * " << VP << " + dim] = x_;\n";
+    else
+      s << "    Vs[dim * " << NKP << " + key] = x_;\n";
+    s << "  }\n";
+  }
+  s << "  __syncthreads();\n";
   // this wave's 16 query rows
   s << "  const i64 q0 = (i64)blockIdx.x * 64 + wave * 16;\n";
   s << "  const i64 qr = q0 + (l & 15);\n";
