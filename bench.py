@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--no-rewrite", action="store_true",
                     help="korch plan: do not consider the transformed primitive graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--time-every", type=int, default=8,
+                    help="bracket the dominant kernel with events on every N-th timed step")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work for the oracle sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, run a plain device copy of this many MiB 3 times (PMC byte calibration)")
@@ -173,35 +175,40 @@ def main():
         r.launch()
     torch.cuda.synchronize()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(nk)]
+    for e in ev:
+        e[0].record(stream)
+        e[1].record(stream)
     per = [[] for _ in range(nk)]
     for _ in range(max(5, args.warmup)):
         for k in range(nk):
-            ev[k][0].record(stream)
-            r.launch_kernels(k, 1)
-            ev[k][1].record(stream)
+            r.launch_timed(k, ev[k][0], ev[k][1])
         torch.cuda.synchronize()
         for k in range(nk):
             per[k].append(ev[k][0].elapsed_time(ev[k][1]) * 1e3)
     dom = max(range(nk), key=lambda k: statistics.median(per[k]))
 
-    # timed region: exactly `steps` plan executions; the dominant kernel is
-    # bracketed by events on the launch stream
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    # timed region: exactly `steps` plan executions, one library call each.  On
+    # every `time_every`-th step the library launches the dominant kernel with a
+    # pair of events (created here, recorded once so that they exist) that take
+    # that dispatch's own start and end timestamps on the launch stream; its
+    # average duration is taken over those sampled launches.
+    sampled = list(range(0, args.steps, max(1, args.time_every)))
+    starts = {i: torch.cuda.Event(enable_timing=True) for i in sampled}
+    ends = {i: torch.cuda.Event(enable_timing=True) for i in sampled}
+    for i in sampled:
+        starts[i].record(stream)
+        ends[i].record(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        if dom > 0:
-            r.launch_kernels(0, dom)
-        starts[i].record(stream)
-        r.launch_kernels(dom, 1)
-        ends[i].record(stream)
-        if dom + 1 < nk:
-            r.launch_kernels(dom + 1, nk - dom - 1)
+        if i in starts:
+            r.launch_timed(dom, starts[i], ends[i])
+        else:
+            r.launch()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    dom_us = statistics.mean(s.elapsed_time(e) * 1e3 for s, e in zip(starts, ends))
+    dom_us = statistics.mean(starts[i].elapsed_time(ends[i]) * 1e3 for i in sampled)
 
     fam, abytes, aflops = r.plan.kernel_info(dom)
     name = r.plan.kernel_name(dom)
@@ -218,6 +225,7 @@ def main():
     roof["traffic"] = traffic_from_profiles(f"{args.workload}/{name}", src_hash)
     roof["kernel"] = name
     roof["kernel_us"] = round(dom_us, 3)
+    roof["timed_launches"] = len(sampled)
     roof["alg_bytes"] = abytes
     roof["alg_flops"] = aflops
 

@@ -222,6 +222,17 @@ int korch_plan_execute(korch_plan* p, const void* const* inputs, void* const* ou
    having run the earlier kernels whose outputs these read. */
 int korch_plan_execute_kernels(korch_plan* p, int32_t first, int32_t count, const void* const* inputs,
                                void* const* outputs, void* workspace, size_t workspace_bytes, void* stream);
+/* korch_plan_execute_kernels with one kernel bracketed by events, so that a
+   timed loop of plan executions measures that kernel's duration in place
+   with one call per execution (the profiler of Section 5.2 times a kernel
+   alone; this times it inside the plan).  `start` and `stop` take the start
+   and end timestamps of kernel `timed`'s own dispatch on `stream` (no marker
+   packets are added); both are hipEvent_t handles owned by the caller
+   (created with timing enabled), and either may be NULL.  KORCH_E_ARG when `timed` is not in [first,
+   first+count); otherwise errors as korch_plan_execute_kernels. */
+int korch_plan_execute_timed(korch_plan* p, int32_t first, int32_t count, const void* const* inputs,
+                             void* const* outputs, void* workspace, size_t workspace_bytes, void* stream, int32_t timed,
+                             void* start, void* stop);
 /* Per-kernel family, algorithmic bytes (compulsory reads of its external
    tensors plus writes of its outputs) and flops (2*M*N*K per contraction). */
 int korch_plan_kernel_info(const korch_plan* p, int32_t k, int32_t* family, double* alg_bytes, double* alg_flops);

@@ -102,6 +102,7 @@ _SIGS = {
     "korch_plan_workspace_bytes": ([_P, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute": ([_P, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
     "korch_plan_execute_kernels": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
+    "korch_plan_execute_timed": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P, _I, _P, _P], C.c_int),
     "korch_plan_kernel_info": ([_P, _I, C.POINTER(_I), C.POINTER(C.c_double), C.POINTER(C.c_double)], C.c_int),
     "korch_plan_kernel_source": ([_P, _I, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_kernel_name": ([_P, _I, C.c_char_p, C.c_size_t], C.c_int),
@@ -135,6 +136,11 @@ def check(rc):
 def _ids(xs):
     xs = [int(x) for x in xs]
     return (C.c_int32 * max(1, len(xs)))(*xs), len(xs)
+
+
+def pointer_array(ptrs):
+    """ctypes array of device pointers (ints), for the execute calls."""
+    return (C.c_void_p * max(1, len(ptrs)))(*[C.c_void_p(int(p)) for p in ptrs])
 
 
 def kernel_desc(prims, outs):
@@ -349,17 +355,28 @@ class Plan:
         return n.value
 
     def execute(self, inputs, outputs, workspace=0, workspace_bytes=0, stream=0):
-        """inputs / outputs: device pointers (ints) in graph input / output order."""
-        ins = (C.c_void_p * max(1, len(inputs)))(*[C.c_void_p(int(p)) for p in inputs])
-        outs = (C.c_void_p * max(1, len(outputs)))(*[C.c_void_p(int(p)) for p in outputs])
+        """inputs / outputs: device pointers (ints) in graph input / output order, or
+        ctypes pointer arrays already built with ``pointer_array``."""
+        ins = inputs if isinstance(inputs, C.Array) else pointer_array(inputs)
+        outs = outputs if isinstance(outputs, C.Array) else pointer_array(outputs)
         check(lib.korch_plan_execute(self.h, ins, outs, C.c_void_p(int(workspace)), int(workspace_bytes),
                                      C.c_void_p(int(stream))))
 
     def execute_kernels(self, first, count, inputs, outputs, workspace=0, workspace_bytes=0, stream=0):
-        ins = (C.c_void_p * max(1, len(inputs)))(*[C.c_void_p(int(p)) for p in inputs])
-        outs = (C.c_void_p * max(1, len(outputs)))(*[C.c_void_p(int(p)) for p in outputs])
+        ins = inputs if isinstance(inputs, C.Array) else pointer_array(inputs)
+        outs = outputs if isinstance(outputs, C.Array) else pointer_array(outputs)
         check(lib.korch_plan_execute_kernels(self.h, int(first), int(count), ins, outs, C.c_void_p(int(workspace)),
                                              int(workspace_bytes), C.c_void_p(int(stream))))
+
+    def execute_timed(self, first, count, inputs, outputs, workspace=0, workspace_bytes=0, stream=0, timed=0,
+                      start=0, stop=0):
+        """execute_kernels with kernel ``timed`` bracketed by the hipEvent_t handles ``start`` / ``stop``.
+        ``inputs`` / ``outputs`` may be ctypes pointer arrays already built (see ``pointer_array``)."""
+        ins = inputs if isinstance(inputs, C.Array) else pointer_array(inputs)
+        outs = outputs if isinstance(outputs, C.Array) else pointer_array(outputs)
+        check(lib.korch_plan_execute_timed(self.h, int(first), int(count), ins, outs, C.c_void_p(int(workspace)),
+                                           int(workspace_bytes), C.c_void_p(int(stream)), int(timed),
+                                           C.c_void_p(int(start)), C.c_void_p(int(stop))))
 
     def kernel_info(self, k):
         fam, b, f = _I(), C.c_double(), C.c_double()

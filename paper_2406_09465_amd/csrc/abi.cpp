@@ -25,7 +25,8 @@ void generate_plan(Plan& p);
 void load_plan(Plan& p);
 void destroy_plan_device(Plan& p);
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
-                  hipStream_t stream, int first, int count);
+                  hipStream_t stream, int first, int count, int timed = -1, hipEvent_t ev_start = nullptr,
+                  hipEvent_t ev_stop = nullptr);
 void compile_candidate(const Graph& g, const KernelDesc& kd);
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream);
@@ -420,6 +421,18 @@ int korch_plan_execute_kernels(korch_plan* p, int32_t first, int32_t count, cons
     NEED(p);
     if (count < 0) fail(KORCH_E_ARG, "negative kernel count");
     execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, first, count);
+  });
+}
+
+int korch_plan_execute_timed(korch_plan* p, int32_t first, int32_t count, const void* const* inputs,
+                             void* const* outputs, void* workspace, size_t workspace_bytes, void* stream, int32_t timed,
+                             void* start, void* stop) {
+  return guard([&] {
+    NEED(p);
+    if (count < 0) fail(KORCH_E_ARG, "negative kernel count");
+    if (timed < first || timed >= first + count) fail(KORCH_E_ARG, "timed kernel outside the launched range");
+    execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, first, count, timed,
+                 (hipEvent_t)start, (hipEvent_t)stop);
   });
 }
 

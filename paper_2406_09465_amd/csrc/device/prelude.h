@@ -90,10 +90,10 @@ __device__ __forceinline__ float k_max(float a, float b) { return a > b ? a : b;
 __device__ __forceinline__ float k_min(float a, float b) { return a < b ? a : b; }
 
 // Mish written as x * n / (n + 2) with n = e^x (e^x + 2), which equals
-// x * tanh(log(1 + e^x)) exactly; for x > 20 the quotient is 1 in fp32.
+// x * tanh(log(1 + e^x)) exactly.  For x >= 20 the quotient rounds to 1 in
+// fp32, so the exponent's argument is clamped there (no overflow, no branch).
 __device__ __forceinline__ float k_mish(float x) {
-  if (x > 20.0f) return x;
-  float ex = expf(x);
+  float ex = expf(k_min(x, 20.0f));
   float n = ex * (ex + 2.0f);
   return x * (n / (n + 2.0f));
 }
@@ -112,8 +112,7 @@ __device__ __forceinline__ float f_gelu_tanh(float x) {
   return 0.5f * x * (1.0f + f_tanh(c * (x + 0.044715f * x * x * x)));
 }
 __device__ __forceinline__ float f_mish(float x) {
-  if (x > 20.0f) return x;
-  float ex = f_exp(x);
+  float ex = f_exp(k_min(x, 20.0f));
   float n = ex * (ex + 2.0f);
   return x * f_div(n, n + 2.0f);
 }

@@ -2,6 +2,15 @@
 // (Korch, Section 5.3) and the single-candidate profiler (Section 5.2).
 #include <hip/hip_runtime_api.h>
 
+// AMD's launch extension (declared in hip_ext.h, whose templates need the
+// device compiler): a module-kernel launch whose start / stop events take the
+// dispatch's own timestamps.  Work sizes are in threads (grid x block).
+extern "C" hipError_t hipExtModuleLaunchKernel(hipFunction_t f, uint32_t globalWorkSizeX, uint32_t globalWorkSizeY,
+                                               uint32_t globalWorkSizeZ, uint32_t localWorkSizeX,
+                                               uint32_t localWorkSizeY, uint32_t localWorkSizeZ, size_t sharedMemBytes,
+                                               hipStream_t hStream, void** kernelParams, void** extra,
+                                               hipEvent_t startEvent, hipEvent_t stopEvent, uint32_t flags);
+
 #include <algorithm>
 #include <atomic>
 #include <cstdlib>
@@ -114,7 +123,7 @@ void load_plan(Plan& p) {
 static bool aligned16(const void* q) { return ((uintptr_t)q & 15) == 0; }
 
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
-                  hipStream_t stream, int first, int count) {
+                  hipStream_t stream, int first, int count, int timed, hipEvent_t ev_start, hipEvent_t ev_stop) {
   load_plan(p);
   const Graph& g = p.g;
   for (size_t i = 0; i < g.inputs.size(); ++i) {
@@ -146,6 +155,15 @@ void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void
       }
     }
     void* params[] = {ptr.data()};
+    if (k == timed && (ev_start || ev_stop)) {
+      // the events take the timestamps of this kernel's own dispatch (no
+      // separate marker packets in the stream)
+      HIPCHECK(hipExtModuleLaunchKernel((hipFunction_t)ck.function, (uint32_t)(ck.gen.grid[0] * ck.gen.block[0]),
+                                        (uint32_t)(ck.gen.grid[1] * ck.gen.block[1]),
+                                        (uint32_t)(ck.gen.grid[2] * ck.gen.block[2]), ck.gen.block[0], ck.gen.block[1],
+                                        ck.gen.block[2], 0, stream, params, nullptr, ev_start, ev_stop, 0));
+      continue;
+    }
     HIPCHECK(hipModuleLaunchKernel((hipFunction_t)ck.function, ck.gen.grid[0], ck.gen.grid[1], ck.gen.grid[2],
                                    ck.gen.block[0], ck.gen.block[1], ck.gen.block[2], 0, stream, params, nullptr));
   }
@@ -221,13 +239,13 @@ float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int re
     }
     void* ws = p.ws_bytes ? alloc(p.ws_bytes) : nullptr;
     void* fl = flush_bytes ? alloc(flush_bytes) : nullptr;
-    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1);
+    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr);
     ev = new hipEvent_t[2 * std::max(reps, 1)];
     for (int r = 0; r < 2 * reps; ++r) HIPCHECK(hipEventCreate(&ev[r]));
     for (int r = 0; r < reps; ++r) {
       if (fl) HIPCHECK(launch_flush(fl, flush_bytes, stream));
       HIPCHECK(hipEventRecord(ev[2 * r], stream));
-      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1);
+      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr);
       HIPCHECK(hipEventRecord(ev[2 * r + 1], stream));
     }
     HIPCHECK(hipStreamSynchronize(stream));

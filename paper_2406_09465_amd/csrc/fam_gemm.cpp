@@ -960,7 +960,7 @@ size_t gemm_smem_bytes(const GemmSpec& sp) {
 
 // Pointwise epilogue over the C tile: every kernel output at (batch, m, n).
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
-                          const std::string& cs_row, const std::set<int>& skip) {
+                          const std::string& cs_row, const std::set<int>& skip, int conv_tw) {
   const Graph& g = ki.g;
   int maxb = 2;
   for (int o : ki.k.outs) maxb = std::max(maxb, dtype_bytes(g.nodes[o].dtype));
@@ -984,14 +984,24 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
   }
   it.push_back(Ix::var("n", 1, VE));
   std::map<std::string, std::string> canon;
+  // C tile values of a full-width product are read into registers with 16-byte
+  // LDS reads before the element loop (rows start 16-byte aligned: LDC and the
+  // column offsets are multiples of 4)
+  std::ostringstream cvload;
   for (size_t j = 0; j < sp.mms.size(); ++j) {
     int mm = sp.mms[j];
     auto bi = broadcast_index(g.nodes[mm].shape, sp.OUT, it);
     std::string base = cs_row + " + " + std::to_string(sp.mms.size() > 1 ? sp.offj[j] : 0);
-    if (sp.Nj[j] == 1 && sp.N != 1)
+    if (sp.Nj[j] == 1 && sp.N != 1) {
       canon[Emitter::key(mm, bi)] = "Cs[" + base + "]";
-    else
+    } else if (VE % 4 == 0) {
+      std::string cv = "_cv" + std::to_string(j);
+      cvload << "      float " << cv << "[" << VE << "];\n#pragma unroll\n      for (int q = 0; q < " << VE / 4
+             << "; ++q) *(float4*)&" << cv << "[4 * q] = *(const float4*)&Cs[" << base << " + nl + 4 * q];\n";
+      canon[Emitter::key(mm, bi)] = cv + "[e]";
+    } else {
       canon[Emitter::key(mm, bi)] = "Cs[" + base + " + nl + e]";
+    }
   }
   em.provide = [&](int node, const std::vector<Ix>& idx, std::string* out) {
     if (!in_vec(sp.mms, node)) return false;
@@ -1032,10 +1042,16 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
   std::ostringstream s;
   s << "  for (int s_ = tid; s_ < " << sp.BM * (cols / VE) << "; s_ += " << sp.NT << ") {\n";
   s << "    const int ml = s_ / " << cols / VE << ", nl = (s_ % " << cols / VE << ") * " << VE << ";\n";
-  s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
-  s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n";
-  if (sp.conv) s << "      const i64 oy = m / " << sp.Wo << "LL, ox = m % " << sp.Wo << "LL;\n";
-  s << em.pre.str() << decl.str();
+  if (conv_tw > 0) {
+    // C tile row ml is pixel (ml / conv_tw, ml % conv_tw) of a 2-D output tile at (ty0, tx0)
+    s << "    const i64 oy = ty0 + ml / " << conv_tw << ", ox = tx0 + ml % " << conv_tw << ", n = n0 + nl;\n";
+    s << "    if (oy < " << sp.Ho << "LL && ox < " << sp.Wo << "LL && n < " << sp.N << "LL) {\n";
+  } else {
+    s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
+    s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n";
+    if (sp.conv) s << "      const i64 oy = m / " << sp.Wo << "LL, ox = m % " << sp.Wo << "LL;\n";
+  }
+  s << cvload.str() << em.pre.str() << decl.str();
   s << "#pragma unroll\n      for (int e = 0; e < " << VE << "; ++e) {\n" << em.body.str() << "      }\n";
   s << after.str() << "    }\n  }\n";
   return s.str();
@@ -1057,6 +1073,10 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   GemmSpec sp;
   std::string why;
   if (!analyze_gemm(ki, sp, &why, false)) fail(KORCH_E_UNSUPPORTED, why);
+  if (sp.conv) {
+    const char* e = getenv("KORCH_CONV_DIRECT");  // "0" keeps the implicit-GEMM kernel
+    if (!(e && atoi(e) == 0) && conv_direct_fits(sp, nullptr)) return gen_conv_direct(ki, sp, index);
+  }
   choose_tiles(sp, false);
   plan_operands(ki, sp);
   if ((sp.K + sp.BK - 1) / sp.BK > 128) sp.NS = 2;  // long contractions use the rolled loop

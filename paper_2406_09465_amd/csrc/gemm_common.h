@@ -61,8 +61,15 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
 // skipped).
 std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "", int64_t kconst = 0,
                           bool kconst_exact = true);
+// Pointwise epilogue over the fp32 C tile `Cs` (row `cs_row`).  conv_tw > 0:
+// the tile is a 2-D block of output pixels conv_tw wide whose origin is
+// (ty0, tx0), and C tile row ml holds pixel (ml / conv_tw, ml % conv_tw).
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
-                          const std::string& cs_row, const std::set<int>& skip = {});
+                          const std::string& cs_row, const std::set<int>& skip = {}, int conv_tw = 0);
+// Direct convolution (stride 1, half precision, input halo tile in LDS,
+// weights in registers); conv_direct_fits says whether it applies.
+bool conv_direct_fits(const GemmSpec& sp, std::string* why);
+GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index);
 std::string gemm_prologue_common(const GemmSpec& sp);
 size_t gemm_smem_bytes(const GemmSpec& sp);
 

@@ -10,7 +10,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from ._abi import Plan
+from ._abi import Plan, pointer_array
 
 TORCH_DTYPE = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -51,15 +51,33 @@ class PlanRunner:
         """storage: {input name: storage array} (synthetic.make_inputs output)."""
         self.ins = [to_device(storage[n], self.w.dtype, self.device) for n in self.w.input_names]
 
+    def _ptrs(self):
+        """ctypes pointer arrays of the current input and output tensors (rebuilt
+        only when a tensor changes, to keep the per-launch host cost low)."""
+        key = tuple(t.data_ptr() for t in self.ins) + (None,) + tuple(t.data_ptr() for t in self.outs)
+        if getattr(self, "_ptr_key", None) != key:
+            self._ptr_key = key
+            self._ptr_arrays = (pointer_array([t.data_ptr() for t in self.ins]),
+                                pointer_array([t.data_ptr() for t in self.outs]))
+        return self._ptr_arrays
+
     def launch(self, stream=None):
         s = stream if stream is not None else torch.cuda.current_stream()
-        self.plan.execute([t.data_ptr() for t in self.ins], [t.data_ptr() for t in self.outs],
-                          self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
+        ins, outs = self._ptrs()
+        self.plan.execute(ins, outs, self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
 
     def launch_kernels(self, first, count, stream=None):
         s = stream if stream is not None else torch.cuda.current_stream()
-        self.plan.execute_kernels(first, count, [t.data_ptr() for t in self.ins], [t.data_ptr() for t in self.outs],
-                                  self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
+        ins, outs = self._ptrs()
+        self.plan.execute_kernels(first, count, ins, outs, self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
+
+    def launch_timed(self, timed, start, stop, stream=None):
+        """One execution of the whole plan with kernel ``timed`` bracketed by the
+        torch events ``start`` / ``stop`` (each recorded once before, so that it exists)."""
+        s = stream if stream is not None else torch.cuda.current_stream()
+        ins, outs = self._ptrs()
+        self.plan.execute_timed(0, self.plan.num_kernels(), ins, outs, self.ws.data_ptr(), self.ws_bytes,
+                                s.cuda_stream, timed, start.cuda_event, stop.cuda_event)
 
     def run(self, storage: dict = None):
         if storage is not None:

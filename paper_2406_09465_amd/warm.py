@@ -29,6 +29,16 @@ SAMPLED = {
     "instnorm": (dict(hh=40, ww=36, c=16), 6, 7),
 }
 
+# Shapes of the convolution-kernel GPU tests, each run with the direct kernel
+# allowed and with the implicit-GEMM kernel forced (KORCH_CONV_DIRECT=0).
+CONV_CASES = [
+    dict(hh=37, ww=29, cin=8, cout=24),
+    dict(hh=15, ww=13, cin=48, cout=16),
+    dict(hh=10, ww=50, cin=16, cout=48),
+    dict(hh=21, ww=40, cin=16, cout=16, k=5),
+    dict(hh=9, ww=70, cin=32, cout=128),
+]
+
 # Sizes at which the chooser profiles every supported candidate (bench.py's
 # measured-cost plan at full size; the chooser GPU test at the sampled sizes).
 CHOOSER = {w: [{}, SAMPLED[w][0]] for w in SAMPLED}
@@ -43,6 +53,9 @@ def _jobs():
             jobs.append(("plans", w, sz, None))
     for w, (sz, n, seed) in SAMPLED.items():
         jobs.append(("sampled", w, sz, (n, seed)))
+    for sz in CONV_CASES + [{}]:
+        for direct in ("1", "0"):
+            jobs.append(("conv_kernels", "conv", sz, direct))
     for w, sizes in CHOOSER.items():
         for sz in sizes:
             jobs.append(("candidates", w, sz, None))
@@ -61,6 +74,21 @@ def _run_job(job, part=0, parts=1):
                 wl.plan(pn).compile()
             except KorchError as e:
                 failures.append((w, sz, pn, str(e)[:200]))
+    elif kind == "conv_kernels":
+        import os
+        prev = os.environ.get("KORCH_CONV_DIRECT")
+        os.environ["KORCH_CONV_DIRECT"] = extra
+        try:
+            for pn in ("layered", "fused"):
+                try:
+                    wl.plan(pn).compile()
+                except KorchError as e:
+                    failures.append((w, sz, f"{pn} direct={extra}", str(e)[:200]))
+        finally:
+            if prev is None:
+                os.environ.pop("KORCH_CONV_DIRECT")
+            else:
+                os.environ["KORCH_CONV_DIRECT"] = prev
     elif kind == "sampled":
         for i, ks in enumerate(search.sampled_plans(wl.graph, *extra)):
             try:

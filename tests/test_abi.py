@@ -274,3 +274,43 @@ def test_sampled_and_sized_plans_compile():
 
     failures = warm.warm_cache(prune_stale=False)
     assert not failures, failures[:3]
+
+
+def test_conv_kernel_variants():
+    """The conv family generates the direct kernel (halo tile in LDS) for
+    half-precision stride-1 convolutions within its register budget, and the
+    implicit-GEMM kernel otherwise or when KORCH_CONV_DIRECT=0."""
+    import os
+    from paper_2406_09465_amd import graphs
+    from paper_2406_09465_amd.warm import CONV_CASES
+
+    def source(sizes, direct):
+        prev = os.environ.get("KORCH_CONV_DIRECT")
+        os.environ["KORCH_CONV_DIRECT"] = direct
+        try:
+            p = graphs.build("conv", **sizes).plan("fused")
+            p.compile()
+            return p.kernel_source(0)
+        finally:
+            if prev is None:
+                os.environ.pop("KORCH_CONV_DIRECT")
+            else:
+                os.environ["KORCH_CONV_DIRECT"] = prev
+
+    direct_cases = [{}] + CONV_CASES[:4]
+    for sz in direct_cases:
+        assert "fetch_halo" in source(sz, "1"), sz
+        assert "fetch_halo" not in source(sz, "0"), sz
+    # 128 output channels need more LDS than two workgroups per compute unit allow
+    assert "fetch_halo" not in source(CONV_CASES[4], "1")
+    # 48 -> 96 channels: the weights of a wave exceed its register budget
+    assert "fetch_halo" not in source(dict(hh=15, ww=13, cin=48, cout=96), "1")
+    assert "fetch_halo" not in source(dict(hh=12, ww=12, cin=8, cout=16, dtype="f32"), "1")
+
+
+def test_timed_execute_rejects_a_kernel_outside_the_range():
+    w = graphs.build("mlp", m=64, d=32, h=48)
+    p = w.plan("layered")
+    n = p.num_kernels()
+    assert code(lambda: p.execute_timed(0, n, [0] * 6, [0], 0, 0, 0, n, 0, 0)) == -1
+    assert code(lambda: p.execute_timed(1, 1, [0] * 6, [0], 0, 0, 0, 0, 0, 0)) == -1

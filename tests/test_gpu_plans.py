@@ -63,3 +63,30 @@ def test_profiler_times_candidates():
     # a kernel no family implements costs infinity (None)
     assert w.graph.profile([ids["var"], ids["ve"], ids["r"], ids["Xh"], ids["Yg"], ids["Y"], ids["H0"]],
                            [ids["H0"]], warmup=1, reps=1) is None
+
+
+def test_timed_execution_matches_plain_execution():
+    """korch_plan_execute_timed launches the same kernels as korch_plan_execute
+    (identical bytes) and brackets the timed kernel with the caller's events."""
+    from paper_2406_09465_amd import graphs
+    from paper_2406_09465_amd.runner import PlanRunner
+    from synthetic import workloads as W
+    sizes = SIZES["mlp"]
+    w = graphs.build("mlp", **sizes)
+    print("\n[case] timed execution, mlp layered", flush=True)
+    r = PlanRunner(w, "layered")
+    r.set_inputs(W.inputs("mlp", **sizes))
+    r.launch()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in r.outs]
+    s = torch.cuda.current_stream()
+    for k in range(r.plan.num_kernels()):
+        for t in r.outs:
+            t.zero_()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        b.record(s)
+        r.launch_timed(k, a, b)
+        torch.cuda.synchronize()
+        assert all(torch.equal(x, y) for x, y in zip(ref, r.outs))
+        assert a.elapsed_time(b) > 0.0
