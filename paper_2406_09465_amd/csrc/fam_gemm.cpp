@@ -849,7 +849,7 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
 }
 
 // The MFMA main loop over k-tiles [kt0, kt1) of the contraction.
-std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t kconst, bool kconst_exact) {
+std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t kconst, bool kconst_exact, bool ctile) {
   std::ostringstream s;
   bool f32 = sp.mtype == KORCH_F32;
   std::string T = ctype(sp.mtype);
@@ -942,6 +942,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
     s << step("1", "(kt + 1)");
     s << "  }\n";
   }
+  if (!ctile) return s.str();
   // accumulators -> LDS C tile (fp32)
   s << "  float* Cs = (float*)smem;\n";
   s << "  " << wguard << "{\n#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
@@ -954,13 +955,14 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
 size_t gemm_smem_bytes(const GemmSpec& sp) {
   size_t bbuf = (size_t)b_buf_elems(sp);
   size_t ab = (size_t)2 * ((size_t)sp.BM * sp.BKP + bbuf) * dtype_bytes(sp.mtype);
-  size_t c = (size_t)sp.BM * sp.LDC * 4;
+  size_t c = (size_t)(sp.CROWS ? sp.CROWS : sp.BM) * sp.LDC * 4;
   return std::max(ab, c);
 }
 
 // Pointwise epilogue over the C tile: every kernel output at (batch, m, n).
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
-                          const std::string& cs_row, const std::set<int>& skip, int conv_tw) {
+                          const std::string& cs_row, const std::set<int>& skip, int conv_tw, int rows,
+                          const std::string& row0) {
   const Graph& g = ki.g;
   int maxb = 2;
   for (int o : ki.k.outs) maxb = std::max(maxb, dtype_bytes(g.nodes[o].dtype));
@@ -1040,8 +1042,11 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
     }
   }
   std::ostringstream s;
-  s << "  for (int s_ = tid; s_ < " << sp.BM * (cols / VE) << "; s_ += " << sp.NT << ") {\n";
-  s << "    const int ml = s_ / " << cols / VE << ", nl = (s_ % " << cols / VE << ") * " << VE << ";\n";
+  if (rows <= 0) rows = sp.BM;
+  s << "  for (int s_ = tid; s_ < " << rows * (cols / VE) << "; s_ += " << sp.NT << ") {\n";
+  s << "    const int mlc = s_ / " << cols / VE << ", ml = " << row0 << " + mlc, nl = (s_ % " << cols / VE << ") * " << VE
+    << ";\n";
+  s << "    (void)mlc;\n";
   if (conv_tw > 0) {
     // C tile row ml is pixel (ml / conv_tw, ml % conv_tw) of a 2-D output tile at (ty0, tx0)
     s << "    const i64 oy = ty0 + ml / " << conv_tw << ", ox = tx0 + ml % " << conv_tw << ", n = n0 + nl;\n";
@@ -1080,6 +1085,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   choose_tiles(sp, false);
   plan_operands(ki, sp);
   if ((sp.K + sp.BK - 1) / sp.BK > 128) sp.NS = 2;  // long contractions use the rolled loop
+  if (sp.WM > 1 && !getenv("KORCH_GEMM_FULL_CTILE")) sp.CROWS = sp.WTM;
   GenKernel gk;
   gk.family = sp.conv ? KORCH_FAM_CONV : KORCH_FAM_GEMM;
   gk.name = kernel_name(index, sp.conv ? "conv" : "gemm");
@@ -1111,8 +1117,27 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   s << "  const int kt0 = 0, kt1 = " << KT << ";\n";
   s << operand_loader(ki, sp, true, slot);
   s << operand_loader(ki, sp, false, slot);
-  s << mfma_mainloop(sp, "", KT);
-  s << gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(sp.LDC));
+  if (sp.CROWS && sp.CROWS < sp.BM) {
+    // The C tile passes through LDS one band of wave rows at a time (waves
+    // with wm == p write rows [p*WTM, (p+1)*WTM), then every thread runs the
+    // epilogue over them), so the fp32 staging area is WTM rows, not BM: the
+    // operand buffers then bound the LDS of a workgroup and more workgroups
+    // fit on a compute unit.
+    s << mfma_mainloop(sp, "", KT, true, false);
+    s << "  float* Cs = (float*)smem;\n";
+    s << "  for (int p_ = 0; p_ < " << sp.WM << "; ++p_) {\n";
+    s << "    if (p_ > 0) __syncthreads();\n";
+    s << "    if (wm == p_) {\n#pragma unroll\n    for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n    for (int j = 0; j < "
+      << sp.FN << "; ++j)\n#pragma unroll\n    for (int r = 0; r < 4; ++r) Cs[(i * 16 + (l >> 4) * 4 + r) * " << sp.LDC
+      << " + wn * " << sp.WTN << " + j * 16 + (l & 15)] = acc[i][j][r];\n    }\n";
+    s << "    __syncthreads();\n";
+    s << gemm_epilogue(ki, sp, slot, "mlc * " + std::to_string(sp.LDC), {}, 0, sp.CROWS,
+                       "p_ * " + std::to_string(sp.CROWS));
+    s << "  }\n";
+  } else {
+    s << mfma_mainloop(sp, "", KT);
+    s << gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(sp.LDC));
+  }
   s << "}\n";
   gk.source = s.str();
   gk.grid[0] = (int)total;

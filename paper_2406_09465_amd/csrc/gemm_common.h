@@ -42,6 +42,8 @@ struct GemmSpec {
   // covers rows {0..3, 8..11} (+ 16 j), and the relative shift of the second
   // block puts those eight 32-byte windows on distinct LDS banks.
   int BSH = 0;
+  // Rows of the fp32 C tile staged in LDS at once for the epilogue (0 = BM).
+  int CROWS = 0;
 };
 
 // LDS element offset of row k of the [k][n] right-operand tile.
@@ -59,13 +61,18 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
 // unrolled completely and uses sp.NS register stages), else 0; kconst_exact:
 // every workgroup runs exactly kconst tiles (else tiles at or past kt1 are
 // skipped).
+// ctile: write the accumulators to the fp32 C tile at smem (and synchronize)
+// after the loop.
 std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "", int64_t kconst = 0,
-                          bool kconst_exact = true);
-// Pointwise epilogue over the fp32 C tile `Cs` (row `cs_row`).  conv_tw > 0:
-// the tile is a 2-D block of output pixels conv_tw wide whose origin is
-// (ty0, tx0), and C tile row ml holds pixel (ml / conv_tw, ml % conv_tw).
+                          bool kconst_exact = true, bool ctile = true);
+// Pointwise epilogue over the fp32 C tile `Cs` (row `cs_row`, an expression of
+// the local row `mlc` or the tile row `ml`).  It covers `rows` tile rows (0 =
+// BM) starting at tile row `row0`.  conv_tw > 0: the tile is a 2-D block of
+// output pixels conv_tw wide whose origin is (ty0, tx0), and C tile row ml
+// holds pixel (ml / conv_tw, ml % conv_tw).
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
-                          const std::string& cs_row, const std::set<int>& skip = {}, int conv_tw = 0);
+                          const std::string& cs_row, const std::set<int>& skip = {}, int conv_tw = 0,
+                          int rows = 0, const std::string& row0 = "0");
 // Direct convolution (stride 1, half precision, input halo tile in LDS,
 // weights in registers); conv_direct_fits says whether it applies.
 bool conv_direct_fits(const GemmSpec& sp, std::string* why);

@@ -123,6 +123,11 @@ std::vector<char> rtc_compile(const std::string& src, const std::string& name) {
       }
     }
   }
+  // hipRTC's in-process compiler keeps process-global state (LLVM's option
+  // parsing among it) and is not safe to call from several threads at once;
+  // cache hits above stay concurrent, compilations take turns.
+  static std::mutex compile_mutex;
+  std::lock_guard<std::mutex> lock(compile_mutex);
   hiprtcProgram prog;
   if (R.create(&prog, src.c_str(), (name + ".hip").c_str(), 0, nullptr, nullptr) != HIPRTC_SUCCESS)
     fail(KORCH_E_COMPILE, "hiprtcCreateProgram failed for " + name);

@@ -13,7 +13,7 @@ from ._abi import KorchError
 # Sizes run by the test suite, smoke() and bench.py.
 SIZES = {
     "attention": [{}, dict(n=50, d=24)],
-    "mlp": [{}, dict(m=300, d=96, h=200), dict(m=256, d=128, h=256)],
+    "mlp": [{}, dict(m=300, d=96, h=200), dict(m=256, d=128, h=256), dict(m=256, d=128, h=192)],
     "sra": [{}, dict(hh=40, ww=24, c=16, r=8)],
     "conv": [{}, dict(hh=37, ww=29, cin=8, cout=24)],
     "linattn": [{}, dict(heads=3, n=300, d=16)],
