@@ -107,9 +107,14 @@ __device__ __forceinline__ float f_div(float x, float y) { return x * __builtin_
 // tanh(x) = 1 - 2 / (e^{2x} + 1): saturates to +-1 when e^{2x} overflows or vanishes.
 __device__ __forceinline__ float f_tanh(float x) { return 1.0f - f_div(2.0f, f_exp(2.0f * x) + 1.0f); }
 __device__ __forceinline__ float f_rsqrt(float x) { return __builtin_amdgcn_rsqf(x); }
+// 0.5 x (1 + tanh(u)) equals x / (1 + e^{-2u}) exactly; with
+// u = sqrt(2/pi) (x + 0.044715 x^3) that is one base-2 exponential of
+// -2 sqrt(2/pi) / ln(2) * x (1 + 0.044715 x^2) and one reciprocal.  Large |x|
+// saturate to x and -0.
 __device__ __forceinline__ float f_gelu_tanh(float x) {
-  const float c = 0.7978845608028654f;
-  return 0.5f * x * (1.0f + f_tanh(c * (x + 0.044715f * x * x * x)));
+  const float k = -2.302208198144325f;
+  const float t = x * __builtin_fmaf(0.044715f * x, x, 1.0f);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(k * t));
 }
 __device__ __forceinline__ float f_mish(float x) {
   float ex = f_exp(k_min(x, 20.0f));

@@ -1094,10 +1094,33 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   int64_t ntn = sp.mms.size() > 1 ? 1 : (sp.N + sp.BN - 1) / sp.BN;
   int64_t ntm = (sp.M + sp.BM - 1) / sp.BM;
   int64_t KT = (sp.K + sp.BK - 1) / sp.BK;
+  // Intra-workgroup split of the contraction: when the tiles leave at most one
+  // workgroup per compute unit (one wave per SIMD, which issues an MFMA only
+  // every other slot) and K is long, the workgroup runs two groups of four
+  // waves, each over half of the k-tiles with operand buffers of its own, and
+  // adds the second group's accumulators to the first group's in the C tile
+  // (a fixed order).  Eight waves per compute unit then issue MFMAs and loads.
+  const size_t op_bytes = (size_t)2 * ((size_t)sp.BM * sp.BKP + (size_t)b_buf_elems(sp)) * dtype_bytes(sp.mtype);
+  const size_t ksplit_lds = std::max(2 * op_bytes, (size_t)sp.BM * sp.LDC * 4);
+  const bool ksplit = !sp.conv && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 && sp.NT == 256 &&
+                      ksplit_lds <= 160 * 1024 && !getenv("KORCH_GEMM_NO_KSPLIT");
+  const int64_t KH = (KT + 1) / 2;
   std::ostringstream s;
   s << source_header((int)gk.args.size());
-  s << "extern \"C\" __global__ void __launch_bounds__(" << sp.NT << ") " << gk.name << "(KArgs a) {\n";
-  s << gemm_prologue_common(sp);
+  if (ksplit) {
+    const std::string T = ctype(sp.mtype);
+    s << "extern \"C\" __global__ void __launch_bounds__(512) " << gk.name << "(KArgs a) {\n";
+    s << "  __shared__ __attribute__((aligned(16))) char smem[" << ksplit_lds << "];\n";
+    s << "  const int kgrp = threadIdx.x >> 8;  // which half of the k-tiles\n";
+    s << "  " << T << "* As = (" << T << "*)(smem + kgrp * " << op_bytes << ");\n";
+    s << "  " << T << "* Bs = As + " << 2 * sp.BM * sp.BKP << ";\n";
+    s << "  const int tid = threadIdx.x & 255, l = tid & 63, wave = tid >> 6;\n";
+    s << "  const int wm = wave / " << sp.WN << ", wn = wave % " << sp.WN << ";\n";
+    s << "  (void)wm; (void)wn;\n";
+  } else {
+    s << "extern \"C\" __global__ void __launch_bounds__(" << sp.NT << ") " << gk.name << "(KArgs a) {\n";
+    s << gemm_prologue_common(sp);
+  }
   // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
   // L2.  Renumber them so every XCD owns a contiguous range of tiles, and order
   // tiles in groups of GM row-tiles so the tiles running together on one XCD
@@ -1114,10 +1137,31 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   s << "  i64 q_ = bz_;\n";
   for (int d = sp.nb - 1; d >= 0; --d)
     s << "  const i64 z" << d << " = q_ % " << sp.OUT[d] << "LL; q_ /= " << sp.OUT[d] << "LL;\n";
-  s << "  const int kt0 = 0, kt1 = " << KT << ";\n";
+  if (ksplit)
+    s << "  const int kt0 = kgrp * " << KH << ", kt1 = kt0 + " << KH << " < " << KT << " ? kt0 + " << KH << " : " << KT
+      << ";\n";
+  else
+    s << "  const int kt0 = 0, kt1 = " << KT << ";\n";
   s << operand_loader(ki, sp, true, slot);
   s << operand_loader(ki, sp, false, slot);
-  if (sp.CROWS && sp.CROWS < sp.BM) {
+  if (ksplit) {
+    s << mfma_mainloop(sp, "", KH, KT % 2 == 0, false);
+    s << "  float* Cs = (float*)smem;\n";
+    auto ctile = [&](const char* op) {
+      std::ostringstream o;
+      o << "#pragma unroll\n    for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n    for (int j = 0; j < " << sp.FN
+        << "; ++j)\n#pragma unroll\n    for (int r = 0; r < 4; ++r) Cs[(wm * " << sp.WTM << " + i * 16 + (l >> 4) * 4 + r) * "
+        << sp.LDC << " + wn * " << sp.WTN << " + j * 16 + (l & 15)] " << op << " acc[i][j][r];\n";
+      return o.str();
+    };
+    s << "  if (kgrp == 0) {\n" << ctile("=") << "  }\n  __syncthreads();\n";
+    s << "  if (kgrp == 1) {\n" << ctile("+=") << "  }\n  __syncthreads();\n";
+    s << "  {\n  const int tid = threadIdx.x;\n";
+    GemmSpec ep = sp;
+    ep.NT = 512;
+    s << gemm_epilogue(ki, ep, slot, "ml * " + std::to_string(sp.LDC));
+    s << "  }\n";
+  } else if (sp.CROWS && sp.CROWS < sp.BM) {
     // The C tile passes through LDS one band of wave rows at a time (waves
     // with wm == p write rows [p*WTM, (p+1)*WTM), then every thread runs the
     // epilogue over them), so the fp32 staging area is WTM rows, not BM: the
@@ -1141,8 +1185,8 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   s << "}\n";
   gk.source = s.str();
   gk.grid[0] = (int)total;
-  gk.block[0] = sp.NT;
-  gk.lds_bytes = (int)gemm_smem_bytes(sp);
+  gk.block[0] = ksplit ? 512 : sp.NT;
+  gk.lds_bytes = ksplit ? (int)ksplit_lds : (int)gemm_smem_bytes(sp);
   if (gk.lds_bytes > 160 * 1024) fail(KORCH_E_UNSUPPORTED, "gemm: tiles need more than 160 KiB of LDS");
   ki.fill_cost(gk);
   return gk;

@@ -39,6 +39,14 @@ CONV_CASES = [
     dict(hh=9, ww=70, cin=32, cout=128),
 ]
 
+# MLP shapes of the GEMM-kernel GPU tests (GEMM2 wider than 128 columns, with one tile per compute
+# unit and a long contraction: an odd and an even number of k-tiles), each run
+# with the intra-workgroup split of K and without it (KORCH_GEMM_NO_KSPLIT=1).
+GEMM_CASES = [
+    dict(m=500, d=256, h=1056),
+    dict(m=256, d=192, h=2048),
+]
+
 # Sizes at which the chooser profiles every supported candidate (bench.py's
 # measured-cost plan at full size; the chooser GPU test at the sampled sizes).
 CHOOSER = {w: [{}, SAMPLED[w][0]] for w in SAMPLED}
@@ -55,7 +63,10 @@ def _jobs():
         jobs.append(("sampled", w, sz, (n, seed)))
     for sz in CONV_CASES + [{}]:
         for direct in ("1", "0"):
-            jobs.append(("conv_kernels", "conv", sz, direct))
+            jobs.append(("env_plans", "conv", sz, ("KORCH_CONV_DIRECT", direct)))
+    for sz in GEMM_CASES:
+        for flag in ("", "1"):
+            jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_NO_KSPLIT", flag)))
     for w, sizes in CHOOSER.items():
         for sz in sizes:
             jobs.append(("candidates", w, sz, None))
@@ -74,21 +85,25 @@ def _run_job(job, part=0, parts=1):
                 wl.plan(pn).compile()
             except KorchError as e:
                 failures.append((w, sz, pn, str(e)[:200]))
-    elif kind == "conv_kernels":
+    elif kind == "env_plans":
         import os
-        prev = os.environ.get("KORCH_CONV_DIRECT")
-        os.environ["KORCH_CONV_DIRECT"] = extra
+        var, val = extra
+        prev = os.environ.get(var)
+        if val:
+            os.environ[var] = val
+        else:
+            os.environ.pop(var, None)
         try:
             for pn in ("layered", "fused"):
                 try:
                     wl.plan(pn).compile()
                 except KorchError as e:
-                    failures.append((w, sz, f"{pn} direct={extra}", str(e)[:200]))
+                    failures.append((w, sz, f"{pn} {var}={val}", str(e)[:200]))
         finally:
             if prev is None:
-                os.environ.pop("KORCH_CONV_DIRECT")
+                os.environ.pop(var, None)
             else:
-                os.environ["KORCH_CONV_DIRECT"] = prev
+                os.environ[var] = prev
     elif kind == "sampled":
         for i, ks in enumerate(search.sampled_plans(wl.graph, *extra)):
             try:

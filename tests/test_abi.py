@@ -219,7 +219,8 @@ def test_every_plan_compiles_for_gfx950(workload):
             src = p.kernel_source(k)
             assert p.kernel_name(k) in src
             grid, block, _ = p.kernel_launch(k)
-            assert min(grid) >= 1 and block == (256, 1, 1)
+            assert min(grid) >= 1 and block in ((256, 1, 1), (512, 1, 1))
+            assert f"__launch_bounds__({block[0]})" in src
 
 
 def test_workspace_holds_only_intermediates():
@@ -314,3 +315,31 @@ def test_timed_execute_rejects_a_kernel_outside_the_range():
     n = p.num_kernels()
     assert code(lambda: p.execute_timed(0, n, [0] * 6, [0], 0, 0, 0, n, 0, 0)) == -1
     assert code(lambda: p.execute_timed(1, 1, [0] * 6, [0], 0, 0, 0, 0, 0, 0)) == -1
+
+
+def test_gemm_k_split_selection():
+    """GEMM2 of the MLP block (256 tiles, 48 k-tiles) and of the odd-k test shape
+    use the intra-workgroup split of K; GEMM1 (768 tiles) and
+    KORCH_GEMM_NO_KSPLIT=1 do not."""
+    from paper_2406_09465_amd.warm import GEMM_CASES
+
+    def sources(sizes, flag):
+        prev = os.environ.pop("KORCH_GEMM_NO_KSPLIT", None)
+        if flag:
+            os.environ["KORCH_GEMM_NO_KSPLIT"] = flag
+        try:
+            p = graphs.build("mlp", **sizes).plan("layered")
+            p.compile()
+            return [p.kernel_source(k) for k in range(p.num_kernels())], [p.kernel_launch(k) for k in range(3)]
+        finally:
+            os.environ.pop("KORCH_GEMM_NO_KSPLIT", None)
+            if prev is not None:
+                os.environ["KORCH_GEMM_NO_KSPLIT"] = prev
+
+    for sz in [{}] + GEMM_CASES:
+        src, launch = sources(sz, "")
+        assert "kgrp" in src[2] and launch[2][1][0] == 512, sz
+        src, launch = sources(sz, "1")
+        assert "kgrp" not in src[2] and launch[2][1][0] == 256, sz
+    src, _ = sources({}, "")
+    assert "kgrp" not in src[1]
