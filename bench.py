@@ -134,22 +134,34 @@ def main():
         # Orchestration over the primitive graph and over its transformed
         # version (Section 3 rewrites); the cheaper measured plan runs.
         from paper_2406_09465_amd import chooser
-        from paper_2406_09465_amd._abi import RW_ALL
-        from paper_2406_09465_amd.warm import CHOOSER_LIMITS
+        from paper_2406_09465_amd._abi import RW_ALL, RW_LAYOUT_VARIANTS
+        from paper_2406_09465_amd.warm import CHOOSER_LIMITS, LAYOUT_WORKLOADS
         t0 = time.time()
         hand = [k for name in ("fused", "layered") for k in w.kernels(name)]
         ch = chooser.korch_plan(w.graph, warmup=10, reps=50, extra=hand, **CHOOSER_LIMITS)
-        best, rules, alt = ch, 0, None
+        best, rules, w0 = ch, 0, w
+        alt = lay = None
         if not args.no_rewrite:
-            w2, napp = graphs.rewritten(w, RW_ALL)
-            if napp:
-                alt = chooser.korch_plan(w2.graph, warmup=10, reps=50, **CHOOSER_LIMITS)
-                if alt.cost_us < ch.cost_us:
-                    best, rules, w = alt, RW_ALL, w2
+            # the transformed graph, and the graph with layout variants of the
+            # computed product operands (layout as a plan variable)
+            for rr in (RW_ALL, RW_LAYOUT_VARIANTS):
+                if rr == RW_LAYOUT_VARIANTS and args.workload not in LAYOUT_WORKLOADS:
+                    continue
+                w2, napp = graphs.rewritten(w0, rr)
+                if not napp:
+                    continue
+                c2 = chooser.korch_plan(w2.graph, warmup=10, reps=50, **CHOOSER_LIMITS)
+                if rr == RW_ALL:
+                    alt = c2
+                else:
+                    lay = c2
+                if c2.cost_us < best.cost_us:
+                    best, rules, w = c2, rr, w2
         chosen = graphs.plan_record(w, best.kernels, rules)
         chosen.update({"predicted_us": round(best.cost_us, 3), "candidates": best.candidates,
                        "search_states": best.states, "original_graph_us": round(ch.cost_us, 3),
                        "rewritten_graph_us": round(alt.cost_us, 3) if alt else None,
+                       "layout_graph_us": round(lay.cost_us, 3) if lay else None,
                        "choose_seconds": round(time.time() - t0, 1)})
         r = PlanRunner(w, kernels=best.kernels)
     else:

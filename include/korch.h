@@ -167,13 +167,20 @@ typedef enum {
   KORCH_RW_REDUCE_AS_PRODUCT = 2,  /* sum over an axis -> product with a ones tensor, where a product
                                       on the same operand exists to merge with                      */
   KORCH_RW_MERGE_PRODUCTS = 4,     /* A . B1, A . B2 -> column slices of A . concat(B1, B2)          */
-  KORCH_RW_ALL = 7
+  KORCH_RW_FOLD_SCALE = 8,         /* (A . B) * s -> A . (B * s), s varying only along the output
+                                      columns (channels); also for convolutions and for division    */
+  KORCH_RW_ALL = 15,
+  KORCH_RW_LAYOUT_VARIANTS = 16    /* layout as a plan variable (Section 8): each computed operand of
+                                      a product is followed by transpose(transpose(x)) of its last
+                                      two axes, so a plan may store x in either layout; applied once,
+                                      after the other rules; not part of KORCH_RW_ALL              */
 } korch_rewrite_rule;
-/* Applies the selected rules until none applies and returns a new finalized
-   graph in *out (the caller destroys it) whose inputs and outputs correspond,
-   in order, to those of g; every output has the same value in exact
-   arithmetic.  *applied (may be NULL) receives the number of applications.
-   Node ids of *out are unrelated to those of g. */
+/* Applies the selected rules until none applies (the layout variants last,
+   once) and returns a new finalized graph in *out (the caller destroys it)
+   whose inputs and outputs correspond, in order, to those of g; every output
+   has the same value in exact arithmetic.  *applied (may be NULL) receives the
+   number of applications (each layout variant counts as one).  Node ids of
+   *out are unrelated to those of g. */
 int korch_graph_rewrite(const korch_graph* g, uint32_t rules, korch_graph** out, int32_t* applied);
 
 /* ---- orchestration analysis (Section 4.1) ------------------------------ */

@@ -101,6 +101,15 @@ bool conv_direct_fits(const GemmSpec& sp, std::string* why) {
   return plan_direct(sp, d, why);
 }
 
+bool conv_uses_direct(const GemmSpec& sp, std::string* why) {
+  const char* e = getenv("KORCH_CONV_DIRECT");
+  if (e && atoi(e) == 0) {
+    if (why) *why = "conv direct: switched off";
+    return false;
+  }
+  return conv_direct_fits(sp, why);
+}
+
 GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   Direct d;
   std::string why;
@@ -124,7 +133,8 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   const int64_t H = sp.H, W = sp.W, Cin = sp.Cin, N = sp.N;
   const int64_t HALO = d.halo_bytes / 2;  // elements of one halo buffer
   const std::string X = "a.p[" + std::to_string(slot.at(sp.A)) + "]";
-  const std::string Wt = "((const " + T + "*)a.p[" + std::to_string(slot.at(sp.Bs[0])) + "])";
+  // the weights as stored (when no prologue computes them)
+  const std::string Wt = sp.pro.empty() ? "((const " + T + "*)a.p[" + std::to_string(slot.at(sp.Bs[0])) + "])" : "";
   const int64_t xbytes = sp.batch * H * W * Cin * 2;
   const int64_t per_img = d.ntx * d.nty;
 
@@ -196,8 +206,28 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   s << "      const int row = v / " << NV << ", nv = v % " << NV << ", tap = row / " << d.CP << ", c = row % " << d.CP
     << ";\n";
   s << "      wv[i] = uint4{0u, 0u, 0u, 0u};\n";
-  s << "      if (v < " << WV << " && c < " << Cin << " && nv * 8 < " << N << ") wv[i] = *(const uint4*)(" << Wt
-    << " + ((i64)tap * " << Cin << " + c) * " << N << " + nv * 8);\n";
+  if (sp.pro.empty()) {
+    s << "      if (v < " << WV << " && c < " << Cin << " && nv * 8 < " << N << ") wv[i] = *(const uint4*)(" << Wt
+      << " + ((i64)tap * " << Cin << " + c) * " << N << " + nv * 8);\n";
+  } else {
+    // the weights are computed by the kernel's prologue (e.g. scaled per
+    // output channel): evaluated here, once per workgroup, 8 channels at a time
+    Emitter em(ki.g);
+    em.inset = sp.pro;
+    em.argslot = slot;
+    em.vec = 8;
+    std::vector<Ix> idx = {Ix::var("ky_"), Ix::var("kx_"), Ix::var("c"), Ix::var("n_", 1, 8)};
+    std::string val = em.value(sp.Bs[0], idx);
+    s << "      if (v < " << WV << " && c < " << Cin << " && nv * 8 < " << N << ") {\n";
+    s << "        const int ky_ = tap / " << sp.KW << ", kx_ = tap % " << sp.KW << ";\n";
+    s << "        const i64 n_ = (i64)nv * 8;\n";
+    s << "        (void)ky_; (void)kx_; (void)n_;\n";
+    s << "        vec_t<8, " << T << "> w_;\n";
+    s << em.pre.str();
+    s << "#pragma unroll\n        for (int e = 0; e < 8; ++e) {\n" << em.body.str() << "          w_[e] = fromf<" << T
+      << ">(" << val << ");\n        }\n";
+    s << "        wv[i] = __builtin_bit_cast(uint4, w_);\n      }\n";
+  }
   s << "    }\n";
   s << "#pragma unroll\n    for (int i = 0; i < " << WPT << "; ++i) {\n";
   s << "      const int v = tid + i * 256;\n";

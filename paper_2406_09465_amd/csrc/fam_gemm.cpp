@@ -35,8 +35,8 @@ bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_re
     sp.mms = {ki.linear[0]};
     sp.A = l0.in[0];
     sp.Bs = {l0.in[1]};
-    if (ki.in.count(sp.A) || ki.in.count(sp.Bs[0])) {
-      *why = "conv: operands must be materialized tensors";
+    if (ki.in.count(sp.A)) {
+      *why = "conv: the input must be a materialized tensor";
       return false;
     }
     const Shape& x = g.nodes[sp.A].shape;
@@ -161,8 +161,8 @@ bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_re
         *why = "gemm: a prologue value is also used after the product";
         return false;
       }
-  if (sp.conv && !sp.pro.empty()) {
-    *why = "conv: operand prologue not supported";
+  if (sp.conv && !sp.pro.empty() && !conv_uses_direct(sp, why)) {
+    if (why) *why = "conv: a weight prologue needs the direct kernel (" + *why + ")";
     return false;
   }
   // epilogue shapes broadcast to the iteration space
@@ -1078,10 +1078,8 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   GemmSpec sp;
   std::string why;
   if (!analyze_gemm(ki, sp, &why, false)) fail(KORCH_E_UNSUPPORTED, why);
-  if (sp.conv) {
-    const char* e = getenv("KORCH_CONV_DIRECT");  // "0" keeps the implicit-GEMM kernel
-    if (!(e && atoi(e) == 0) && conv_direct_fits(sp, nullptr)) return gen_conv_direct(ki, sp, index);
-  }
+  if (sp.conv && conv_uses_direct(sp, nullptr)) return gen_conv_direct(ki, sp, index);
+  if (sp.conv && !sp.pro.empty()) fail(KORCH_E_UNSUPPORTED, "conv: a weight prologue needs the direct kernel");
   choose_tiles(sp, false);
   plan_operands(ki, sp);
   if ((sp.K + sp.BK - 1) / sp.BK > 128) sp.NS = 2;  // long contractions use the rolled loop

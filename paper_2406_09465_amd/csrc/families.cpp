@@ -689,7 +689,60 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
 // Dispatcher
 // ---------------------------------------------------------------------------
 
+// A transpose of a transpose with inverse permutations is the identity.  When
+// a kernel computes both (a layout-variant pair, or any such chain) and the
+// inner one is not an output, the kernel's nodes that read the outer one read
+// the original tensor instead, and transposes left without a reader in the
+// kernel (and not outputs) are dropped.  The families then see the kernel
+// as if the pair were not there.  g2 differs from g only in those edges, so
+// node ids (and the plan's storage) are unchanged.  Returns false when
+// nothing collapses.
+static bool collapse_identity_layouts(const Graph& g, const KernelDesc& k, Graph& g2, KernelDesc& k2) {
+  std::set<int> in(k.prims.begin(), k.prims.end()), outs(k.outs.begin(), k.outs.end());
+  std::map<int, int> alias;
+  for (int v : k.prims) {
+    const Node& n = g.nodes[v];
+    if (n.op != KORCH_TRANSPOSE || outs.count(v) || !in.count(n.in[0])) continue;
+    const Node& t = g.nodes[n.in[0]];
+    if (t.op != KORCH_TRANSPOSE) continue;
+    bool ident = true;
+    for (int d = 0; d < n.attrs.rank; ++d) ident = ident && t.attrs.perm[n.attrs.perm[d]] == d;
+    if (ident) alias[v] = t.in[0];
+  }
+  if (alias.empty()) return false;
+  g2 = g;
+  g2.finalized = false;
+  for (int v : k.prims)
+    for (int& u : g2.nodes[v].in) {
+      auto f = alias.find(u);
+      if (f != alias.end()) u = f->second;
+    }
+  g2.finalize();
+  std::set<int> keep;
+  for (int v : k.prims)
+    if (!alias.count(v)) keep.insert(v);
+  for (auto& [v, x] : alias) {
+    (void)x;
+    int t = g.nodes[v].in[0];
+    bool read = outs.count(t) > 0;
+    for (int c : g2.consumers[t]) read = read || keep.count(c);
+    if (!read) keep.erase(t);
+  }
+  k2.prims.assign(keep.begin(), keep.end());
+  k2.outs = k.outs;
+  return true;
+}
+
+static int match_family_canonical(const Graph& g, const KernelDesc& k, std::string* why);
+
 int match_family(const Graph& g, const KernelDesc& k, std::string* why) {
+  Graph g2;
+  KernelDesc k2;
+  if (collapse_identity_layouts(g, k, g2, k2)) return match_family_canonical(g2, k2, why);
+  return match_family_canonical(g, k, why);
+}
+
+static int match_family_canonical(const Graph& g, const KernelDesc& k, std::string* why) {
   std::string w;
   if (!why) why = &w;
   try {
@@ -722,9 +775,18 @@ int match_family(const Graph& g, const KernelDesc& k, std::string* why) {
   return KORCH_FAM_NONE;
 }
 
+static GenKernel generate_canonical(const Graph& g, const KernelDesc& k, int index);
+
 GenKernel generate_kernel(const Graph& g, const KernelDesc& k, int index) {
+  Graph g2;
+  KernelDesc k2;
+  if (collapse_identity_layouts(g, k, g2, k2)) return generate_canonical(g2, k2, index);
+  return generate_canonical(g, k, index);
+}
+
+static GenKernel generate_canonical(const Graph& g, const KernelDesc& k, int index) {
   std::string why;
-  int fam = match_family(g, k, &why);
+  int fam = match_family_canonical(g, k, &why);
   KInfo ki(g, k);
   bool half_outputs = true;
   for (int o : k.outs)

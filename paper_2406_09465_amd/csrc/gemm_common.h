@@ -76,6 +76,9 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
 // Direct convolution (stride 1, half precision, input halo tile in LDS,
 // weights in registers); conv_direct_fits says whether it applies.
 bool conv_direct_fits(const GemmSpec& sp, std::string* why);
+// conv_direct_fits and not switched off (KORCH_CONV_DIRECT=0 keeps the
+// implicit-GEMM kernel, which takes no operand prologue).
+bool conv_uses_direct(const GemmSpec& sp, std::string* why);
 GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index);
 std::string gemm_prologue_common(const GemmSpec& sp);
 size_t gemm_smem_bytes(const GemmSpec& sp);

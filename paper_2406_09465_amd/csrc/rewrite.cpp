@@ -9,7 +9,20 @@
 //    T . 1 (a ones column); a sum over the last axis of a tensor that is the
 //    left operand of a product equals X . 1;
 //  * product merge: A . B1 and A . B2 equal two column slices of
-//    A . concat(B1, B2) (concatenation along the column axis).
+//    A . concat(B1, B2) (concatenation along the column axis);
+//  * scale folding: a product or convolution scaled (multiplied or divided)
+//    by a tensor that varies only along the output-column (output-channel)
+//    axis equals the product with that scale applied to the columns of its
+//    right operand (the weights), e.g. inference BatchNorm folded into a
+//    convolution's weights.
+//
+// Layout variants (the data-layout extension of the orchestration problem,
+// Section 8): every intermediate tensor that a product reads as an operand is
+// followed by a pair of mutually inverse transposes of its last two axes, and
+// its consumers read the second.  A plan may then materialize the tensor in
+// its own layout or in the transposed one (the first transpose), and each
+// consuming kernel reads whichever is available; the measured-cost chooser
+// picks.  The pair is inserted once, after the other rules, and is not folded.
 //
 // The graph is rebuilt after every application: a recursive emitter creates
 // each needed node after its operands (so the order is topological and dead
@@ -332,6 +345,79 @@ std::vector<Subst> merge_products(const Graph& g) {
   return out;
 }
 
+std::vector<Subst> fold_scale(const Graph& g) {
+  std::vector<Subst> out;
+  std::vector<char> is_out(g.nodes.size(), 0);
+  for (int o : g.outputs) is_out[o] = 1;
+  for (const Node& m : g.nodes) {
+    if ((m.op != KORCH_MUL && m.op != KORCH_DIV) || m.attrs.has_scalar || m.in.size() != 2) continue;
+    for (int side = 0; side < 2; ++side) {
+      if (m.op == KORCH_DIV && side == 1) break;  // only (product) / scale
+      const Node& lin = g.nodes[m.in[side]];
+      if (lin.op != KORCH_MATMUL && lin.op != KORCH_CONV2D) continue;
+      if (g.consumers[lin.id].size() != 1 || is_out[lin.id]) continue;
+      const Node& sc = g.nodes[m.in[1 - side]];
+      const int64_t N = lin.shape.back();
+      if (sc.shape.empty() || sc.shape.back() != N || sc.shape.size() > lin.shape.size() || m.shape != lin.shape) continue;
+      bool cols_only = true;
+      for (size_t d = 0; d + 1 < sc.shape.size(); ++d) cols_only = cols_only && sc.shape[d] == 1;
+      if (!cols_only) continue;
+      const int A = lin.in[0], B = lin.in[1], S = sc.id, op = m.op, lop = lin.op, mdt = m.dtype;
+      const int bdt = g.nodes[B].dtype, sdt = sc.dtype;
+      const korch_attrs la = lin.attrs;
+      Subst sub;
+      sub[m.id] = [=](Builder& b) {
+        int s1 = reshape(b, b.get(S), {N}, sdt);
+        int bs = b.add(op, {b.get(B), s1}, no_attrs(), bdt);
+        return b.add(lop, {b.get(A), bs}, la, mdt);
+      };
+      out.push_back(sub);
+    }
+  }
+  return out;
+}
+
+// The layout-variant graph (see the header comment).  Eligible: a computed
+// tensor (not a graph input or output, not a layout node or constant) of rank
+// >= 2 whose last two axes both exceed 1 and that some product or convolution
+// reads as an operand.
+Graph layout_variants(const Graph& g, int* applied) {
+  Graph out;
+  std::vector<int> map(g.nodes.size(), -1);
+  std::vector<char> is_out(g.nodes.size(), 0);
+  for (int o : g.outputs) is_out[o] = 1;
+  int n = 0;
+  for (const Node& v : g.nodes) {
+    if (v.op == KORCH_INPUT) {
+      map[v.id] = out.add_input(v.dtype, v.shape);
+      continue;
+    }
+    std::vector<int> in;
+    for (int u : v.in) in.push_back(map[u]);
+    int id = out.add_op(v.op, in, &v.attrs, v.dtype);
+    map[v.id] = id;
+    const int r = (int)v.shape.size();
+    Kind k = op_kind(v.op);
+    bool eligible = !is_out[v.id] && r >= 2 && v.shape[r - 1] > 1 && v.shape[r - 2] > 1 && k != Kind::Layout &&
+                    v.op != KORCH_FILL;
+    bool operand = false;
+    for (int c : g.consumers[v.id])
+      if (g.nodes[c].op == KORCH_MATMUL || g.nodes[c].op == KORCH_CONV2D) operand = true;
+    if (!eligible || !operand) continue;
+    korch_attrs t = no_attrs();
+    t.rank = r;
+    for (int d = 0; d < r; ++d) t.perm[d] = d;
+    std::swap(t.perm[r - 1], t.perm[r - 2]);
+    int vt = out.add_op(KORCH_TRANSPOSE, {id}, &t, v.dtype);
+    map[v.id] = out.add_op(KORCH_TRANSPOSE, {vt}, &t, v.dtype);
+    ++n;
+  }
+  for (int o : g.outputs) out.add_output(map[o]);
+  out.finalize();
+  if (applied) *applied = n;
+  return out;
+}
+
 Graph replay(const Graph& g, const Subst& sub) {
   Builder b(g);
   b.subst = sub;
@@ -348,6 +434,7 @@ Graph rewrite_graph(const Graph& g0, uint32_t rules, int* applied) {
   if (rules & KORCH_RW_DEFER_DIV) active.push_back(defer_div);
   if (rules & KORCH_RW_REDUCE_AS_PRODUCT) active.push_back(reduce_as_product);
   if (rules & KORCH_RW_MERGE_PRODUCTS) active.push_back(merge_products);
+  if (rules & KORCH_RW_FOLD_SCALE) active.push_back(fold_scale);
   for (int iter = 0; iter < 256; ++iter) {
     bool changed = false;
     for (Rule r : active) {
@@ -364,6 +451,11 @@ Graph rewrite_graph(const Graph& g0, uint32_t rules, int* applied) {
       if (changed) break;
     }
     if (!changed) break;
+  }
+  if (rules & KORCH_RW_LAYOUT_VARIANTS) {
+    int m = 0;
+    g = layout_variants(g, &m);
+    n += m;
   }
   if (applied) *applied = n;
   return g;

@@ -2,12 +2,23 @@
 
   python -m paper_2406_09465_amd.experiments shapes --out profiles/chooser_shapes.md
 
+  python -m paper_2406_09465_amd.experiments layouts --out profiles/chooser_layouts.md
+
 ``shapes``: the measured-cost chooser on one workload at several sizes.  The
 paper observes that the best orchestration of the same subgraph changes with its
 shape (a memory-bound subgraph fused into one kernel at batch 1 but split into
 several at batch 16, Section 6): the chosen plan here is recorded per size with
 its number of kernels, its predicted cost (sum of measured kernel latencies)
 and the cost of fusing everything the families allow into the fewest kernels.
+
+``layouts``: data layout as a plan variable (the extension of the
+orchestration formulation in Section 8).  Each workload's graph gets a
+transposed-layout variant of every computed operand of a product
+(``RW_LAYOUT_VARIANTS``); the chooser then decides, per tensor, in which layout
+it is materialized and how each consumer reads it.  Recorded per workload: the
+chosen plan on the original and on the variant graph, and, for each variant,
+the cheapest plan that stores that tensor only in the transposed layout (its
+row-major kernels removed), i.e. what the layout choice is weighed against.
 """
 
 from __future__ import annotations
@@ -88,14 +99,66 @@ def shapes(workload, out, warmup=10, reps=50):
     open(out, "w").write("\n".join(lines) + "\n")
 
 
+def layouts(out, workloads=None, warmup=10, reps=50):
+    from ._abi import RW_LAYOUT_VARIANTS
+    from .warm import LAYOUT_WORKLOADS
+    wls = list(workloads or LAYOUT_WORKLOADS)
+    lines = ["# Data layout as a plan variable", "", "Command:", "", "```",
+             f"python -m paper_2406_09465_amd.experiments layouts --out {out}", "```", "",
+             f"Full-size workloads; costs are medians of {reps} launches after {warmup} warm-up launches, each after a "
+             "512 MiB cache flush.  `x^T` is tensor x stored with its last two axes swapped.", "",
+             "| workload | original graph (us, kernels) | variant graph (us, kernels) | layouts chosen | "
+             "cheapest plan storing only x^T, per variant (us) |", "|---|---|---|---|---|"]
+    for wl in wls:
+        w = graphs.build(wl)
+        base = chooser.korch_plan(w.graph, **LIMITS, warmup=warmup, reps=reps)
+        w2, n = graphs.rewritten(w, RW_LAYOUT_VARIANTS)
+        g = w2.graph
+        ch = chooser.korch_plan(g, **LIMITS, warmup=warmup, reps=reps)
+        view = GraphView(g)
+        # variant pairs: x -> x^T -> (x^T)^T
+        pairs = []
+        for v in range(g.num_nodes()):
+            if view.op[v] == "transpose" and view.op[view.ins[v][0]] != "transpose":
+                nxt = [c for c in range(g.num_nodes()) if view.op[c] == "transpose" and view.ins[c] == [v]]
+                if nxt:
+                    pairs.append((view.ins[v][0], v))
+        names = {}
+        orig_names = {v: k for k, v in w.ids.items()}
+        for x, xt in pairs:
+            op, _, shape = g.node_info(x)
+            names[x] = f"{op}{list(shape)}"
+            names[xt] = names[x] + "^T"
+        chosen_t = sorted({names[o] for _, outs in ch.kernels for o in outs if o in names and o in dict(pairs).values()})
+        forced = []
+        cands = list(ch.costs)
+        for x, xt in pairs:
+            costs = [None if x in o else ch.costs[(p, o)] for p, o in cands]
+            try:
+                f = chooser.choose(view, cands, costs)
+                forced.append(f"{names[xt]}: {f.cost_us:.2f}")
+            except RuntimeError:
+                forced.append(f"{names[xt]}: no plan")
+        lines.append(f"| {wl} | {base.cost_us:.2f}, {len(base.kernels)} | {ch.cost_us:.2f}, {len(ch.kernels)} | "
+                     f"{', '.join(chosen_t) or 'none (all row-major)'} | {'; '.join(forced)} |")
+        print(lines[-1], flush=True)
+    open(out, "w").write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="mode", required=True)
     s = sub.add_parser("shapes")
     s.add_argument("--workload", default="attention", choices=list(SWEEPS))
     s.add_argument("--out", required=True)
+    lo = sub.add_parser("layouts")
+    lo.add_argument("--out", required=True)
+    lo.add_argument("--workloads", nargs="*", default=None)
     a = ap.parse_args()
-    shapes(a.workload, a.out)
+    if a.mode == "shapes":
+        shapes(a.workload, a.out)
+    else:
+        layouts(a.out, a.workloads)
 
 
 if __name__ == "__main__":

@@ -277,8 +277,10 @@ def rewritten(w: Workload, rules=None):
 def plan_record(w: Workload, kernels, rules=0):
     """JSON-able record of a plan of ``w`` (or of its rewritten graph when
     ``rules`` is non-zero): node ids, plus names where the workload names them."""
+    from ._abi import RW_LAYOUT_VARIANTS
     names = {v: k for k, v in w.ids.items()} if not rules else {}
-    return {"graph": "rewritten" if rules else "original", "rules": int(rules),
+    label = "original" if not rules else "layout variants" if rules == RW_LAYOUT_VARIANTS else "rewritten"
+    return {"graph": label, "rules": int(rules),
             "kernel_ids": [[list(map(int, p)), list(map(int, o))] for p, o in kernels],
             "kernels": [[[names.get(v, f"#{v}") for v in p], [names.get(v, f"#{v}") for v in o]] for p, o in kernels]}
 

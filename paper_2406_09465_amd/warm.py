@@ -47,6 +47,9 @@ GEMM_CASES = [
     dict(m=256, d=192, h=2048),
 ]
 
+# Workloads whose computed product operands get layout variants.
+LAYOUT_WORKLOADS = ("attention", "mlp", "sra", "linattn")
+
 # Sizes at which the chooser profiles every supported candidate (bench.py's
 # measured-cost plan at full size; the chooser GPU test at the sampled sizes).
 CHOOSER = {w: [{}, SAMPLED[w][0]] for w in SAMPLED}
@@ -61,6 +64,8 @@ def _jobs():
             jobs.append(("plans", w, sz, None))
     for w, (sz, n, seed) in SAMPLED.items():
         jobs.append(("sampled", w, sz, (n, seed)))
+        if w in LAYOUT_WORKLOADS:
+            jobs.append(("sampled_layouts", w, sz, (n, seed)))
     for sz in CONV_CASES + [{}]:
         for direct in ("1", "0"):
             jobs.append(("env_plans", "conv", sz, ("KORCH_CONV_DIRECT", direct)))
@@ -71,6 +76,8 @@ def _jobs():
         for sz in sizes:
             jobs.append(("candidates", w, sz, None))
             jobs.append(("candidates", w, sz, "rewritten"))
+            if w in LAYOUT_WORKLOADS:
+                jobs.append(("candidates", w, sz, "layouts"))
     return jobs
 
 
@@ -104,15 +111,19 @@ def _run_job(job, part=0, parts=1):
                 os.environ.pop(var, None)
             else:
                 os.environ[var] = prev
-    elif kind == "sampled":
+    elif kind in ("sampled", "sampled_layouts"):
+        if kind == "sampled_layouts":
+            from ._abi import RW_LAYOUT_VARIANTS
+            wl, _ = graphs.rewritten(wl, RW_LAYOUT_VARIANTS)
         for i, ks in enumerate(search.sampled_plans(wl.graph, *extra)):
             try:
                 graphs.Plan(wl.graph, ks).compile()
             except KorchError as e:
                 failures.append((w, sz, f"sampled {i}", str(e)[:200]))
     else:
-        if extra == "rewritten":
-            wl, n = graphs.rewritten(wl)
+        if extra in ("rewritten", "layouts"):
+            from ._abi import RW_LAYOUT_VARIANTS
+            wl, n = graphs.rewritten(wl, RW_LAYOUT_VARIANTS if extra == "layouts" else None)
             if n == 0:
                 return failures
         cands = wl.graph.candidates(only_supported=True, **CHOOSER_LIMITS)

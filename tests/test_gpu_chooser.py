@@ -53,7 +53,7 @@ def test_chosen_plan(workload):
         assert ok, f"{workload} chosen plan {ch.kernels}: max err {mx:.3e} rel {rel:.3e}"
 
 
-@pytest.mark.parametrize("workload", ["attention", "sra", "linattn"])
+@pytest.mark.parametrize("workload", ["attention", "sra", "linattn", "conv"])
 def test_chosen_plan_of_transformed_graph(workload):
     """Orchestration of the rewritten primitive graph (Section 3 transformations):
     the chosen plan must reproduce the oracle of the original graph."""
@@ -73,3 +73,32 @@ def test_chosen_plan_of_transformed_graph(workload):
     for name in w.output_names:
         ok, mx, rel = close(out[name], ref[name], TOL[w.dtype])
         assert ok, f"{workload} transformed plan {ch.kernels}: max err {mx:.3e} rel {rel:.3e}"
+
+
+@pytest.mark.parametrize("workload", ["attention", "mlp", "sra", "linattn"])
+def test_layout_variant_plans(workload):
+    """Layout as a plan variable: on the graph with a transposed-layout variant
+    of every computed product operand, seeded random valid plans (which
+    materialize some operands transposed) and the measured-cost choice both
+    reproduce the oracle of the original graph."""
+    from paper_2406_09465_amd import chooser, graphs, search
+    from paper_2406_09465_amd._abi import RW_LAYOUT_VARIANTS
+    from paper_2406_09465_amd.runner import PlanRunner
+    from paper_2406_09465_amd.warm import CHOOSER_LIMITS, SAMPLED
+    sizes = SIZES[workload]
+    assert SAMPLED[workload][0] == sizes
+    w, napp = graphs.rewritten(graphs.build(workload, **sizes), RW_LAYOUT_VARIANTS)
+    assert napp > 0
+    raw, x64 = inputs_f64(workload, **sizes)
+    ref = run_unfused(OC.build(workload, **sizes), x64)
+    _, n, seed = SAMPLED[workload]
+    plans = search.sampled_plans(w.graph, n, seed)
+    print(f"\n[case] {workload} layout variants at {sizes}", flush=True)
+    ch = chooser.korch_plan(w.graph, warmup=3, reps=10, flush_bytes=64 << 20, **CHOOSER_LIMITS)
+    assert not ch.failures, ch.failures[:2]
+    for i, ks in enumerate(plans + [ch.kernels]):
+        print(f"[case] {workload} layout plan {i}: {len(ks)} kernels", flush=True)
+        out = PlanRunner(w, kernels=ks).run(raw)
+        for name in w.output_names:
+            ok, mx, rel = close(out[name], ref[name], TOL[w.dtype])
+            assert ok, f"{workload} layout plan {i} {ks}: max err {mx:.3e} rel {rel:.3e}"

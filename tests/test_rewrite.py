@@ -23,7 +23,8 @@ SMALL = {
     "instnorm": dict(hh=6, ww=5, c=8),
 }
 RULESETS = [K.RW_DEFER_DIV, K.RW_REDUCE_AS_PRODUCT, K.RW_MERGE_PRODUCTS,
-            K.RW_REDUCE_AS_PRODUCT | K.RW_MERGE_PRODUCTS, K.RW_ALL]
+            K.RW_REDUCE_AS_PRODUCT | K.RW_MERGE_PRODUCTS, K.RW_FOLD_SCALE, K.RW_ALL, K.RW_LAYOUT_VARIANTS,
+            K.RW_ALL | K.RW_LAYOUT_VARIANTS]
 
 
 def to_oracle(g):
@@ -150,3 +151,73 @@ def test_rewritten_workload_keeps_names():
     w2, n = graphs.rewritten(w)
     assert n > 0 and w2.input_names == w.input_names and w2.output_names == w.output_names
     assert [w2.ids[k] for k in w2.input_names] == w2.graph.inputs()
+
+
+def test_batchnorm_scale_folds_into_the_convolution_weights():
+    """conv(X, W) * scale + shift becomes conv(X, W * scale) + shift."""
+    w = graphs.build("conv", **SMALL["conv"])
+    g2, n = w.graph.rewrite(K.RW_FOLD_SCALE)
+    assert n == 1
+    conv = [v for v in range(g2.num_nodes()) if g2.node_info(v)[0] == "conv2d"]
+    assert len(conv) == 1
+    x, wt = g2.node_inputs(conv[0])
+    assert g2.node_info(x)[0] == "input" and g2.node_info(wt)[0] == "mul"
+    assert [g2.node_info(u)[0] for u in g2.node_inputs(wt)][0] == "input"
+    assert g2.node_info(wt)[2] == (3, 3, 8, 16)
+    (c,) = [v for v in range(g2.num_nodes()) if conv[0] in g2.node_inputs(v)]
+    assert g2.node_info(c)[0] == "add"
+
+
+def _product_then(op, scale_shape, second_consumer=False):
+    g = K.Graph()
+    a = g.input("f32", (6, 5))
+    b = g.input("f32", (5, 4))
+    s = g.input("f32", scale_shape)
+    m = g.op("matmul", [a, b], "f32")
+    y = g.op(op, [m, s], "f32")
+    g.output(y)
+    if second_consumer:
+        g.output(g.op("relu", [m], "f32"))
+    g.finalize()
+    return g
+
+
+def test_fold_scale_applies_only_to_column_scales_of_a_single_use_product():
+    assert _product_then("mul", (4,)).rewrite(K.RW_FOLD_SCALE)[1] == 1
+    assert _product_then("div", (1, 4)).rewrite(K.RW_FOLD_SCALE)[1] == 1
+    assert _product_then("mul", (6, 1)).rewrite(K.RW_FOLD_SCALE)[1] == 0  # varies along rows
+    assert _product_then("add", (4,)).rewrite(K.RW_FOLD_SCALE)[1] == 0
+    assert _product_then("mul", (4,), second_consumer=True).rewrite(K.RW_FOLD_SCALE)[1] == 0
+
+
+def test_fold_scale_division_in_float64():
+    """(A . B) / s equals A . (B / s) on random data."""
+    g = _product_then("div", (4,))
+    g2, n = g.rewrite(K.RW_FOLD_SCALE)
+    rng = np.random.default_rng(3)
+    x = [rng.normal(size=(6, 5)), rng.normal(size=(5, 4)), rng.uniform(0.5, 2.0, size=(4,))]
+    (y,) = outputs_by_position(to_oracle(g2), x)
+    assert n == 1 and np.allclose(y, (x[0] @ x[1]) / x[2], rtol=1e-13, atol=1e-13)
+
+
+def test_layout_variants_follow_product_operands():
+    """Each computed operand of a product gets transpose(transpose(.)) of its
+    last two axes; the MLP block's normalized input Y and hidden Hg qualify."""
+    w = graphs.build("mlp", **SMALL["mlp"])
+    g2, n = w.graph.rewrite(K.RW_LAYOUT_VARIANTS)
+    assert n == 2
+    pairs = 0
+    for v in range(g2.num_nodes()):
+        op, _, shape = g2.node_info(v)
+        if op != "transpose":
+            continue
+        (u,) = g2.node_inputs(v)
+        if g2.node_info(u)[0] == "transpose":
+            pairs += 1
+            (x,) = g2.node_inputs(u)
+            assert g2.node_info(x)[2] == shape and g2.node_attrs(v)["perm"] == (1, 0)
+            assert any(g2.node_info(c)[0] == "matmul" for c in range(g2.num_nodes()) if v in g2.node_inputs(c))
+    assert pairs == 2
+    # graph inputs and outputs, layout nodes and row vectors never get variants
+    assert graphs.build("conv", **SMALL["conv"]).graph.rewrite(K.RW_LAYOUT_VARIANTS)[1] == 0
+    assert graphs.build("instnorm", **SMALL["instnorm"]).graph.rewrite(K.RW_LAYOUT_VARIANTS)[1] == 0
