@@ -225,8 +225,11 @@ def main():
     fam, abytes, aflops = r.plan.kernel_info(dom)
     name = r.plan.kernel_name(dom)
     src_hash = hashlib.sha256(r.plan.kernel_source(dom).encode()).hexdigest()[:16]
-    if aflops > 0 and fam in ("gemm", "conv", "attention", "splitk") and aflops / max(abytes, 1) > 100:
-        peak = PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK[f"mfma_{w.dtype}_TFLOPs"]
+    # bound by the roofline: above the ridge (peak flops of the dtype / HBM
+    # bandwidth) the kernel is compute-bound, below it memory-bound
+    peak = PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK[f"mfma_{w.dtype}_TFLOPs"]
+    ridge = peak * 1e12 / (PEAK["hbm_GBs"] * 1e9)
+    if aflops > 0 and fam in ("gemm", "conv", "attention", "splitk") and aflops / max(abytes, 1) > ridge:
         achieved = aflops / (dom_us * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4)}
