@@ -210,13 +210,15 @@ def main():
     for i in sampled:
         starts[i].record(stream)
         ends[i].record(stream)
+    r.bind(stream)
+    timed_at = [starts.get(i) for i in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        if i in starts:
-            r.launch_timed(dom, starts[i], ends[i])
+        if timed_at[i] is not None:
+            r.launch_timed_bound(dom, timed_at[i], ends[i])
         else:
-            r.launch()
+            r.launch_bound()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
@@ -244,6 +246,27 @@ def main():
     roof["alg_bytes"] = abytes
     roof["alg_flops"] = aflops
 
+    # context floors (same run, same stream): a launch of a one-element kernel,
+    # and a device copy moving the plan's algorithmic bytes per step (half read,
+    # half written), each timed back to back
+    def per_launch_us(fn, n=200):
+        fn()
+        a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a_.record(stream)
+        for _ in range(n):
+            fn()
+        b_.record(stream)
+        torch.cuda.synchronize()
+        return a_.elapsed_time(b_) * 1e3 / n
+    step_bytes = sum(r.plan.kernel_info(k)[1] for k in range(nk))
+    one = torch.zeros(1, device="cuda")
+    csrc = torch.empty(max(16, int(step_bytes) // 2), dtype=torch.uint8, device="cuda")
+    cdst = torch.empty_like(csrc)
+    floors = {"empty_kernel_us": round(per_launch_us(lambda: one.add_(1.0)), 3),
+              "copy_us": round(per_launch_us(lambda: cdst.copy_(csrc)), 3), "copy_bytes_moved": 2 * csrc.numel()}
+    del one, csrc, cdst
+
     kernels = []
     for k in range(nk):
         f, b, fl = r.plan.kernel_info(k)
@@ -266,6 +289,7 @@ def main():
         "config": {"workload": DESCR[args.workload], "plan": "recorded" if args.kernels_json else args.plan,
                    "kernels": nk},
         "roofline": roof,
+        "floors": floors,
         "kernels": kernels,
     }
     if chosen:

@@ -12,9 +12,7 @@ extern "C" hipError_t hipExtModuleLaunchKernel(hipFunction_t f, uint32_t globalW
                                                hipEvent_t startEvent, hipEvent_t stopEvent, uint32_t flags);
 
 #include <algorithm>
-#include <atomic>
 #include <cstdlib>
-#include <thread>
 
 #include "families.h"
 #include "plan.h"
@@ -49,33 +47,22 @@ void generate_plan(Plan& p) {
   plan_workspace(p);
 }
 
+// Kernels are compiled on the calling thread: hipRTC runs in a link namespace
+// of its own with its own C library, whose per-thread state does not cover
+// threads created by the process's main C library.
 void compile_plan(Plan& p) {
   if (p.compiled) return;
   generate_plan(p);
   int n = (int)p.ck.size();
-  int nt = std::min(n, 8);
-  std::atomic<int> next{0};
-  std::vector<std::string> errors(n);
-  std::vector<int> codes(n, 0);
-  auto work = [&]() {
-    for (int k = next++; k < n; k = next++) {
-      try {
-        p.ck[k].code = rtc_compile(p.ck[k].gen.source, p.ck[k].gen.name);
-      } catch (Error& e) {
-        errors[k] = e.what();
-        codes[k] = e.code;
-      } catch (std::exception& e) {
-        errors[k] = e.what();
-        codes[k] = KORCH_E_COMPILE;
-      }
+  for (int k = 0; k < n; ++k) {
+    try {
+      p.ck[k].code = rtc_compile(p.ck[k].gen.source, p.ck[k].gen.name);
+    } catch (Error& e) {
+      fail(e.code, "kernel " + std::to_string(k) + ": " + e.what());
+    } catch (std::exception& e) {
+      fail(KORCH_E_COMPILE, "kernel " + std::to_string(k) + ": " + e.what());
     }
-  };
-  std::vector<std::thread> th;
-  for (int t = 1; t < nt; ++t) th.emplace_back(work);
-  work();
-  for (auto& t : th) t.join();
-  for (int k = 0; k < n; ++k)
-    if (codes[k]) fail(codes[k], "kernel " + std::to_string(k) + ": " + errors[k]);
+  }
   p.compiled = true;
 }
 

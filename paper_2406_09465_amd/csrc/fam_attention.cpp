@@ -188,6 +188,18 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   size_t smem = ks_bytes + v_bytes + p_bytes;
   if (smem != attention_lds_bytes(a) || smem > 160 * 1024)
     fail(KORCH_E_UNSUPPORTED, "attention: keys and values exceed the 160 KiB of LDS");
+  // Few query rows (fewer than 64 workgroups of 64 rows): split the keys over
+  // the four waves instead, one workgroup per 16 query rows.  Each wave scores
+  // its quarter of the keys; row maxima and row sums are combined across the
+  // waves through LDS, and the four partial P.V products are added in wave
+  // order (deterministic).
+  const int kalign = f32 ? 16 : 32;  // keys per S fragment / per P.V step
+  const int64_t NKW = nkp / 4;
+  const size_t red_off = (smem + 15) / 16 * 16, op_off = red_off + 2 * 4 * 16 * 4;
+  const size_t smem_split = op_off + (size_t)4 * 16 * dvp * 4;
+  const bool ksplit = (a.nq + 63) / 64 * a.batch < 64 && nkp % (4 * kalign) == 0 && smem_split <= 160 * 1024 &&
+                      !getenv("KORCH_ATTN_NO_KEY_SPLIT");
+  if (ksplit) smem = smem_split;
   std::string Q = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.q)) + "])";
   std::string K = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.kx)) + "])";
   std::string V = "((const " + T + "*)a.p[" + std::to_string(slot.at(a.v)) + "])";
@@ -249,6 +261,98 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     s << "  }\n";
   }
   s << "  __syncthreads();\n";
+  std::string chain_expr = "x";
+  for (int c : a.chain) {
+    const Node& cn = g.nodes[c];
+    if (op_kind(cn.op) == Kind::Unary)
+      chain_expr = unary_expr(cn.op, chain_expr);
+    else
+      chain_expr = binary_expr(cn.op, chain_expr, flit(cn.attrs.scalar));
+  }
+  if (ksplit) {
+    const int NFW = (int)(NKW / 16);
+    s << "  const i64 q0 = (i64)blockIdx.x * 16;\n";
+    s << "  const i64 qr = q0 + (l & 15);\n";
+    s << "  const bool qv = qr < " << a.nq << "LL;\n";
+    s << "  const int kb = wave * " << NKW << ";  // this wave's keys [kb, kb + " << NKW << ")\n";
+    s << "  f32x4 sc[" << NFW << "];\n";
+    s << "#pragma unroll\n  for (int f = 0; f < " << NFW << "; ++f) sc[f] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
+    if (f32) {
+      s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 4 << "; ++kk) {\n";
+      s << "    const int dim = kk * 4 + (l >> 4);\n";
+      s << "    const float qa = (qv && dim < " << a.d << ") ? " << Q << "[qoff + qr * " << a.d << " + dim] : 0.0f;\n";
+      s << "#pragma unroll\n    for (int f = 0; f < " << NFW << "; ++f) sc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, Ks[(kb + f * 16 + (l & 15)) * "
+        << KSP << " + dim], sc[f], 0, 0, 0);\n  }\n";
+    } else {
+      std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
+      std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
+      s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 32 << "; ++kk) {\n";
+      s << "    const int dim = kk * 32 + (l >> 4) * 8;\n";
+      s << "    " << V8 << " qa;\n";
+      s << "    if (qv && dim + 8 <= " << a.d << ") qa = *(const " << V8 << "*)(" << Q << " + qoff + qr * " << a.d << " + dim);\n";
+      s << "    else {\n#pragma unroll\n      for (int j = 0; j < 8; ++j) qa[j] = (qv && dim + j < " << a.d << ") ? " << Q
+        << "[qoff + qr * " << a.d << " + dim + j] : fromf<" << T << ">(0.0f);\n    }\n";
+      s << "#pragma unroll\n    for (int f = 0; f < " << NFW << "; ++f) sc[f] = " << fn << "(qa, *(const " << V8
+        << "*)(Ks + (kb + f * 16 + (l & 15)) * " << KSP << " + dim), sc[f], 0, 0, 0);\n  }\n";
+    }
+    // rows (l>>4)*4 + i of the 16, key kb + f*16 + (l&15)
+    s << "  float mx[4], sm[4];\n";
+    s << "  float* red = (float*)(smem + " << red_off << ");  // [2][wave][16 rows]\n";
+    s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = -__builtin_huge_valf();\n";
+    s << "#pragma unroll\n  for (int f = 0; f < " << NFW << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
+    s << "    const float x = sc[f][i];\n    sc[f][i] = " << chain_expr << ";\n";
+    if (nkp != a.nk) s << "    if (kb + f * 16 + (l & 15) >= " << a.nk << ") sc[f][i] = -__builtin_huge_valf();\n";
+    s << "    mx[i] = k_max(mx[i], sc[f][i]);\n  }\n";
+    s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = group_max<16>(mx[i]);\n";
+    s << "  if ((l & 15) == 0) {\n#pragma unroll\n    for (int i = 0; i < 4; ++i) red[wave * 16 + (l >> 4) * 4 + i] = mx[i];\n  }\n";
+    s << "  __syncthreads();\n";
+    s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n    const int r = (l >> 4) * 4 + i;\n";
+    s << "    mx[i] = k_max(k_max(red[r], red[16 + r]), k_max(red[32 + r], red[48 + r]));\n    sm[i] = 0.0f;\n  }\n";
+    s << "#pragma unroll\n  for (int f = 0; f < " << NFW << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
+    s << "    sc[f][i] = " << unary_expr(KORCH_EXP, "(sc[f][i] - mx[i])") << ";\n    sm[i] += sc[f][i];\n  }\n";
+    s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = group_sum<16>(sm[i]);\n";
+    s << "  if ((l & 15) == 0) {\n#pragma unroll\n    for (int i = 0; i < 4; ++i) red[64 + wave * 16 + (l >> 4) * 4 + i] = sm[i];\n  }\n";
+    s << "  __syncthreads();\n";
+    s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n    const int r = 64 + (l >> 4) * 4 + i;\n";
+    s << "    sm[i] = ((red[r] + red[16 + r]) + red[32 + r]) + red[48 + r];\n  }\n";
+    s << "  " << T << "* Pw = Ps + wave * " << 16 * NKP << ";  // this wave's probabilities, keys local\n";
+    s << "#pragma unroll\n  for (int f = 0; f < " << NFW << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) Pw[((l >> 4) * 4 + i) * "
+      << NKP << " + f * 16 + (l & 15)] = fromf<" << T << ">(" << binary_expr(KORCH_DIV, "sc[f][i]", "sm[i]") << ");\n";
+    s << "  __syncthreads();\n";
+    s << "  f32x4 oc[" << OF << "];\n";
+    s << "#pragma unroll\n  for (int f = 0; f < " << OF << "; ++f) oc[f] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
+    if (f32) {
+      s << "#pragma unroll\n  for (int kk = 0; kk < " << NKW / 4 << "; ++kk) {\n";
+      s << "    const int key = kk * 4 + (l >> 4);\n";
+      s << "    const float pa = Pw[(l & 15) * " << NKP << " + key];\n";
+      s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, Vs[(kb + key) * " << VP
+        << " + f * 16 + (l & 15)], oc[f], 0, 0, 0);\n  }\n";
+    } else {
+      std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
+      std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
+      s << "#pragma unroll\n  for (int kk = 0; kk < " << NKW / 32 << "; ++kk) {\n";
+      s << "    const int key = kk * 32 + (l >> 4) * 8;\n";
+      s << "    const " << V8 << " pa = *(const " << V8 << "*)(Pw + (l & 15) * " << NKP << " + key);\n";
+      s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = " << fn << "(pa, *(const " << V8
+        << "*)(Vs + (f * 16 + (l & 15)) * " << NKP << " + kb + key), oc[f], 0, 0, 0);\n  }\n";
+    }
+    s << "  float* Op = (float*)(smem + " << op_off << ");  // [wave][16 rows][" << dvp << "]\n";
+    s << "#pragma unroll\n  for (int f = 0; f < " << OF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) Op[(wave * 16 + (l >> 4) * 4 + i) * "
+      << dvp << " + f * 16 + (l & 15)] = oc[f][i];\n";
+    s << "  __syncthreads();\n";
+    s << "  for (int t = tid; t < " << 16 * dvp << "; t += 256) {\n";
+    s << "    const int row = t / " << dvp << ", col = t % " << dvp << ";\n";
+    s << "    const float o_ = ((Op[t] + Op[" << 16 * dvp << " + t]) + Op[" << 32 * dvp << " + t]) + Op[" << 48 * dvp << " + t];\n";
+    s << "    if (q0 + row < " << a.nq << "LL && col < " << a.dv << ") st1(" << O << " + ooff + (q0 + row) * " << a.dv
+      << " + col, o_);\n  }\n";
+    s << "}\n";
+    gk.source = s.str();
+    gk.grid[0] = (int)((a.nq + 15) / 16);
+    gk.grid[1] = (int)a.batch;
+    gk.lds_bytes = (int)smem;
+    ki.fill_cost(gk);
+    return gk;
+  }
   // this wave's 16 query rows
   s << "  const i64 q0 = (i64)blockIdx.x * 64 + wave * 16;\n";
   s << "  const i64 qr = q0 + (l & 15);\n";
@@ -274,14 +378,6 @@ GenKernel gen_attention(const KInfo& ki, int index) {
       << "*)(Ks + (f * 16 + (l & 15)) * " << KSP << " + dim), sc[f], 0, 0, 0);\n  }\n";
   }
   // score chain, row max, exp, row sum, divide -- rows (l>>4)*4 + i, key f*16 + (l&15)
-  std::string chain_expr = "x";
-  for (int c : a.chain) {
-    const Node& cn = g.nodes[c];
-    if (op_kind(cn.op) == Kind::Unary)
-      chain_expr = unary_expr(cn.op, chain_expr);
-    else
-      chain_expr = binary_expr(cn.op, chain_expr, flit(cn.attrs.scalar));
-  }
   s << "  float mx[4], sm[4];\n";
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = -__builtin_huge_valf();\n";
   s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";

@@ -125,7 +125,7 @@ std::vector<char> rtc_compile(const std::string& src, const std::string& name) {
   }
   // hipRTC's in-process compiler keeps process-global state (LLVM's option
   // parsing among it) and is not safe to call from several threads at once;
-  // cache hits above stay concurrent, compilations take turns.
+  // callers that compile from several threads take turns here.
   static std::mutex compile_mutex;
   std::lock_guard<std::mutex> lock(compile_mutex);
   hiprtcProgram prog;

@@ -10,7 +10,9 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from ._abi import Plan, pointer_array
+import ctypes as C
+
+from ._abi import Plan, check, lib, pointer_array
 
 TORCH_DTYPE = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -70,6 +72,31 @@ class PlanRunner:
         s = stream if stream is not None else torch.cuda.current_stream()
         ins, outs = self._ptrs()
         self.plan.execute_kernels(first, count, ins, outs, self.ws.data_ptr(), self.ws_bytes, s.cuda_stream)
+
+    def bind(self, stream=None):
+        """Builds every C argument of one plan execution on ``stream`` (default:
+        the current stream) once, for ``launch_bound`` / ``launch_timed_bound``:
+        one library call per launch with no per-call conversions.  Bind again
+        after ``set_inputs``."""
+        s = stream if stream is not None else torch.cuda.current_stream()
+        ins, outs = self._ptrs()
+        self._bound = (self.plan.h, ins, outs, C.c_void_p(self.ws.data_ptr()), C.c_size_t(self.ws_bytes),
+                       C.c_void_p(s.cuda_stream))
+        self._nk = self.plan.num_kernels()
+        return self
+
+    def launch_bound(self):
+        rc = lib.korch_plan_execute(*self._bound)
+        if rc:
+            check(rc)
+
+    def launch_timed_bound(self, timed, start, stop):
+        """``launch_timed`` on the bound arguments (``start`` / ``stop``: torch events, each recorded once before)."""
+        h, ins, outs, ws, wsb, st = self._bound
+        rc = lib.korch_plan_execute_timed(h, 0, self._nk, ins, outs, ws, wsb, st, timed, C.c_void_p(start.cuda_event),
+                                          C.c_void_p(stop.cuda_event))
+        if rc:
+            check(rc)
 
     def launch_timed(self, timed, start, stop, stream=None):
         """One execution of the whole plan with kernel ``timed`` bracketed by the

@@ -47,6 +47,16 @@ GEMM_CASES = [
     dict(m=256, d=192, h=2048),
 ]
 
+# Attention shapes of the attention-kernel GPU tests (few query rows: the keys
+# are split over the waves; fp32 and fp16, padded keys), each run with the key
+# split and without it (KORCH_ATTN_NO_KEY_SPLIT=1).
+ATTN_CASES = [
+    ("attention", dict(n=50, d=16)),
+    ("attention", dict(n=128, d=64)),
+    ("sra", dict(hh=16, ww=32, c=32, r=2)),
+    ("sra", dict(hh=8, ww=56, c=16, r=2)),
+]
+
 # Workloads whose computed product operands get layout variants.
 LAYOUT_WORKLOADS = ("attention", "mlp", "sra", "linattn")
 
@@ -72,6 +82,9 @@ def _jobs():
     for sz in GEMM_CASES:
         for flag in ("", "1"):
             jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_NO_KSPLIT", flag)))
+    for wl, sz in ATTN_CASES:
+        for flag in ("", "1"):
+            jobs.append(("env_plans", wl, sz, ("KORCH_ATTN_NO_KEY_SPLIT", flag)))
     for w, sizes in CHOOSER.items():
         for sz in sizes:
             jobs.append(("candidates", w, sz, None))

@@ -343,3 +343,31 @@ def test_gemm_k_split_selection():
         assert "kgrp" not in src[2] and launch[2][1][0] == 256, sz
     src, _ = sources({}, "")
     assert "kgrp" not in src[1]
+
+
+def test_attention_key_split_selection():
+    """Few query rows split the keys over the waves (one workgroup per 16 rows);
+    the SRA workload's 16384 queries keep one workgroup per 64 rows."""
+    from paper_2406_09465_amd.warm import ATTN_CASES
+
+    def launch_and_src(workload, sizes):
+        p = graphs.build(workload, **sizes).plan("fused")
+        p.compile()
+        k = [i for i in range(p.num_kernels()) if "attention" in p.kernel_name(i)][0]
+        return p.kernel_launch(k), p.kernel_source(k)
+
+    prev = os.environ.pop("KORCH_ATTN_NO_KEY_SPLIT", None)
+    try:
+        for wl, sz in ATTN_CASES:
+            (grid, _, _), src = launch_and_src(wl, sz)
+            nq = sz["n"] if wl == "attention" else sz["hh"] * sz["ww"]
+            assert "this wave's keys" in src and grid[0] == (nq + 15) // 16, (wl, sz)
+        (grid, _, _), src = launch_and_src("sra", {})
+        assert "this wave's keys" not in src and grid[0] == 16384 // 64
+        os.environ["KORCH_ATTN_NO_KEY_SPLIT"] = "1"
+        (grid, _, _), src = launch_and_src("attention", {})
+        assert "this wave's keys" not in src and grid[0] == 2
+    finally:
+        os.environ.pop("KORCH_ATTN_NO_KEY_SPLIT", None)
+        if prev is not None:
+            os.environ["KORCH_ATTN_NO_KEY_SPLIT"] = prev

@@ -90,3 +90,15 @@ def test_timed_execution_matches_plain_execution():
         torch.cuda.synchronize()
         assert all(torch.equal(x, y) for x, y in zip(ref, r.outs))
         assert a.elapsed_time(b) > 0.0
+        # the same through the pre-bound arguments
+        for t in r.outs:
+            t.zero_()
+        r.bind()
+        r.launch_timed_bound(k, a, b)
+        torch.cuda.synchronize()
+        assert all(torch.equal(x, y) for x, y in zip(ref, r.outs))
+        for t in r.outs:
+            t.zero_()
+        r.launch_bound()
+        torch.cuda.synchronize()
+        assert all(torch.equal(x, y) for x, y in zip(ref, r.outs))
