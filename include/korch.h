@@ -201,6 +201,13 @@ int korch_enumerate_candidates(const korch_graph* g, int32_t max_prims, int32_t 
                                int (*cb)(const korch_kernel_desc* k, void* user), void* user);
 /* Which family implements kernel k (KORCH_FAM_NONE = unsupported, cost infinity). */
 int korch_kernel_family(const korch_graph* g, const korch_kernel_desc* k, int32_t* family);
+/* The HIP source a plan of g would generate for kernel k (Section 5.2's
+   kernel generation, within the whole graph: its external tensors are those
+   of g), for inspection.  Needs no GPU and compiles nothing.  *len receives
+   the source length; at most cap - 1 bytes and a terminating 0 are written to
+   buf (may be NULL when cap is 0).  KORCH_E_UNSUPPORTED when no family
+   implements k. */
+int korch_kernel_source(const korch_graph* g, const korch_kernel_desc* k, char* buf, size_t cap, size_t* len);
 
 /* ---- plans -------------------------------------------------------------- */
 /* Validates an ordered plan (rules of Definitions 1 and 3 and the output and

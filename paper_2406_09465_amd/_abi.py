@@ -17,6 +17,9 @@ LIB_PATH = os.path.join(PKG, "libkorch.so")
 # caller chose another directory.
 os.environ.setdefault("KORCH_CACHE_DIR", os.path.join(PKG, "_kcache"))
 
+# KORCH_LIB loads another build of the library instead (e.g. one built with a
+# host-code sanitizer).
+LIB_PATH = os.environ.get("KORCH_LIB") or LIB_PATH
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2406_09465_amd.build`")
 # A process must hold one HIP runtime.  PyTorch ships its own copy; loading it
@@ -103,6 +106,7 @@ _SIGS = {
     "korch_plan_workspace_bytes": ([_P, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute": ([_P, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
     "korch_plan_execute_kernels": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
+    "korch_kernel_source": ([_P, _P, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute_timed": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P, _I, _P, _P], C.c_int),
     "korch_plan_kernel_info": ([_P, _I, C.POINTER(_I), C.POINTER(C.c_double), C.POINTER(C.c_double)], C.c_int),
     "korch_plan_kernel_source": ([_P, _I, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
@@ -293,6 +297,15 @@ class Graph:
         fam = _I()
         check(lib.korch_kernel_family(self.h, C.byref(d), C.byref(fam)))
         return FAMILIES[fam.value]
+
+    def kernel_source(self, prims, outs):
+        """HIP source generated for kernel (prims, outs) within this graph."""
+        d, keep = kernel_desc(prims, outs)
+        n = C.c_size_t()
+        check(lib.korch_kernel_source(self.h, C.byref(d), None, 0, C.byref(n)))
+        buf = C.create_string_buffer(n.value + 1)
+        check(lib.korch_kernel_source(self.h, C.byref(d), buf, n.value + 1, None))
+        return buf.value.decode()
 
     def compile_candidate(self, prims, outs):
         """Compiles the single kernel (prims, outs) as the profiler will; False when unsupported."""

@@ -2,6 +2,7 @@
 
 Host C++ sources are compiled with g++ against the HIP runtime headers, the
 HIP source with hipcc for gfx950, and everything is linked with hipcc.  The
+runtime compiler helper `korch_rtc` (csrc/tools) is built next to the library.  The
 device prelude that generated kernels include at run time is embedded into
 the library as a string.
 
@@ -20,6 +21,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libkorch.so")
+RTC_HELPER = os.path.join(PKG, "korch_rtc")  # runtime compiler, run by the library as a child process
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
@@ -73,6 +75,10 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, f"-L{ROCM}/lib", "-ldl",
           f"-Wl,-rpath,{ROCM}/lib", "-o", tmp])
     os.replace(tmp, LIB)
+    tmp = RTC_HELPER + ".tmp"
+    _run(["g++", "-O2", "-std=c++17", "-Wall", "-D__HIP_PLATFORM_AMD__", f"-I{ROCM}/include",
+          os.path.join(CSRC, "tools", "korch_rtc.cpp"), "-ldl", "-o", tmp])
+    os.replace(tmp, RTC_HELPER)
     return LIB
 
 

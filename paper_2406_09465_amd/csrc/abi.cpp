@@ -448,6 +448,27 @@ int korch_plan_kernel_info(const korch_plan* p, int32_t k, int32_t* family, doub
   });
 }
 
+int korch_kernel_source(const korch_graph* g, const korch_kernel_desc* k, char* buf, size_t cap, size_t* len) {
+  return guard([&] {
+    NEED(g);
+    NEED(k);
+    if (!g->g.finalized) fail(KORCH_E_STATE, "graph is not finalized");
+    KernelDesc d = to_desc(*k);
+    if (d.prims.empty() || d.outs.empty()) fail(KORCH_E_ARG, "empty kernel");
+    for (int v : d.prims)
+      if (v < 0 || v >= (int)g->g.nodes.size() || !g->g.is_prim(v)) fail(KORCH_E_ARG, "bad primitive id");
+    for (int v : d.outs)
+      if (std::find(d.prims.begin(), d.prims.end(), v) == d.prims.end()) fail(KORCH_E_ARG, "output outside the kernel");
+    std::string s = generate_kernel(g->g, d, 0).source;
+    if (len) *len = s.size();
+    if (buf && cap) {
+      size_t n = std::min(cap - 1, s.size());
+      memcpy(buf, s.data(), n);
+      buf[n] = 0;
+    }
+  });
+}
+
 int korch_plan_kernel_source(const korch_plan* p, int32_t k, char* buf, size_t cap, size_t* len) {
   return guard([&] {
     NEED(p);

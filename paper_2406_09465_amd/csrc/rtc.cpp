@@ -2,19 +2,23 @@
 // on-disk cache of code objects keyed by a hash of source, options and the
 // compiler library.
 //
-// hipRTC is loaded from the ROCm installation ($ROCM_PATH, default /opt/rocm)
-// into a link-map namespace of its own.  hipRTC finds its compiler (comgr) by
-// soname at run time; in the process's main namespace that lookup would pick
-// whichever comgr another library (e.g. a framework's bundled ROCm) loaded
-// first, so the generated code would depend on import order.
+// A code object missing from the cache is compiled by the helper executable
+// `korch_rtc` (built next to this library) in a child process: hipRTC's
+// in-process compiler keeps process-global state and brings its own copy of
+// the compiler libraries, and running it inside a process that also drives
+// the GPU (and whose framework may have loaded another compiler library) is
+// avoided altogether.  The helper loads hipRTC from the ROCm installation
+// ($ROCM_PATH, default /opt/rocm).
 #include <dlfcn.h>
-#include <hip/hiprtc.h>
 #include <limits.h>
+#include <spawn.h>
 #include <sys/stat.h>
+#include <sys/wait.h>
 #include <unistd.h>
 #include <utime.h>
 
 #include <atomic>
+#include <cerrno>
 #include <cstdio>
 #include <cstdlib>
 #include <fstream>
@@ -23,6 +27,8 @@
 
 #include "ir.h"
 
+extern char** environ;
+
 namespace korch {
 
 static const char* kOptions[] = {"--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
@@ -30,49 +36,40 @@ static const char* kOptions[] = {"--offload-arch=gfx950", "-O3", "-std=c++17", "
 
 namespace {
 
-struct Rtc {
-  std::string path;  // resolved file of the loaded hipRTC
-  hiprtcResult (*create)(hiprtcProgram*, const char*, const char*, int, const char**, const char**) = nullptr;
-  hiprtcResult (*compile)(hiprtcProgram, int, const char**) = nullptr;
-  hiprtcResult (*log_size)(hiprtcProgram, size_t*) = nullptr;
-  hiprtcResult (*log)(hiprtcProgram, char*) = nullptr;
-  hiprtcResult (*code_size)(hiprtcProgram, size_t*) = nullptr;
-  hiprtcResult (*code)(hiprtcProgram, char*) = nullptr;
-  hiprtcResult (*destroy)(hiprtcProgram*) = nullptr;
-  std::string error;
-};
-
-template <class F>
-bool sym(void* h, const char* name, F& f, std::string& err) {
-  f = reinterpret_cast<F>(dlsym(h, name));
-  if (!f) err = std::string("hipRTC lacks ") + name;
-  return f != nullptr;
-}
-
-const Rtc& rtc() {
-  static Rtc r = [] {
-    Rtc x;
+// The hipRTC library the helper loads (its resolved path is part of the cache key).
+const std::string& hiprtc_path() {
+  static const std::string p = [] {
     const char* root = getenv("ROCM_PATH");
     std::string file = std::string(root && *root ? root : "/opt/rocm") + "/lib/libhiprtc.so.7";
-    void* h = dlmopen(LM_ID_NEWLM, file.c_str(), RTLD_NOW | RTLD_LOCAL);
-    if (!h) {
-      const char* e = dlerror();
-      x.error = "cannot load " + file + ": " + (e ? e : "unknown error");
-      return x;
-    }
     char real[PATH_MAX];
-    x.path = realpath(file.c_str(), real) ? real : file;
-    std::string& err = x.error;
-    sym(h, "hiprtcCreateProgram", x.create, err) && sym(h, "hiprtcCompileProgram", x.compile, err) &&
-        sym(h, "hiprtcGetProgramLogSize", x.log_size, err) && sym(h, "hiprtcGetProgramLog", x.log, err) &&
-        sym(h, "hiprtcGetCodeSize", x.code_size, err) && sym(h, "hiprtcGetCode", x.code, err) &&
-        sym(h, "hiprtcDestroyProgram", x.destroy, err);
-    return x;
+    return std::string(realpath(file.c_str(), real) ? real : file.c_str());
   }();
-  return r;
+  return p;
+}
+
+// The helper executable: korch_rtc in the directory of this library.
+const std::string& helper_path() {
+  static const std::string p = [] {
+    Dl_info info;
+    std::string dir = ".";
+    if (dladdr((void*)&hiprtc_path, &info) && info.dli_fname) {
+      std::string f = info.dli_fname;
+      size_t slash = f.rfind('/');
+      if (slash != std::string::npos) dir = f.substr(0, slash);
+    }
+    return dir + "/korch_rtc";
+  }();
+  return p;
 }
 
 std::atomic<unsigned> tmp_counter{0};
+
+std::string read_file(const std::string& path) {
+  std::ifstream f(path, std::ios::binary);
+  std::stringstream ss;
+  ss << f.rdbuf();
+  return ss.str();
+}
 
 }  // namespace
 
@@ -106,9 +103,7 @@ static void mkdirs(const std::string& path) {
 std::vector<char> rtc_compile(const std::string& src, const std::string& name) {
   std::string opts;
   for (auto o : kOptions) opts += std::string(o) + " ";
-  const Rtc& R = rtc();
-  if (!R.error.empty()) fail(KORCH_E_COMPILE, R.error);
-  uint64_t h = fnv1a(src, fnv1a(opts + R.path + name));
+  uint64_t h = fnv1a(src, fnv1a(opts + hiprtc_path() + name));
   char hex[32];
   snprintf(hex, sizeof(hex), "%016llx", (unsigned long long)h);
   std::string dir = cache_dir();
@@ -123,36 +118,42 @@ std::vector<char> rtc_compile(const std::string& src, const std::string& name) {
       }
     }
   }
-  // hipRTC's in-process compiler keeps process-global state (LLVM's option
-  // parsing among it) and is not safe to call from several threads at once;
-  // callers that compile from several threads take turns here.
-  static std::mutex compile_mutex;
-  std::lock_guard<std::mutex> lock(compile_mutex);
-  hiprtcProgram prog;
-  if (R.create(&prog, src.c_str(), (name + ".hip").c_str(), 0, nullptr, nullptr) != HIPRTC_SUCCESS)
-    fail(KORCH_E_COMPILE, "hiprtcCreateProgram failed for " + name);
-  hiprtcResult r = R.compile(prog, (int)(sizeof(kOptions) / sizeof(kOptions[0])), kOptions);
-  if (r != HIPRTC_SUCCESS) {
-    size_t ls = 0;
-    R.log_size(prog, &ls);
-    std::string log(ls, '\0');
-    if (ls) R.log(prog, &log[0]);
-    R.destroy(&prog);
-    if (log.size() > 4000) log = log.substr(0, 4000);
-    fail(KORCH_E_COMPILE, "hipRTC failed for " + name + ": " + log);
-  }
-  size_t cs = 0;
-  R.code_size(prog, &cs);
-  std::vector<char> code(cs);
-  R.code(prog, code.data());
-  R.destroy(&prog);
   mkdirs(dir);
-  std::string tmp = path + ".tmp" + std::to_string(getpid()) + "." + std::to_string(tmp_counter++);
+  const std::string tmp = path + ".tmp" + std::to_string(getpid()) + "." + std::to_string(tmp_counter++);
+  const std::string src_file = tmp + ".hip", obj_file = tmp + ".co", log_file = tmp + ".log";
   {
-    std::ofstream f(tmp, std::ios::binary);
-    f.write(code.data(), (std::streamsize)code.size());
+    std::ofstream f(src_file, std::ios::binary);
+    f.write(src.data(), (std::streamsize)src.size());
+    if (!f) fail(KORCH_E_COMPILE, "cannot write " + src_file);
   }
-  rename(tmp.c_str(), path.c_str());
+  std::vector<std::string> args = {helper_path(), src_file, name, obj_file, log_file};
+  for (auto o : kOptions) args.push_back(o);
+  std::vector<char*> argv;
+  for (auto& a : args) argv.push_back(&a[0]);
+  argv.push_back(nullptr);
+  pid_t pid;
+  int rc = posix_spawn(&pid, helper_path().c_str(), nullptr, nullptr, argv.data(), environ);
+  int status = 0;
+  if (rc == 0) {
+    while (waitpid(pid, &status, 0) < 0 && errno == EINTR) {
+    }
+  }
+  std::string log = read_file(log_file);
+  std::vector<char> code;
+  if (rc == 0 && WIFEXITED(status) && WEXITSTATUS(status) == 0) {
+    std::string obj = read_file(obj_file);
+    code.assign(obj.begin(), obj.end());
+  }
+  unlink(src_file.c_str());
+  unlink(log_file.c_str());
+  if (code.empty()) {
+    unlink(obj_file.c_str());
+    if (rc != 0) fail(KORCH_E_COMPILE, "cannot run " + helper_path() + " (build the library)");
+    if (log.size() > 4000) log = log.substr(0, 4000);
+    fail(KORCH_E_COMPILE, "hipRTC failed for " + name + ": " +
+                              (log.empty() ? "helper exited with status " + std::to_string(status) : log));
+  }
+  rename(obj_file.c_str(), path.c_str());
   return code;
 }
 

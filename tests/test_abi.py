@@ -371,3 +371,22 @@ def test_attention_key_split_selection():
         os.environ.pop("KORCH_ATTN_NO_KEY_SPLIT", None)
         if prev is not None:
             os.environ["KORCH_ATTN_NO_KEY_SPLIT"] = prev
+
+
+def test_runtime_compiler_helper(tmp_path):
+    """The helper that compiles cache misses in a child process: a code object
+    for a valid kernel, exit status 1 and the compiler's log for a broken one."""
+    import subprocess
+    helper = os.path.join(os.path.dirname(K.LIB_PATH), "korch_rtc")
+    opts = ["--offload-arch=gfx950", "-O3", "-std=c++17"]
+    good = tmp_path / "good.hip"
+    good.write_text('extern "C" __global__ void k(float* p) { p[threadIdx.x] += 1.0f; }\n')
+    r = subprocess.run([helper, str(good), "k", str(tmp_path / "good.co"), str(tmp_path / "good.log"), *opts],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert (tmp_path / "good.co").read_bytes()[:4] in (b"\x7fELF", b"__CL")
+    bad = tmp_path / "bad.hip"
+    bad.write_text('extern "C" __global__ void k(float* p) { p[threadIdx.x] += undeclared_name; }\n')
+    r = subprocess.run([helper, str(bad), "k", str(tmp_path / "bad.co"), str(tmp_path / "bad.log"), *opts],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 1 and "undeclared_name" in (tmp_path / "bad.log").read_text()
