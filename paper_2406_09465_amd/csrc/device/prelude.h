@@ -122,6 +122,19 @@ __device__ __forceinline__ float f_mish(float x) {
   return x * f_div(n, n + 2.0f);
 }
 
+// ---- fp32 partial results handed from workgroup to workgroup --------------
+// Device-scope (agent) atomic stores and loads are performed at the point of
+// coherence of the whole device, so a value one workgroup stores this way is
+// read by a workgroup on another XCD without an L2 write-back on the writer's
+// side or an L2 invalidate on the reader's (the device-scope release and
+// acquire fences would do both for the whole L2).
+__device__ __forceinline__ void coherent_store(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float coherent_load(float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---- reductions across a group of G lanes of a wavefront (G power of two <= 64)
 template <int G> __device__ __forceinline__ float group_sum(float v) {
 #pragma unroll

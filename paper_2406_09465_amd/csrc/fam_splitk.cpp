@@ -302,29 +302,31 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "  const i64 tix = bz * " << mtiles << " + mt;\n";
   s << "  float* part = (float*)a.p[" << scr_slot << "];\n";
   s << "  float* sidep = part + " << base * S * tile << "LL;\n";
-  s << "  for (int i = tid; i < " << tile << "; i += 256) part[(tix * " << S << " + split) * " << tile
-    << "LL + i] = Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "];\n";
-  if (nside) s << "  if (tid < " << sp.BM << ") sidep[(tix * " << S << " + split) * " << sp.BM << " + tid] = side_acc;\n";
-  // Every wave's partial stores precede the barrier; the counter increment by
-  // thread 0 is a device-scope release that publishes the workgroup's
-  // partials, and only the last workgroup performs the device-scope acquire
-  // (each is an L2 write-back or invalidate on this multi-XCD device, so no
-  // other fence is issued).  The reset of the counter is ordered before its
-  // next use by the end of the kernel.
+  s << "  for (int i = tid; i < " << tile << "; i += 256) coherent_store(&part[(tix * " << S << " + split) * " << tile
+    << "LL + i], Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "]);\n";
+  if (nside)
+    s << "  if (tid < " << sp.BM << ") coherent_store(&sidep[(tix * " << S << " + split) * " << sp.BM << " + tid], side_acc);\n";
+  // The partials are stored at the device's point of coherence; every wave
+  // waits for its stores to complete (a workgroup barrier alone does not wait
+  // for global stores), and only after the barrier does thread 0 count the
+  // workgroup in.  The last workgroup to arrive reads all partials the same
+  // coherent way, so no cache write-back or invalidate is needed.  The counter
+  // is reset by the last workgroup for the next launch (ordered before it by
+  // the end of the kernel).
+  s << "  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are performed\n";
   s << "  __syncthreads();\n";
   s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
-  s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);\n";
+  s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
   s << "    last_ = (old == " << S - 1 << ");\n";
-  s << "    if (last_) {\n      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, \"agent\");\n"
-    << "      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n    }\n  }\n";
+  s << "    if (last_) __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
   s << "  __syncthreads();\n  if (!last_) return;\n";
   // deterministic sum of the partials, split 0 first
   s << "  for (int i = tid; i < " << tile << "; i += 256) {\n    float acc_ = 0.0f;\n";
-  s << "    for (int p = 0; p < " << S << "; ++p) acc_ += part[(tix * " << S << " + p) * " << tile << "LL + i];\n";
+  s << "    for (int p = 0; p < " << S << "; ++p) acc_ += coherent_load(&part[(tix * " << S << " + p) * " << tile << "LL + i]);\n";
   s << "    Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "] = acc_;\n  }\n";
   if (nside) {
     s << "  if (tid < " << sp.BM << ") {\n    float acc_ = 0.0f;\n";
-    s << "    for (int p = 0; p < " << S << "; ++p) acc_ += sidep[(tix * " << S << " + p) * " << sp.BM << " + tid];\n";
+    s << "    for (int p = 0; p < " << S << "; ++p) acc_ += coherent_load(&sidep[(tix * " << S << " + p) * " << sp.BM << " + tid]);\n";
     s << "    side_s[tid] = acc_;\n  }\n";
   }
   s << "  __syncthreads();\n";

@@ -641,16 +641,18 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     << ";\n    }\n  }\n";
   if (SPLIT > 1) {
     s << "  float* part = (float*)a.p[" << scr_slot << "];\n";
-    s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) part[(ay * " << SPLIT
-      << " + blockIdx.z) * " << B << "LL + bi + e] = s[e];\n  }\n";
+    s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) coherent_store(&part[(ay * " << SPLIT
+      << " + blockIdx.z) * " << B << "LL + bi + e], s[e]);\n  }\n";
+    // partials stored and read at the device's point of coherence; each wave
+    // waits for its stores to complete before the barrier, after which thread
+    // 0 counts the workgroup in
+    s << "  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are performed\n";
     s << "  __syncthreads();\n";
     s << "  const i64 tix = ay * " << ctiles << " + blockIdx.x;\n";
-    // release by thread 0 with the increment; acquire only in the last workgroup
     s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
-    s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);\n";
+    s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
     s << "    last_ = (old == " << SPLIT - 1 << ");\n";
-    s << "    if (last_) {\n      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, \"agent\");\n"
-      << "      __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n    }\n  }\n";
+    s << "    if (last_) __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
     s << "  __syncthreads();\n  if (!last_) return;\n";
     // every thread of the last workgroup sums a group of splits for one column
     // of the tile; the groups are then combined in order (deterministic)
@@ -661,7 +663,7 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     s << "      const int g = " << (G > 1 ? "tid / " + std::to_string(TC) : std::string("0")) << ";\n";
     s << "      float t_ = " << ident << ";\n";
     s << "      if (cb + c < " << B << "LL)\n#pragma unroll 4\n        for (int z = g; z < " << SPLIT << "; z += " << G
-      << ") t_ = " << comb("t_", "part[(ay * " + std::to_string(SPLIT) + " + z) * " + std::to_string(B) + "LL + cb + c]")
+      << ") t_ = " << comb("t_", "coherent_load(&part[(ay * " + std::to_string(SPLIT) + " + z) * " + std::to_string(B) + "LL + cb + c])")
       << ";\n";
     s << "      red[g * " << TC << " + c] = t_;\n    }\n  }\n  __syncthreads();\n";
     s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n";
