@@ -96,7 +96,11 @@ struct Emitter {
   std::function<bool(int, const std::vector<Ix>&, std::string*)> provide;
   bool force_gather = false;           // all loads per-lane (guarded contexts)
   int tmp = 0;
-  int guard_depth = 0;
+  int guard_depth = 0;                 // enclosing guards whose condition varies with the vector lane
+  // Enclosing guards whose condition is the same for every lane of a vector
+  // (e.g. a spatial pad around a channel vector): loads under them are still
+  // hoisted as uniform / vector loads, each executed only when the guards hold.
+  std::vector<std::string> lane_invariant_guards;
   int n_gather = 0, n_vector = 0, n_uniform = 0;
   std::vector<std::map<std::string, std::string>> memo{1};
   // Staged loads: a hoisted (uniform or vector) load becomes an assignment into

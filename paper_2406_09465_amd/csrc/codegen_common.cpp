@@ -324,7 +324,9 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
   std::string T = ctype(n.dtype);
   std::string P = "((const " + T + "*)a.p[" + std::to_string(it->second) + "])";
   bool hoist = guard_depth == 0 && !force_gather;
-  if (staged && hoist && off.affine && (off.c == 0 || (off.c == 1 && vec > 1 && off.al % vec == 0))) {
+  std::string gcond;  // conjunction of the enclosing lane-invariant guards
+  for (const std::string& c : lane_invariant_guards) gcond += (gcond.empty() ? "" : " && ") + c;
+  if (staged && hoist && gcond.empty() && off.affine && (off.c == 0 || (off.c == 1 && vec > 1 && off.al % vec == 0))) {
     bool shared = !slot_var.empty() && !uses_var(off.b, slot_var);
     std::string v = fresh(off.c == 0 ? "su" : "sx");
     std::string ty = off.c == 0 ? T : "vec_t<" + std::to_string(vec) + ", " + T + ">";
@@ -343,13 +345,20 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
   if (hoist && off.affine && off.c == 0) {
     ++n_uniform;
     std::string v = fresh("u");
-    pre << "  const float " << v << " = ld1(" << P << " + " << off.b << ");\n";
+    if (gcond.empty())
+      pre << "  const float " << v << " = ld1(" << P << " + " << off.b << ");\n";
+    else
+      pre << "  const float " << v << " = (" << gcond << ") ? ld1(" << P << " + " << off.b << ") : 0.0f;\n";
     return v;
   }
   if (hoist && off.affine && off.c == 1 && vec > 1 && off.al % vec == 0) {
     ++n_vector;
     std::string v = fresh("x");
-    pre << "  float " << v << "[" << vec << "]; ldv<" << vec << ">(" << v << ", " << P << " + " << off.b << ");\n";
+    if (gcond.empty())
+      pre << "  float " << v << "[" << vec << "]; ldv<" << vec << ">(" << v << ", " << P << " + " << off.b << ");\n";
+    else
+      pre << "  float " << v << "[" << vec << "] = {}; if (" << gcond << ") ldv<" << vec << ">(" << v << ", " << P << " + "
+          << off.b << ");\n";
     return v + "[e]";
   }
   ++n_gather;
@@ -434,16 +443,27 @@ std::string Emitter::value(int node, const std::vector<Ix>& idx) {
                     std::to_string(n.attrs.begin[d] + s[d]) + ")";
           }
         }
+        // the condition is the same for every lane of a vector when no padded
+        // dimension's index moves with the lane
+        bool lane_invariant = true;
+        for (size_t d = 0; d < idx.size(); ++d)
+          if ((n.attrs.begin[d] > 0 || n.attrs.end[d] > 0) && (!idx[d].affine || idx[d].c != 0)) lane_invariant = false;
         if (cond.empty()) {
           out = value(n.in[0], src);
         } else {
           out = fresh("p");
           body << "    float " << out << " = " << flit(n.attrs.pad_value) << ";\n    if (" << cond << ") {\n";
           memo.emplace_back();
-          ++guard_depth;
+          if (lane_invariant)
+            lane_invariant_guards.push_back("(" + cond + ")");
+          else
+            ++guard_depth;
           std::string x = value(n.in[0], src);
           body << "    " << out << " = " << x << ";\n    }\n";
-          --guard_depth;
+          if (lane_invariant)
+            lane_invariant_guards.pop_back();
+          else
+            --guard_depth;
           memo.pop_back();
         }
       } else if (n.op == KORCH_CONCAT) {
