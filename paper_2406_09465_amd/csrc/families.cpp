@@ -580,7 +580,9 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     return true;
   };
   // prologue outputs (same shape as the reduced operand) are stored in the loop
+  // (one vector store of the VB consecutive elements when they are contiguous)
   std::set<int> pro_out;
+  std::ostringstream pdecl, pafter;
   for (int o : ki.k.outs)
     if (o != r && ki.ancestor(o, r)) {
       pro_out.insert(o);
@@ -588,8 +590,16 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
       auto strd = strides_of(S);
       Ix off = Ix::k(0);
       for (int d = 0; d < R; ++d) off = ix_add(off, ix_mulk(xi[d], strd[d], VB));
-      pe.body << "      if (bv) st1((" << ctype(g.nodes[o].dtype) << "*)a.p[" << ki.out_slot(o) << "] + " << off.at()
-              << ", " << v << ");\n";
+      const std::string T = ctype(g.nodes[o].dtype);
+      if (VB > 1 && off.affine && off.c == 1 && off.al % VB == 0) {
+        std::string arr = "_po" + std::to_string(o);
+        pdecl << "    float " << arr << "[" << VB << "];\n";
+        pe.body << "      " << arr << "[e] = " << v << ";\n";
+        pafter << "    if (bv) stv<" << VB << ">((" << T << "*)a.p[" << ki.out_slot(o) << "] + " << off.b << ", " << arr
+               << ");\n";
+      } else {
+        pe.body << "      if (bv) st1((" << T << "*)a.p[" << ki.out_slot(o) << "] + " << off.at() << ", " << v << ");\n";
+      }
     }
   for (int o : ki.k.outs) {
     if (pro_out.count(o)) continue;
@@ -631,14 +641,24 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
   s << "  const i64 l0 = (i64)blockIdx.z * " << chunk << ", l1 = l0 + " << chunk << " < " << Lr << "LL ? l0 + " << chunk
     << " : " << Lr << "LL;\n";
   s << "  float acc[" << VB << "];\n#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) acc[e] = " << ident << ";\n";
-  s << "#pragma unroll 4\n  for (i64 l = l0 + ly; l < l1; l += " << LY << ") {\n" << pe.pre.str() << "#pragma unroll\n    for (int e = 0; e < "
-    << VB << "; ++e) {\n" << pe.body.str() << "      acc[e] = " << comb("acc[e]", xv) << ";\n    }\n  }\n";
-  s << "#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) red[e * 256 + tid] = acc[e];\n  __syncthreads();\n";
-  // fixed-order combine of the LY rows of this workgroup: s[e] for column bi + e
+  s << "#pragma unroll 4\n  for (i64 l = l0 + ly; l < l1; l += " << LY << ") {\n" << pe.pre.str() << pdecl.str()
+    << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n" << pe.body.str() << "      acc[e] = "
+    << comb("acc[e]", xv) << ";\n    }\n" << pafter.str() << "  }\n";
+  // combine the LY rows of this workgroup in a fixed order: first the rows of
+  // each wave (lanes bl, bl + BB, ... exchanged pairwise), then the four wave
+  // results through LDS; s[e] is the result for column bi + e
+  s << "  const int wv_ = tid >> 6, lane_ = tid & 63;\n";
+  if (BB < 64) {
+    s << "#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) {\n";
+    s << "#pragma unroll\n    for (int m = " << BB << "; m < 64; m <<= 1) acc[e] = " << comb("acc[e]", "__shfl_xor(acc[e], m, 64)")
+      << ";\n  }\n";
+  }
+  s << "  if (lane_ < " << BB << ") {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) red[(wv_ * " << VB << " + e) * "
+    << BB << " + lane_] = acc[e];\n  }\n  __syncthreads();\n";
   s << "  float s[" << VB << "];\n";
-  s << "  if (ly == 0) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n      s[e] = red[e * 256 + bl];\n"
-    << "      for (int y = 1; y < " << LY << "; ++y) s[e] = " << comb("s[e]", "red[e * 256 + y * " + std::to_string(BB) + " + bl]")
-    << ";\n    }\n  }\n";
+  s << "  if (ly == 0) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n      s[e] = red[e * " << BB
+    << " + bl];\n#pragma unroll\n      for (int w = 1; w < 4; ++w) s[e] = "
+    << comb("s[e]", "red[(w * " + std::to_string(VB) + " + e) * " + std::to_string(BB) + " + bl]") << ";\n    }\n  }\n";
   if (SPLIT > 1) {
     s << "  float* part = (float*)a.p[" << scr_slot << "];\n";
     s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) coherent_store(&part[(ay * " << SPLIT
@@ -662,9 +682,15 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     s << "    for (int c = tid % " << std::min(TC, 256) << "; c < " << TC << "; c += 256) {\n";
     s << "      const int g = " << (G > 1 ? "tid / " + std::to_string(TC) : std::string("0")) << ";\n";
     s << "      float t_ = " << ident << ";\n";
-    s << "      if (cb + c < " << B << "LL)\n#pragma unroll 4\n        for (int z = g; z < " << SPLIT << "; z += " << G
-      << ") t_ = " << comb("t_", "coherent_load(&part[(ay * " + std::to_string(SPLIT) + " + z) * " + std::to_string(B) + "LL + cb + c])")
-      << ";\n";
+    // the loads of a batch are all issued before the first is combined (one
+    // round trip to the point of coherence per batch of up to 32 splits)
+    const int64_t NZ = (SPLIT + G - 1) / G, NBT = std::min<int64_t>(NZ, 32);
+    s << "      if (cb + c < " << B << "LL)\n        for (int z0 = g; z0 < " << SPLIT << "; z0 += " << NBT * G << ") {\n";
+    s << "          float v_[" << NBT << "];\n#pragma unroll\n          for (int j = 0; j < " << NBT << "; ++j) {\n";
+    s << "            const int z = z0 + j * " << G << ";\n";
+    s << "            v_[j] = z < " << SPLIT << " ? coherent_load(&part[(ay * " << SPLIT << " + z) * " << B
+      << "LL + cb + c]) : " << ident << ";\n          }\n";
+    s << "#pragma unroll\n          for (int j = 0; j < " << NBT << "; ++j) t_ = " << comb("t_", "v_[j]") << ";\n        }\n";
     s << "      red[g * " << TC << " + c] = t_;\n    }\n  }\n  __syncthreads();\n";
     s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n";
     s << "      s[e] = red[bl * " << VB << " + e];\n";
