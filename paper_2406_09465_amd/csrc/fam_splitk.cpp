@@ -278,9 +278,16 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   gk.args.push_back(cnt);
   std::string T = ctype(sp.mtype);
   std::ostringstream hook;
+  // Side sums: every thread adds a fixed segment of one row of each staged A
+  // tile (rows over tid % BM, segments over tid / BM); the segments of a row
+  // are combined in segment order once the loop is done.
+  const int NSEG = sp.BM <= 256 && 256 % sp.BM == 0 && sp.BK % (256 / sp.BM) == 0 ? 256 / sp.BM : 1;
+  const int KPS = sp.BK / NSEG;
   if (nside) {
-    hook << "      if (tid < " << sp.BM << ") {\n        float t_ = 0.0f;\n";
-    hook << "        for (int k = 0; k < " << sp.BK << "; ++k) t_ += tof(Ab[tid * " << sp.BKP << " + k]);\n";
+    hook << "      if (tid < " << sp.BM * NSEG << ") {\n        float t_ = 0.0f;\n";
+    hook << "        const " << ctype(sp.mtype) << "* Ar = Ab + (tid % " << sp.BM << ") * " << sp.BKP << " + (tid / " << sp.BM
+         << ") * " << KPS << ";\n";
+    hook << "#pragma unroll\n        for (int k = 0; k < " << KPS << "; ++k) t_ += tof(Ar[k]);\n";
     hook << "        side_acc += t_;\n      }\n";
   }
   size_t smem = gemm_smem_bytes(sp);
@@ -298,6 +305,12 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << operand_loader(ki, sp, true, slot);
   s << operand_loader(ki, sp, false, slot);
   s << mfma_mainloop(sp, hook.str(), ktper <= 128 ? ktper : 0, exact);
+  if (nside && NSEG > 1) {
+    s << "  __shared__ float side_r[" << sp.BM * NSEG << "];\n";
+    s << "  side_r[tid] = side_acc;\n  __syncthreads();\n";
+    s << "  if (tid < " << sp.BM << ") {\n#pragma unroll\n    for (int g_ = 1; g_ < " << NSEG << "; ++g_) side_acc += side_r[g_ * "
+      << sp.BM << " + tid];\n  }\n";
+  }
   // partial tile -> scratch
   s << "  const i64 tix = bz * " << mtiles << " + mt;\n";
   s << "  float* part = (float*)a.p[" << scr_slot << "];\n";
