@@ -135,6 +135,17 @@ __device__ __forceinline__ float coherent_load(float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Four consecutive fp32 partials at byte offset `off` of a buffer (16-byte
+// aligned), loaded or stored with the cache policy of the device-scope
+// accesses above (performed at the device's point of coherence).
+__device__ __forceinline__ float4 coherent_load4(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 16));
+}
+typedef unsigned int u32x4_ __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void coherent_store4(__amdgpu_buffer_rsrc_t r, unsigned off, float4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_, v), r, off, 0, 16);
+}
+
 // ---- reductions across a group of G lanes of a wavefront (G power of two <= 64)
 template <int G> __device__ __forceinline__ float group_sum(float v) {
 #pragma unroll

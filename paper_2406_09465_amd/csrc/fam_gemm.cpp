@@ -259,7 +259,9 @@ void choose_tiles(GemmSpec& sp, bool split) {
     int64_t tiles = (sp.M + 127) / 128 * ((sp.N + sp.BN - 1) / sp.BN) * sp.batch;
     if (tiles < 240 && sp.M > 64) sp.BM = 64;
   }
-  if (split) sp.BM = sp.M <= 16 ? 16 : 32;
+  // split-K: 32-row tiles, or 16 when that is what brings the workgroup count
+  // (tiles times up to 16 splits) toward one per compute unit
+  if (split) sp.BM = sp.M <= 16 || (sp.M + 31) / 32 * sp.batch * 16 < 256 ? 16 : 32;
   sp.WN = sp.BN >= 64 ? 2 : 1;
   sp.WM = 4 / sp.WN;
   while (sp.BM / sp.WM < 16) {

@@ -315,8 +315,19 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "  const i64 tix = bz * " << mtiles << " + mt;\n";
   s << "  float* part = (float*)a.p[" << scr_slot << "];\n";
   s << "  float* sidep = part + " << base * S * tile << "LL;\n";
-  s << "  for (int i = tid; i < " << tile << "; i += 256) coherent_store(&part[(tix * " << S << " + split) * " << tile
-    << "LL + i], Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "]);\n";
+  // partial tiles move as float4 when rows of the C tile are 16-byte aligned
+  // and the tile partials fit a buffer resource's 32-bit offsets
+  const bool vec4 = tile % 4 == 0 && sp.BN % 4 == 0 && sp.LDC % 4 == 0 && base * S * tile * 4 < (int64_t(1) << 31);
+  if (vec4) {
+    s << "  const __amdgpu_buffer_rsrc_t rsP = __builtin_amdgcn_make_buffer_rsrc(part, 0, " << base * S * tile * 4
+      << ", 0x00020000);\n";
+    s << "#pragma unroll\n  for (int i = tid * 4; i < " << tile << "; i += 1024) coherent_store4(rsP, (unsigned)(((tix * " << S
+      << " + split) * " << tile << "LL + i) * 4), *(const float4*)&Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN
+      << "]);\n";
+  } else {
+    s << "  for (int i = tid; i < " << tile << "; i += 256) coherent_store(&part[(tix * " << S << " + split) * " << tile
+      << "LL + i], Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "]);\n";
+  }
   if (nside)
     s << "  if (tid < " << sp.BM << ") coherent_store(&sidep[(tix * " << S << " + split) * " << sp.BM << " + tid], side_acc);\n";
   // The partials are stored at the device's point of coherence; every wave
@@ -334,9 +345,21 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "    if (last_) __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
   s << "  __syncthreads();\n  if (!last_) return;\n";
   // deterministic sum of the partials, split 0 first
-  s << "  for (int i = tid; i < " << tile << "; i += 256) {\n    float acc_ = 0.0f;\n";
-  s << "    for (int p = 0; p < " << S << "; ++p) acc_ += coherent_load(&part[(tix * " << S << " + p) * " << tile << "LL + i]);\n";
-  s << "    Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "] = acc_;\n  }\n";
+  if (vec4) {
+    // all partial loads of a thread's float4 issued before they are summed
+    s << "#pragma unroll\n  for (int i = tid * 4; i < " << tile << "; i += 1024) {\n    float4 v_[" << S << "];\n";
+    s << "#pragma unroll\n    for (int p = 0; p < " << S << "; ++p) v_[p] = coherent_load4(rsP, (unsigned)(((tix * " << S
+      << " + p) * " << tile << "LL + i) * 4));\n";
+    s << "    float4 acc_ = make_float4(0.0f, 0.0f, 0.0f, 0.0f);\n";
+    s << "#pragma unroll\n    for (int p = 0; p < " << S << "; ++p) {\n      acc_.x += v_[p].x;\n      acc_.y += v_[p].y;\n"
+      << "      acc_.z += v_[p].z;\n      acc_.w += v_[p].w;\n    }\n";
+    s << "    *(float4*)&Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "] = acc_;\n  }\n";
+  } else {
+    s << "  for (int i = tid; i < " << tile << "; i += 256) {\n    float acc_ = 0.0f;\n";
+    s << "    for (int p = 0; p < " << S << "; ++p) acc_ += coherent_load(&part[(tix * " << S << " + p) * " << tile
+      << "LL + i]);\n";
+    s << "    Cs[(i / " << sp.BN << ") * " << sp.LDC << " + i % " << sp.BN << "] = acc_;\n  }\n";
+  }
   if (nside) {
     s << "  if (tid < " << sp.BM << ") {\n    float acc_ = 0.0f;\n";
     s << "    for (int p = 0; p < " << S << "; ++p) acc_ += coherent_load(&sidep[(tix * " << S << " + p) * " << sp.BM << " + tid]);\n";
