@@ -146,9 +146,9 @@ static size_t attention_lds_bytes(const AttnSpec& a) {
   int64_t dpad = (a.d + kstep - 1) / kstep * kstep;
   int64_t nkp = f32 ? (a.nk + 15) / 16 * 16 : (a.nk + 31) / 32 * 32;
   int64_t KSP = dpad + (f32 ? 4 : 8), NKP = nkp + (f32 ? 4 : 8);
-  int64_t dvp = (a.dv + 15) / 16 * 16, VP = dvp + 4;
+  int64_t dvp = (a.dv + 15) / 16 * 16, VP = dvp + (f32 ? 4 : 8);
   size_t ks = (size_t)(nkp * KSP * dtype_bytes(a.dtype));
-  size_t v = f32 ? (size_t)(nkp * VP * 4) : (size_t)(dvp * NKP * 2);
+  size_t v = (size_t)(nkp * VP * dtype_bytes(a.dtype));
   return ks + v + (size_t)(4 * 16 * NKP * dtype_bytes(a.dtype));
 }
 
@@ -180,10 +180,10 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   int KSP = (int)dpad + (f32 ? 4 : 8);                // Ks row pitch (elements)
   int NKP = (int)nkp + (f32 ? 4 : 8);                 // Ps / Vt row pitch
   int64_t dvp = (a.dv + 15) / 16 * 16;                // value width padded with zero columns
-  int VP = (int)dvp + 4;                              // fp32 V row pitch
+  int VP = (int)dvp + (f32 ? 4 : 8);                  // V row pitch ([key][dim] in LDS)
   int NF = (int)(nkp / 16), OF = (int)(dvp / 16);
   size_t ks_bytes = (size_t)nkp * KSP * dtype_bytes(a.dtype);
-  size_t v_bytes = f32 ? (size_t)nkp * VP * 4 : (size_t)dvp * NKP * 2;
+  size_t v_bytes = (size_t)nkp * VP * dtype_bytes(a.dtype);
   size_t p_bytes = (size_t)4 * 16 * NKP * dtype_bytes(a.dtype);
   size_t smem = ks_bytes + v_bytes + p_bytes;
   if (smem != attention_lds_bytes(a) || smem > 160 * 1024)
@@ -215,50 +215,79 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   s << "  const i64 bz = blockIdx.y;\n";
   s << "  const i64 qoff = bz * " << a.nq * a.d << "LL, koff = bz * " << a.nk * a.d << "LL, voff = bz * "
     << a.nk * a.dv << "LL, ooff = bz * " << a.nq * a.dv << "LL;\n";
-  // K into LDS as [key][dim] (zero-padded dims); 16-byte vectors along dim
-  // when the rows allow (row pitches are multiples of 16 bytes)
+  // K and V into LDS as [key][dim] (zero-padded), 16-byte vectors along dim
+  // when the rows allow (row pitches are multiples of 16 bytes).  When a
+  // thread's share is small, all of its loads are issued before the first
+  // LDS write (one round trip to memory); the query fragments of the
+  // half-precision paths are loaded before them as well.
   const int VL = 16 / dtype_bytes(a.dtype);
   const std::string VT = "vec_t<" + std::to_string(VL) + ", " + T + ">";
-  if (!a.k_is_kt && a.d % VL == 0 && dpad % VL == 0) {
-    s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dpad / VL << "; i += 256) {\n";
-    s << "    const int key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
-    s << "    " << VT << " x_ = {};\n";
-    s << "    if (dim < " << a.d << " && key < " << a.nk << ") x_ = *(const " << VT << "*)(" << K << " + koff + (i64)key * "
+  const std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
+  const int64_t QF = f32 ? 0 : dpad / 32;  // query fragments per lane
+  if (!f32) {
+    s << "  const i64 qr_ = " << (ksplit ? "(i64)blockIdx.x * 16" : "(i64)blockIdx.x * 64 + wave * 16") << " + (l & 15);\n";
+    s << "  " << V8 << " qa_[" << QF << "];\n";
+    s << "#pragma unroll\n  for (int kk = 0; kk < " << QF << "; ++kk) {\n";
+    s << "    const int dim = kk * 32 + (l >> 4) * 8;\n";
+    s << "    if (qr_ < " << a.nq << "LL && dim + 8 <= " << a.d << ") qa_[kk] = *(const " << V8 << "*)(" << Q << " + qoff + qr_ * "
       << a.d << " + dim);\n";
-    s << "    *(" << VT << "*)(Ks + key * " << KSP << " + dim) = x_;\n  }\n";
-  } else {
-    s << "  for (int i = tid; i < " << nkp * dpad << "; i += 256) {\n";
-    s << "    const int key = i / " << dpad << ", dim = i % " << dpad << ";\n";
-    if (a.k_is_kt)
-      s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K
-        << "[koff + (i64)dim * " << a.nk << " + key] : fromf<" << T << ">(0.0f);\n";
-    else
-      s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K
-        << "[koff + (i64)key * " << a.d << " + dim] : fromf<" << T << ">(0.0f);\n";
-    s << "  }\n";
+    s << "    else {\n#pragma unroll\n      for (int j = 0; j < 8; ++j) qa_[kk][j] = (qr_ < " << a.nq << "LL && dim + j < " << a.d
+      << ") ? " << Q << "[qoff + qr_ * " << a.d << " + dim + j] : fromf<" << T << ">(0.0f);\n    }\n  }\n";
   }
-  // V into LDS: fp32 natural [key][dim]; half precision transposed [dim][key]
-  if (a.dv % VL == 0 && dvp % VL == 0) {
-    s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dvp / VL << "; i += 256) {\n";
-    s << "    const int key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
-    s << "    " << VT << " x_ = {};\n";
-    s << "    if (key < " << a.nk << " && dim < " << a.dv << ") x_ = *(const " << VT << "*)(" << V << " + voff + (i64)key * "
-      << a.dv << " + dim);\n";
-    if (f32)
-      s << "    *(" << VT << "*)(Vs + key * " << VP << " + dim) = x_;\n";
-    else
-      s << "#pragma unroll\n    for (int e = 0; e < " << VL << "; ++e) Vs[(dim + e) * " << NKP << " + key] = x_[e];\n";
-    s << "  }\n";
+  const bool vecK = !a.k_is_kt && a.d % VL == 0 && dpad % VL == 0;
+  const bool vecV = a.dv % VL == 0 && dvp % VL == 0;
+  const int64_t NIK = (nkp * dpad / VL + 255) / 256, NIV = (nkp * dvp / VL + 255) / 256;
+  if (vecK && vecV && NIK + NIV <= 24) {
+    s << "  " << VT << " kx_[" << NIK << "], vx_[" << NIV << "];\n";
+    s << "#pragma unroll\n  for (int j = 0; j < " << NIK << "; ++j) {\n";
+    s << "    const int i = tid + j * 256, key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
+    s << "    kx_[j] = " << VT << "{};\n";
+    s << "    if (i < " << nkp * dpad / VL << " && dim < " << a.d << " && key < " << a.nk << ") kx_[j] = *(const " << VT << "*)(" << K
+      << " + koff + (i64)key * " << a.d << " + dim);\n  }\n";
+    s << "#pragma unroll\n  for (int j = 0; j < " << NIV << "; ++j) {\n";
+    s << "    const int i = tid + j * 256, key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
+    s << "    vx_[j] = " << VT << "{};\n";
+    s << "    if (i < " << nkp * dvp / VL << " && key < " << a.nk << " && dim < " << a.dv << ") vx_[j] = *(const " << VT << "*)(" << V
+      << " + voff + (i64)key * " << a.dv << " + dim);\n  }\n";
+    s << "#pragma unroll\n  for (int j = 0; j < " << NIK << "; ++j) {\n";
+    s << "    const int i = tid + j * 256, key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
+    s << "    if (i < " << nkp * dpad / VL << ") *(" << VT << "*)(Ks + key * " << KSP << " + dim) = kx_[j];\n  }\n";
+    s << "#pragma unroll\n  for (int j = 0; j < " << NIV << "; ++j) {\n";
+    s << "    const int i = tid + j * 256, key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
+    s << "    if (i < " << nkp * dvp / VL << ") *(" << VT << "*)(Vs + key * " << VP << " + dim) = vx_[j];\n  }\n";
   } else {
-    s << "  for (int i = tid; i < " << nkp * dvp << "; i += 256) {\n";
-    s << "    const int key = i / " << dvp << ", dim = i % " << dvp << ";\n";
-    s << "    const " << T << " x_ = (key < " << a.nk << " && dim < " << a.dv << ") ? " << V << "[voff + (i64)key * "
-      << a.dv << " + dim] : fromf<" << T << ">(0.0f);\n";
-    if (f32)
-      s << "    Vs[key * " << VP << " + dim] = x_;\n";
-    else
-      s << "    Vs[dim * " << NKP << " + key] = x_;\n";
-    s << "  }\n";
+    if (vecK) {
+      s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dpad / VL << "; i += 256) {\n";
+      s << "    const int key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
+      s << "    " << VT << " x_ = {};\n";
+      s << "    if (dim < " << a.d << " && key < " << a.nk << ") x_ = *(const " << VT << "*)(" << K << " + koff + (i64)key * "
+        << a.d << " + dim);\n";
+      s << "    *(" << VT << "*)(Ks + key * " << KSP << " + dim) = x_;\n  }\n";
+    } else {
+      s << "  for (int i = tid; i < " << nkp * dpad << "; i += 256) {\n";
+      s << "    const int key = i / " << dpad << ", dim = i % " << dpad << ";\n";
+      if (a.k_is_kt)
+        s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K
+          << "[koff + (i64)dim * " << a.nk << " + key] : fromf<" << T << ">(0.0f);\n";
+      else
+        s << "    Ks[key * " << KSP << " + dim] = (dim < " << a.d << " && key < " << a.nk << ") ? " << K
+          << "[koff + (i64)key * " << a.d << " + dim] : fromf<" << T << ">(0.0f);\n";
+      s << "  }\n";
+    }
+    if (vecV) {
+      s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dvp / VL << "; i += 256) {\n";
+      s << "    const int key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
+      s << "    " << VT << " x_ = {};\n";
+      s << "    if (key < " << a.nk << " && dim < " << a.dv << ") x_ = *(const " << VT << "*)(" << V << " + voff + (i64)key * "
+        << a.dv << " + dim);\n";
+      s << "    *(" << VT << "*)(Vs + key * " << VP << " + dim) = x_;\n  }\n";
+    } else {
+      s << "  for (int i = tid; i < " << nkp * dvp << "; i += 256) {\n";
+      s << "    const int key = i / " << dvp << ", dim = i % " << dvp << ";\n";
+      s << "    Vs[key * " << VP << " + dim] = (key < " << a.nk << " && dim < " << a.dv << ") ? " << V << "[voff + (i64)key * "
+        << a.dv << " + dim] : fromf<" << T << ">(0.0f);\n";
+      s << "  }\n";
+    }
   }
   s << "  __syncthreads();\n";
   std::string chain_expr = "x";
@@ -284,14 +313,10 @@ GenKernel gen_attention(const KInfo& ki, int index) {
       s << "#pragma unroll\n    for (int f = 0; f < " << NFW << "; ++f) sc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, Ks[(kb + f * 16 + (l & 15)) * "
         << KSP << " + dim], sc[f], 0, 0, 0);\n  }\n";
     } else {
-      std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
       std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
       s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 32 << "; ++kk) {\n";
       s << "    const int dim = kk * 32 + (l >> 4) * 8;\n";
-      s << "    " << V8 << " qa;\n";
-      s << "    if (qv && dim + 8 <= " << a.d << ") qa = *(const " << V8 << "*)(" << Q << " + qoff + qr * " << a.d << " + dim);\n";
-      s << "    else {\n#pragma unroll\n      for (int j = 0; j < 8; ++j) qa[j] = (qv && dim + j < " << a.d << ") ? " << Q
-        << "[qoff + qr * " << a.d << " + dim + j] : fromf<" << T << ">(0.0f);\n    }\n";
+      s << "    const " << V8 << " qa = qa_[kk];\n";
       s << "#pragma unroll\n    for (int f = 0; f < " << NFW << "; ++f) sc[f] = " << fn << "(qa, *(const " << V8
         << "*)(Ks + (kb + f * 16 + (l & 15)) * " << KSP << " + dim), sc[f], 0, 0, 0);\n  }\n";
     }
@@ -328,13 +353,14 @@ GenKernel gen_attention(const KInfo& ki, int index) {
       s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, Vs[(kb + key) * " << VP
         << " + f * 16 + (l & 15)], oc[f], 0, 0, 0);\n  }\n";
     } else {
-      std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
       std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
       s << "#pragma unroll\n  for (int kk = 0; kk < " << NKW / 32 << "; ++kk) {\n";
       s << "    const int key = kk * 32 + (l >> 4) * 8;\n";
       s << "    const " << V8 << " pa = *(const " << V8 << "*)(Pw + (l & 15) * " << NKP << " + key);\n";
-      s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = " << fn << "(pa, *(const " << V8
-        << "*)(Vs + (f * 16 + (l & 15)) * " << NKP << " + kb + key), oc[f], 0, 0, 0);\n  }\n";
+      // V[key][dim] read transposed: lane l gets keys key..key+7 of column f*16 + (l & 15)
+      s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = " << fn << "(pa, __builtin_bit_cast(" << V8
+        << ", lds_tr_k8(Vs + (kb + key + ((l & 15) >> 2)) * " << VP << " + f * 16 + 4 * (l & 3), " << VP
+        << ")), oc[f], 0, 0, 0);\n  }\n";
     }
     s << "  float* Op = (float*)(smem + " << op_off << ");  // [wave][16 rows][" << dvp << "]\n";
     s << "#pragma unroll\n  for (int f = 0; f < " << OF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) Op[(wave * 16 + (l >> 4) * 4 + i) * "
@@ -366,14 +392,10 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     s << "#pragma unroll\n    for (int f = 0; f < " << NF << "; ++f) sc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, Ks[(f * 16 + (l & 15)) * "
       << KSP << " + dim], sc[f], 0, 0, 0);\n  }\n";
   } else {
-    std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
     std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
     s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 32 << "; ++kk) {\n";
     s << "    const int dim = kk * 32 + (l >> 4) * 8;\n";
-    s << "    " << V8 << " qa;\n";
-    s << "    if (qv && dim + 8 <= " << a.d << ") qa = *(const " << V8 << "*)(" << Q << " + qoff + qr * " << a.d << " + dim);\n";
-    s << "    else {\n#pragma unroll\n      for (int j = 0; j < 8; ++j) qa[j] = (qv && dim + j < " << a.d << ") ? " << Q
-      << "[qoff + qr * " << a.d << " + dim + j] : fromf<" << T << ">(0.0f);\n    }\n";
+    s << "    const " << V8 << " qa = qa_[kk];\n";
     s << "#pragma unroll\n    for (int f = 0; f < " << NF << "; ++f) sc[f] = " << fn << "(qa, *(const " << V8
       << "*)(Ks + (f * 16 + (l & 15)) * " << KSP << " + dim), sc[f], 0, 0, 0);\n  }\n";
   }
@@ -403,13 +425,13 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, Vs[key * " << VP
       << " + f * 16 + (l & 15)], oc[f], 0, 0, 0);\n  }\n";
   } else {
-    std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
     std::string fn = a.dtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16" : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
     s << "#pragma unroll\n  for (int kk = 0; kk < " << nkp / 32 << "; ++kk) {\n";
     s << "    const int key = kk * 32 + (l >> 4) * 8;\n";
     s << "    const " << V8 << " pa = *(const " << V8 << "*)(Pw + (l & 15) * " << NKP << " + key);\n";
-    s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = " << fn << "(pa, *(const " << V8
-      << "*)(Vs + (f * 16 + (l & 15)) * " << NKP << " + key), oc[f], 0, 0, 0);\n  }\n";
+    // V[key][dim] read transposed: lane l gets keys key..key+7 of column f*16 + (l & 15)
+    s << "#pragma unroll\n    for (int f = 0; f < " << OF << "; ++f) oc[f] = " << fn << "(pa, __builtin_bit_cast(" << V8
+      << ", lds_tr_k8(Vs + (key + ((l & 15) >> 2)) * " << VP << " + f * 16 + 4 * (l & 3), " << VP << ")), oc[f], 0, 0, 0);\n  }\n";
   }
   s << "#pragma unroll\n  for (int f = 0; f < " << OF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
   s << "    const i64 row = q0 + (l >> 4) * 4 + i;\n";
