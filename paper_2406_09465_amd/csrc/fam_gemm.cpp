@@ -240,11 +240,15 @@ void choose_tiles(GemmSpec& sp, bool split) {
   if (!split && nt > 64 && sp.mms.size() == 1) {
     // Tile shape by a throughput model of 256 compute units: tiles run in
     // rounds of 256, each round costs its tile area, and every tile pays for
-    // re-reading its operand panels (proportional to 1/BM + 1/BN).
+    // re-reading its operand panels (proportional to 1/BM + 1/BN).  192-wide
+    // tiles (half precision, k-tiles of 32 so that two workgroups still share
+    // a compute unit's LDS) serve products whose 128-wide tiles would leave a
+    // half-filled last round.
     double best = 1e300;
     for (int bm : {128, 64}) {
-      for (int bn : {128, 96, 64}) {
+      for (int bn : {128, 96, 64, 192}) {
         if (bn == 96 && sp.N % 96 != 0) continue;
+        if (bn == 192 && (sp.N % 192 != 0 || f32 || bm != 128)) continue;
         int64_t tiles = (sp.M + bm - 1) / bm * ((sp.N + bn - 1) / bn) * sp.batch;
         double rounds = (double)((tiles + 255) / 256);
         double cost = rounds * bm * bn * (1.0 + 24.0 * (1.0 / bm + 1.0 / bn));
@@ -255,6 +259,7 @@ void choose_tiles(GemmSpec& sp, bool split) {
         }
       }
     }
+    if (sp.BN == 192) sp.BK = std::min(sp.BK, 32);
   } else if (!split) {
     int64_t tiles = (sp.M + 127) / 128 * ((sp.N + sp.BN - 1) / sp.BN) * sp.batch;
     if (tiles < 240 && sp.M > 64) sp.BM = 64;

@@ -47,6 +47,10 @@ GEMM_CASES = [
     dict(m=256, d=192, h=2048),
 ]
 
+# An MLP block whose first product takes 128 x 192 tiles: ragged rows (4000)
+# and a ragged contraction (176 = 5.5 k-tiles of 32).
+WIDE_TILE_CASE = dict(m=4000, d=176, h=1536)
+
 # Attention shapes of the attention-kernel GPU tests (few query rows: the keys
 # are split over the waves; fp32 and fp16, padded keys), each run with the key
 # split and without it (KORCH_ATTN_NO_KEY_SPLIT=1).
@@ -82,6 +86,7 @@ def _jobs():
     for sz in GEMM_CASES:
         for flag in ("", "1"):
             jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_NO_KSPLIT", flag)))
+    jobs.append(("plans", "mlp", WIDE_TILE_CASE, None))
     for wl, sz in ATTN_CASES:
         for flag in ("", "1"):
             jobs.append(("env_plans", wl, sz, ("KORCH_ATTN_NO_KEY_SPLIT", flag)))

@@ -319,7 +319,7 @@ def test_timed_execute_rejects_a_kernel_outside_the_range():
 
 def test_gemm_k_split_selection():
     """GEMM2 of the MLP block (256 tiles, 48 k-tiles) and of the odd-k test shape
-    use the intra-workgroup split of K; GEMM1 (768 tiles) and
+    use the intra-workgroup split of K; GEMM1 (512 tiles) and
     KORCH_GEMM_NO_KSPLIT=1 do not."""
     from paper_2406_09465_amd.warm import GEMM_CASES
 
@@ -343,6 +343,28 @@ def test_gemm_k_split_selection():
         assert "kgrp" not in src[2] and launch[2][1][0] == 256, sz
     src, _ = sources({}, "")
     assert "kgrp" not in src[1]
+
+
+def test_gemm_wide_tile_selection():
+    """GEMM1 of the MLP block (4096 x 3072 output) takes 128 x 192 tiles with
+    k-tiles of 32: 512 tiles, two per compute unit in one round, where 128 x 128
+    tiles would leave a half-filled second round.  The ragged 4000 x 1536 shape
+    of the GPU test takes them too (32 x 8 tiles); a hidden width that 192 does
+    not divide keeps narrower tiles."""
+    from paper_2406_09465_amd.warm import WIDE_TILE_CASE
+
+    def gemm1(sizes):
+        p = graphs.build("mlp", **sizes).plan("layered")
+        p.compile()
+        return p.kernel_launch(1), p.kernel_source(1)
+
+    (grid, block, _), src = gemm1({})
+    assert grid == (512, 1, 1) and block == (256, 1, 1)
+    assert "* 40 + " in src  # A tile rows of 32 + 8 halves (k-tiles of 32)
+    (grid, _, _), _ = gemm1(WIDE_TILE_CASE)
+    assert grid == (32 * 8, 1, 1)
+    (grid, _, _), _ = gemm1(dict(m=500, d=256, h=1056))
+    assert grid[0] != 4 * 1056 // 192
 
 
 def test_attention_key_split_selection():

@@ -40,3 +40,17 @@ def test_gemm_k_split(sizes, plan, no_split, monkeypatch):
     out = PlanRunner(w, plan).run(raw)
     ok, mx, rel = close(out["out"], ref["out"], TOL[w.dtype])
     assert ok, f"mlp {sizes}: max abs err {mx:.3e}, normwise rel {rel:.3e}"
+
+
+@pytest.mark.parametrize("plan", ["layered", "fused"])
+def test_gemm_wide_tiles(plan):
+    """128 x 192 tiles with k-tiles of 32 (ragged rows and contraction)."""
+    from paper_2406_09465_amd import graphs
+    from paper_2406_09465_amd.runner import PlanRunner
+    from paper_2406_09465_amd.warm import WIDE_TILE_CASE as sizes
+    print(f"\n[case] mlp {sizes} {plan} wide tiles", flush=True)
+    w = graphs.build("mlp", **sizes)
+    raw, ref = reference("mlp", sizes)
+    out = PlanRunner(w, plan).run(raw)
+    ok, mx, rel = close(out["out"], ref["out"], TOL[w.dtype])
+    assert ok, f"mlp {sizes}: max abs err {mx:.3e}, normwise rel {rel:.3e}"
