@@ -1100,11 +1100,12 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   int64_t ntm = (sp.M + sp.BM - 1) / sp.BM;
   int64_t KT = (sp.K + sp.BK - 1) / sp.BK;
   // Intra-workgroup split of the contraction: when the tiles leave at most one
-  // workgroup per compute unit (one wave per SIMD, which issues an MFMA only
-  // every other slot) and K is long, the workgroup runs two groups of four
-  // waves, each over half of the k-tiles with operand buffers of its own, and
-  // adds the second group's accumulators to the first group's in the C tile
-  // (a fixed order).  Eight waves per compute unit then issue MFMAs and loads.
+  // workgroup per compute unit (one wave per SIMD, which then waits alone on
+  // its loads, LDS traffic and barriers) and K is long, the workgroup runs two
+  // groups of four waves, each over half of the k-tiles with operand buffers
+  // of its own, and adds the second group's accumulators to the first group's
+  // in the C tile (a fixed order).  Eight waves per compute unit then issue
+  // MFMAs and loads, one group's waits covered by the other's products.
   const size_t op_bytes = (size_t)2 * ((size_t)sp.BM * sp.BKP + (size_t)b_buf_elems(sp)) * dtype_bytes(sp.mtype);
   const size_t ksplit_lds = std::max(2 * op_bytes, (size_t)sp.BM * sp.LDC * 4);
   const bool ksplit = !sp.conv && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 && sp.NT == 256 &&
