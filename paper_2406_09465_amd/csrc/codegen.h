@@ -115,6 +115,16 @@ struct Emitter {
   // thread: a staged load whose offset does not use it is issued once per stage
   // (slot 0) and shared by all slots.
   std::string slot_var;
+  // Loop-invariant loads: when `varying` is set, a hoisted (non-staged) load
+  // whose offset uses none of these iteration variables is the same for every
+  // element a thread visits.  It goes to `inv` instead of `pre`, as a
+  // declaration followed by a block that opens with `inv_defs` (definitions
+  // of the invariant variables the offset uses) and loads only when
+  // `inv_guard` holds (the value stays 0 otherwise).
+  std::vector<std::string> varying;
+  std::string inv_defs, inv_guard;
+  std::ostringstream inv;
+  int n_invariant = 0;
 
   Emitter(const Graph& gg) : g(gg) {}
   std::string value(int node, const std::vector<Ix>& idx);
@@ -129,5 +139,13 @@ std::vector<Ix> broadcast_index(const Shape& shape, const Shape& itshape, const 
 
 // Common header for generated sources.
 std::string source_header(int nargs);
+
+// Store of V consecutive elements of kernel output `node` from the float array
+// `src` (V = 0: the one float value `src`) at element offset `off` of its
+// storage `P` (a uniform base pointer): written
+// through to the device's point of coherence (`stv_out` / `st1_out`) unless the
+// tensor is 2 GiB or larger.
+std::string out_store(const Graph& g, int node, const std::string& P, const std::string& off, int V,
+                      const std::string& src);
 
 }  // namespace korch

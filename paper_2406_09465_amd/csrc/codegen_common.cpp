@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <numeric>
 
 #include "codegen.h"
@@ -314,6 +315,16 @@ static bool uses_var(const std::string& e, const std::string& v) {
   return false;
 }
 
+std::string out_store(const Graph& g, int node, const std::string& P, const std::string& off, int V,
+                      const std::string& src) {
+  const Node& n = g.nodes[node];
+  static const bool plain = getenv("KORCH_OUT_PLAIN") && atoi(getenv("KORCH_OUT_PLAIN")) != 0;  // ablation switch
+  const bool big = plain || (double)numel(n.shape) * dtype_bytes(n.dtype) >= 2147483648.0;
+  if (V == 0) return big ? "st1(" + P + " + " + off + ", " + src + ")" : "st1_out(" + P + ", " + off + ", " + src + ")";
+  const std::string v = std::to_string(V);
+  return big ? "stv<" + v + ">(" + P + " + " + off + ", " + src + ")" : "stv_out<" + v + ">(" + P + ", " + off + ", " + src + ")";
+}
+
 std::string Emitter::load(int node, const std::vector<Ix>& idx) {
   auto it = argslot.find(node);
   if (it == argslot.end()) fail(KORCH_E_UNSUPPORTED, "emitter: node " + std::to_string(node) + " is not available");
@@ -341,6 +352,22 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
     ++n_vector;
     pre << "*(const " << ty << "*)(" << P << " + " << off.b << ");\n";
     return "tof(" + v + at + "[e])";
+  }
+  bool invariant = hoist && gcond.empty() && off.affine && !varying.empty() &&
+                   (off.c == 0 || (off.c == 1 && vec > 1 && off.al % vec == 0));
+  for (const std::string& v : varying)
+    if (invariant && uses_var(off.b, v)) invariant = false;
+  if (invariant) {
+    ++n_invariant;
+    std::string v = fresh(off.c == 0 ? "iu" : "ix");
+    if (off.c == 0) {
+      inv << "  float " << v << " = 0.0f;\n  {\n    " << inv_defs << "\n    if (" << inv_guard << ") " << v << " = ld1(" << P
+          << " + " << off.b << ");\n  }\n";
+      return v;
+    }
+    inv << "  float " << v << "[" << vec << "] = {};\n  {\n    " << inv_defs << "\n    if (" << inv_guard << ") ldv<" << vec
+        << ">(" << v << ", " << P << " + " << off.b << ");\n  }\n";
+    return v + "[e]";
   }
   if (hoist && off.affine && off.c == 0) {
     ++n_uniform;

@@ -78,6 +78,53 @@ __device__ __forceinline__ void stv(T* __restrict__ p, const float* s) {
 template <typename T> __device__ __forceinline__ float ld1(const T* __restrict__ p) { return tof(*p); }
 template <typename T> __device__ __forceinline__ void st1(T* __restrict__ p, float v) { *p = fromf<T>(v); }
 
+// ---- kernel output stores --------------------------------------------------
+// A kernel output is written once and read only by later kernels.  It is
+// stored with the device-scope cache policy (sc1), which writes it through
+// the XCD's L2 to the device's point of coherence while the kernel runs.  A
+// plain store leaves the line dirty in L2, and the release at the end of the
+// kernel then writes back every such line after the last workgroup has
+// finished (about 0.16 us per MB of output on this part, not overlapped with
+// any work).  `base` is the tensor's (uniform) base pointer, `off` the element
+// offset of the first of V consecutive elements; tensors stay below 2 GiB.
+typedef unsigned int u32x2_ __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4o_ __attribute__((ext_vector_type(4)));
+template <int V, typename T>
+__device__ __forceinline__ void stv_out(T* base, i64 off, const float* s) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
+  const unsigned o = (unsigned)(off * (i64)sizeof(T));
+  typedef typename VecOf<V, T>::type VT;
+  VT v;
+  if constexpr (V == 1) {
+    v = fromf<T>(s[0]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < V; ++i) v[i] = fromf<T>(s[i]);
+  }
+  constexpr int B = V * (int)sizeof(T);
+  if constexpr (B == 16) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4o_, v), r, o, 0, 16);
+  } else if constexpr (B == 8) {
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_, v), r, o, 0, 16);
+  } else if constexpr (B == 4) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, o, 0, 16);
+  } else if constexpr (B == 2) {
+    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, v), r, o, 0, 16);
+  } else if constexpr (B % 16 == 0) {
+    struct W {
+      u32x4o_ q[B / 16];
+    };
+    const W w = __builtin_bit_cast(W, v);
+#pragma unroll
+    for (int q = 0; q < B / 16; ++q) __builtin_amdgcn_raw_buffer_store_b128(w.q[q], r, o + 16 * q, 0, 16);
+  } else {
+    *reinterpret_cast<VT*>(base + off) = v;
+  }
+}
+template <typename T> __device__ __forceinline__ void st1_out(T* base, i64 off, float v) {
+  stv_out<1, T>(base, off, &v);
+}
+
 // ---- elementwise functions (fp32) -----------------------------------------
 __device__ __forceinline__ float k_relu(float x) { return x > 0.0f ? x : 0.0f; }
 __device__ __forceinline__ float k_rsqrt(float x) { return 1.0f / sqrtf(x); }

@@ -369,8 +369,8 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     s << "  for (int t = tid; t < " << 16 * dvp << "; t += 256) {\n";
     s << "    const int row = t / " << dvp << ", col = t % " << dvp << ";\n";
     s << "    const float o_ = ((Op[t] + Op[" << 16 * dvp << " + t]) + Op[" << 32 * dvp << " + t]) + Op[" << 48 * dvp << " + t];\n";
-    s << "    if (q0 + row < " << a.nq << "LL && col < " << a.dv << ") st1(" << O << " + ooff + (q0 + row) * " << a.dv
-      << " + col, o_);\n  }\n";
+    s << "    if (q0 + row < " << a.nq << "LL && col < " << a.dv << ") "
+      << out_store(g, a.o, O, "ooff + (q0 + row) * " + std::to_string(a.dv) + " + col", 0, "o_") << ";\n  }\n";
     s << "}\n";
     gk.source = s.str();
     gk.grid[0] = (int)((a.nq + 15) / 16);
@@ -436,8 +436,8 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   s << "#pragma unroll\n  for (int f = 0; f < " << OF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
   s << "    const i64 row = q0 + (l >> 4) * 4 + i;\n";
   s << "    const int col = f * 16 + (l & 15);\n";
-  s << "    if (row < " << a.nq << "LL && col < " << a.dv << ") st1(" << O << " + ooff + row * " << a.dv
-    << " + col, oc[f][i]);\n  }\n";
+  s << "    if (row < " << a.nq << "LL && col < " << a.dv << ") "
+    << out_store(g, a.o, O, "ooff + row * " + std::to_string(a.dv) + " + col", 0, "oc[f][i]") << ";\n  }\n";
   s << "}\n";
   gk.source = s.str();
   gk.grid[0] = (int)((a.nq + 63) / 64);

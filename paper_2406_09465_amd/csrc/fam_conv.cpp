@@ -65,13 +65,17 @@ bool plan_direct(const GemmSpec& sp, Direct& d, std::string* why) {
   for (int wn : {1, 2, 4})
     if (!d.WN && fn_all % wn == 0 && fn_all / wn <= 2) d.WN = wn;
   if (!d.WN) d.WN = fn_all % 4 == 0 ? 4 : fn_all % 2 == 0 ? 2 : 1;
+  if (const char* e = getenv("KORCH_CONV_WN")) {  // waves along channels (launch-shape sweeps)
+    const int wn = atoi(e);
+    if ((wn == 1 || wn == 2 || wn == 4) && fn_all % wn == 0) d.WN = wn;
+  }
   d.FN = fn_all / d.WN;
   d.WTN = d.FN * 16;
   d.WM = 4 / d.WN;
   d.PW = 128 / d.WM;
   d.FM = d.PW / 16;
   // weight fragments held per lane: taps x chunks x FN fragments of 4 VGPRs
-  if (d.taps * d.CC * d.FN * 4 > 128) return no("weights of a wave exceed 128 registers per lane");
+  if (d.taps * d.CC * d.FN * 4 > 144) return no("weights of a wave exceed 144 registers per lane");
   d.TW = sp.Wo > 16 ? 32 : 16;
   d.TH = 128 / d.TW;
   d.HR = d.TH + (int)sp.KH - 1;
@@ -244,6 +248,10 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   s << "  stash_halo(0);\n  __syncthreads();\n";
   // per-lane part of the halo address of a fragment: pixel column (l & 15), channels (l >> 4) * 8
   s << "  const int lane_off = (l & 15) * " << d.CPP << " + (l >> 4) * 8;\n";
+  // per-channel epilogue operands are loaded once, before the tile loop
+  std::string inv;
+  const std::string epi = gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(d.LDC), {}, d.TW, 0, "0", &inv);
+  s << inv;
   s << "  int b = 0;\n";
   s << "  for (;;) {\n";
   s << "    const int tn = t + tstep;\n    const bool more = tn < tend;\n";
@@ -252,18 +260,31 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   s << "#pragma unroll\n    for (int f = 0; f < " << d.FM << "; ++f)\n#pragma unroll\n    for (int j = 0; j < " << d.FN
     << "; ++j) acc[f][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
   s << "    const " << T << "* Hb = Hs + b * " << HALO << " + lane_off;\n";
-  s << "#pragma unroll\n    for (int tp = 0; tp < " << d.taps << "; ++tp) {\n";
-  s << "      const int ky = tp / " << sp.KW << ", kx = tp % " << sp.KW << ";\n";
-  s << "#pragma unroll\n      for (int cc = 0; cc < " << d.CC << "; ++cc) {\n";
-  s << "        " << V8 << " af[" << d.FM << "];\n";
-  s << "#pragma unroll\n        for (int f = 0; f < " << d.FM << "; ++f) {\n";
-  s << "          const int pb = wm * " << d.PW << " + f * 16, ty = pb / " << d.TW << ", tx = pb % " << d.TW << ";\n";
-  s << "          af[f] = *(const " << V8 << "*)(Hb + ((ty + ky) * " << d.HC << " + tx + kx) * " << d.CPP
-    << " + cc * 32);\n";
-  s << "        }\n";
-  s << "#pragma unroll\n        for (int f = 0; f < " << d.FM << "; ++f)\n#pragma unroll\n        for (int j = 0; j < " << d.FN
-    << "; ++j) acc[f][j] = " << mfma << "(af[f], bfr[tp][cc][j], acc[f][j], 0, 0, 0);\n";
-  s << "      }\n    }\n";
+  // The wave's pixels are R rows of TW columns.  Every left-operand fragment
+  // (16 pixels of one halo row at a column shift kx) is read from LDS once and
+  // used for each of the wave's rows fr it serves (filter row ky = hr - fr), so
+  // a wave reads (R + KH - 1) * KW fragments per column block instead of
+  // R * KH * KW.  For each output fragment the taps still accumulate in
+  // (ky, kx, channel chunk) order.
+  const int R = d.PW / d.TW, FC = d.TW / 16;
+  s << "    const " << T << "* Hw = Hb + wm * " << R * d.HC * d.CPP << ";\n";
+  for (int hr = 0; hr < R + (int)sp.KH - 1; ++hr)
+    for (int kx = 0; kx < (int)sp.KW; ++kx)
+      for (int fc = 0; fc < FC; ++fc)
+        for (int cc = 0; cc < d.CC; ++cc) {
+          s << "    {\n      const " << V8 << " af = *(const " << V8 << "*)(Hw + " << ((int64_t)hr * d.HC + fc * 16 + kx) * d.CPP + cc * 32
+            << ");\n";
+          for (int fr = 0; fr < R; ++fr) {
+            const int ky = hr - fr;
+            if (ky < 0 || ky >= (int)sp.KH) continue;
+            const int f = fr * FC + fc, tp = ky * (int)sp.KW + kx;
+            for (int j = 0; j < d.FN; ++j)
+              s << "      acc[" << f << "][" << j << "] = " << mfma << "(af, bfr[" << tp << "][" << cc << "][" << j << "], acc[" << f
+                << "][" << j << "], 0, 0, 0);\n";
+          }
+          s << "    }\n";
+        }
+
   s << "#pragma unroll\n    for (int f = 0; f < " << d.FM << "; ++f)\n#pragma unroll\n    for (int j = 0; j < " << d.FN
     << "; ++j)\n#pragma unroll\n    for (int r = 0; r < 4; ++r) Cs[(wm * " << d.PW << " + f * 16 + (l >> 4) * 4 + r) * "
     << d.LDC << " + wn * " << d.WTN << " + j * 16 + (l & 15)] = acc[f][j][r];\n";
@@ -271,7 +292,7 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   s << "    {\n    " << origin("t");
   if (sp.nb) s << "    const i64 z0 = z_;\n";
   s << "    (void)z_;\n";
-  s << gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(d.LDC), {}, d.TW);
+  s << epi;
   s << "    }\n";
   s << "    if (more) stash_halo(b ^ 1);\n";
   s << "    __syncthreads();\n";

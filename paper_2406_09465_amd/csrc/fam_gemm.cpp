@@ -969,7 +969,7 @@ size_t gemm_smem_bytes(const GemmSpec& sp) {
 // Pointwise epilogue over the C tile: every kernel output at (batch, m, n).
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
                           const std::string& cs_row, const std::set<int>& skip, int conv_tw, int rows,
-                          const std::string& row0) {
+                          const std::string& row0, std::string* hoisted) {
   const Graph& g = ki.g;
   int maxb = 2;
   for (int o : ki.k.outs) maxb = std::max(maxb, dtype_bytes(g.nodes[o].dtype));
@@ -992,6 +992,12 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
     it.push_back(Ix::var("m"));
   }
   it.push_back(Ix::var("n", 1, VE));
+  if (sp.NT % (cols / VE) == 0) {
+    // every element of a thread has the same column vector
+    for (size_t d = 0; d + 1 < it.size(); ++d) em.varying.push_back(it[d].b);
+    em.inv_defs = "const i64 n = n0 + (i64)((tid % " + std::to_string(cols / VE) + ") * " + std::to_string(VE) + ");";
+    em.inv_guard = "n < " + std::to_string(sp.N) + "LL";
+  }
   std::map<std::string, std::string> canon;
   // C tile values of a full-width product are read into registers with 16-byte
   // LDS reads before the element loop (rows start 16-byte aligned: LDC and the
@@ -1034,7 +1040,7 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
       std::string arr = "_o" + std::to_string(o);
       decl << "      float " << arr << "[" << VE << "];\n";
       em.body << "        " << arr << "[e] = " << v << ";\n";
-      after << "      stv<" << VE << ">(" << P << " + " << off.b << ", " << arr << ");\n";
+      after << "      " << out_store(g, o, P, off.b, VE, arr) << ";\n";
     } else {
       std::string cond;
       int lead = (int)sp.OUT.size() - (int)on.shape.size();
@@ -1044,11 +1050,14 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
         if (!cond.empty()) cond += " && ";
         cond += "(" + it[d].at() + " == 0)";
       }
-      em.body << "        if (" << (cond.empty() ? "true" : cond) << ") st1(" << P << " + " << off.at() << ", " << v
-              << ");\n";
+      em.body << "        if (" << (cond.empty() ? "true" : cond) << ") " << out_store(g, o, P, off.at(), 0, v) << ";\n";
     }
   }
   std::ostringstream s;
+  if (hoisted)
+    *hoisted += em.inv.str();
+  else
+    s << em.inv.str();
   if (rows <= 0) rows = sp.BM;
   s << "  for (int s_ = tid; s_ < " << rows * (cols / VE) << "; s_ += " << sp.NT << ") {\n";
   s << "    const int mlc = s_ / " << cols / VE << ", ml = " << row0 << " + mlc, nl = (s_ % " << cols / VE << ") * " << VE

@@ -210,11 +210,11 @@ static std::string row_epilogue(const KInfo& ki, const GemmSpec& sp, const std::
         if (o == mm)
           stores << "    float _mmv" << j << "[" << VEC << "];\n#pragma unroll\n    for (int e = 0; e < " << VEC
                  << "; ++e) _mmv" << j << "[e] = Cs[mlc * " << sp.LDC << " + cb" << j << " + e];\n";
-        stores << "    if (rv" << (gd.empty() ? "" : " && " + gd) << ") stv<" << VEC << ">(" << P << " + row * " << L
-               << "LL + cb" << j << ", " << src << ");\n";
+        stores << "    if (rv" << (gd.empty() ? "" : " && " + gd) << ") "
+               << out_store(g, o, P, "row * " + std::to_string(L) + "LL + cb" + std::to_string(j), VEC, src) << ";\n";
       }
     } else {
-      stores << "    if (rv && lane == 0) st1(" << P << " + row, s" << o << ");\n";
+      stores << "    if (rv && lane == 0) " << out_store(g, o, P, "row", 0, "s" + std::to_string(o)) << ";\n";
     }
   }
   std::ostringstream s;
@@ -370,8 +370,10 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
     const Node& rn = g.nodes[r];
     if (!has(ki.k.outs, r)) continue;
     std::string val = rn.op == KORCH_REDUCE_MEAN ? "side_s[tid] / " + flit((double)sp.K) : "side_s[tid]";
-    s << "  if (tid < " << sp.BM << " && m0 + tid < " << sp.M << "LL) st1((" << ctype(rn.dtype) << "*)a.p["
-      << ki.out_slot(r) << "] + bz * " << sp.M << "LL + m0 + tid, " << val << ");\n";
+    s << "  if (tid < " << sp.BM << " && m0 + tid < " << sp.M << "LL) "
+      << out_store(g, r, "((" + ctype(rn.dtype) + "*)a.p[" + std::to_string(ki.out_slot(r)) + "])",
+                   "bz * " + std::to_string(sp.M) + "LL + m0 + tid", 0, val)
+      << ";\n";
   }
   bool any_tile_out = false;
   for (int o : ki.k.outs)

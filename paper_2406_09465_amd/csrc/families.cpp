@@ -145,7 +145,7 @@ GenKernel gen_pointwise(const KInfo& ki, int index) {
       std::string arr = "o" + std::to_string(o);
       decl << "  float " << arr << "[" << vec << "];\n";
       em.body << "    " << arr << "[e] = " << v << ";\n";
-      after << "  stv<" << vec << ">(" << P << " + t * " << vec << ", " << arr << ");\n";
+      after << "  " << out_store(g, o, P, "t * " + std::to_string(vec), vec, arr) << ";\n";
     } else {
       auto st = strides_of(os);
       Ix off = Ix::k(0);
@@ -158,8 +158,7 @@ GenKernel gen_pointwise(const KInfo& ki, int index) {
         if (!cond.empty()) cond += " && ";
         cond += "(" + it[d].at() + " == 0)";
       }
-      em.body << "    if (" << (cond.empty() ? "true" : cond) << ") st1(" << P << " + " << off.at() << ", " << v
-              << ");\n";
+      em.body << "    if (" << (cond.empty() ? "true" : cond) << ") " << out_store(g, o, P, off.at(), 0, v) << ";\n";
     }
   }
   std::ostringstream s;
@@ -444,11 +443,13 @@ GenKernel gen_row(const KInfo& ki, int index) {
     if (cls[o] == FULL) {
       for (int j = 0; j < NC; ++j) {
         std::string gd = chunk_guard(j);
-        stores << "  if (rv" << (gd.empty() ? "" : " && " + gd) << ") stv<" << VEC << ">(" << P << " + row * "
-               << rs.L << "LL + cb" << j << ", v" << o << "[" << j << "]);\n";
+        stores << "  if (rv" << (gd.empty() ? "" : " && " + gd) << ") "
+               << out_store(g, o, P, "row * " + std::to_string(rs.L) + "LL + cb" + std::to_string(j), VEC,
+                            "v" + std::to_string(o) + "[" + std::to_string(j) + "]")
+               << ";\n";
       }
     } else {
-      stores << "  if (rv && lane == 0) st1(" << P << " + row, s" << o << ");\n";
+      stores << "  if (rv && lane == 0) " << out_store(g, o, P, "row", 0, "s" + std::to_string(o)) << ";\n";
     }
   }
   std::ostringstream s;
@@ -595,10 +596,11 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
         std::string arr = "_po" + std::to_string(o);
         pdecl << "    float " << arr << "[" << VB << "];\n";
         pe.body << "      " << arr << "[e] = " << v << ";\n";
-        pafter << "    if (bv) stv<" << VB << ">((" << T << "*)a.p[" << ki.out_slot(o) << "] + " << off.b << ", " << arr
-               << ");\n";
+        pafter << "    if (bv) "
+               << out_store(g, o, "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.b, VB, arr) << ";\n";
       } else {
-        pe.body << "      if (bv) st1((" << T << "*)a.p[" << ki.out_slot(o) << "] + " << off.at() << ", " << v << ");\n";
+        pe.body << "      if (bv) "
+                << out_store(g, o, "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.at(), 0, v) << ";\n";
       }
     }
   for (int o : ki.k.outs) {
@@ -609,8 +611,9 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     auto strd = strides_of(on.shape);
     Ix off = Ix::k(0);
     for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], strd[d], VB));
-    ee.body << "        st1((" << ctype(on.dtype) << "*)a.p[" << ki.out_slot(o) << "] + " << off.at() << ", " << v
-            << ");\n";
+    ee.body << "        "
+            << out_store(g, o, "((" + ctype(on.dtype) + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.at(), 0, v)
+            << ";\n";
   }
   int scr_slot = -1, cnt_slot = -1;
   if (SPLIT > 1) {

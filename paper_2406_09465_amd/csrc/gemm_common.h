@@ -70,9 +70,14 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook = "", int6
 // BM) starting at tile row `row0`.  conv_tw > 0: the tile is a 2-D block of
 // output pixels conv_tw wide whose origin is (ty0, tx0), and C tile row ml
 // holds pixel (ml / conv_tw, ml % conv_tw).
+// Loads that are the same for every element a thread visits (per-column
+// vectors such as a BatchNorm scale, when the workgroup's thread count is a
+// multiple of the column vectors of a row) are issued once before the element
+// loop; with `hoisted` set they are returned there instead, for the caller to
+// place before a loop over several tiles of the same columns.
 std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
                           const std::string& cs_row, const std::set<int>& skip = {}, int conv_tw = 0,
-                          int rows = 0, const std::string& row0 = "0");
+                          int rows = 0, const std::string& row0 = "0", std::string* hoisted = nullptr);
 // Direct convolution (stride 1, half precision, input halo tile in LDS,
 // weights in registers); conv_direct_fits says whether it applies.
 bool conv_direct_fits(const GemmSpec& sp, std::string* why);
