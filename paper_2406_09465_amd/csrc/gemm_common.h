@@ -44,6 +44,10 @@ struct GemmSpec {
   int BSH = 0;
   // Rows of the fp32 C tile staged in LDS at once for the epilogue (0 = BM).
   int CROWS = 0;
+  // Scheduling hints for the unrolled main loop (both operands staged by
+  // branch-free buffer loads): LDS writes and global loads per thread and
+  // k-tile; 0 leaves the instruction order to the compiler.
+  int sched_w = 0, sched_g = 0;
 };
 
 // LDS element offset of row k of the [k][n] right-operand tile.
