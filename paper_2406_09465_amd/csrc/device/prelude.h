@@ -126,15 +126,19 @@ template <typename T> __device__ __forceinline__ void st1_out(T* base, i64 off, 
 }
 
 // ---- elementwise functions (fp32) -----------------------------------------
-__device__ __forceinline__ float k_relu(float x) { return x > 0.0f ? x : 0.0f; }
+// max / min / ReLU are the single-instruction v_max_f32 / v_min_f32 (a
+// compare and a select would take two, with the compare's mask in scalar
+// registers); they agree with the comparison forms on every non-NaN input
+// (up to the sign of a zero result).
+__device__ __forceinline__ float k_relu(float x) { return __builtin_fmaxf(x, 0.0f); }
 __device__ __forceinline__ float k_rsqrt(float x) { return 1.0f / sqrtf(x); }
 __device__ __forceinline__ float k_gelu_tanh(float x) {
   // 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))
   const float c = 0.7978845608028654f;
   return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
 }
-__device__ __forceinline__ float k_max(float a, float b) { return a > b ? a : b; }
-__device__ __forceinline__ float k_min(float a, float b) { return a < b ? a : b; }
+__device__ __forceinline__ float k_max(float a, float b) { return __builtin_fmaxf(a, b); }
+__device__ __forceinline__ float k_min(float a, float b) { return __builtin_fminf(a, b); }
 
 // Mish written as x * n / (n + 2) with n = e^x (e^x + 2), which equals
 // x * tanh(log(1 + e^x)) exactly.  For x >= 20 the quotient rounds to 1 in

@@ -140,6 +140,16 @@ static bool analyze_attention(const KInfo& ki, AttnSpec& a, std::string* why) {
 }
 
 // LDS bytes of the kernel: all keys, all values and one score tile per wave.
+// Keys and values read from the same stored tensor with the same [key][dim]
+// geometry (attention whose keys and values are one projection, as in
+// spatial-reduction attention) are staged into LDS once and read as both.
+static bool kv_shared(const AttnSpec& a) {
+  bool f32 = a.dtype == KORCH_F32;
+  int kstep = f32 ? 4 : 32;
+  int64_t dpad = (a.d + kstep - 1) / kstep * kstep, dvp = (a.dv + 15) / 16 * 16;
+  return a.kx == a.v && !a.k_is_kt && a.d == a.dv && dpad == dvp && !getenv("KORCH_ATTN_NO_KV_SHARE");
+}
+
 static size_t attention_lds_bytes(const AttnSpec& a) {
   bool f32 = a.dtype == KORCH_F32;
   int kstep = f32 ? 4 : 32;
@@ -148,7 +158,7 @@ static size_t attention_lds_bytes(const AttnSpec& a) {
   int64_t KSP = dpad + (f32 ? 4 : 8), NKP = nkp + (f32 ? 4 : 8);
   int64_t dvp = (a.dv + 15) / 16 * 16, VP = dvp + (f32 ? 4 : 8);
   size_t ks = (size_t)(nkp * KSP * dtype_bytes(a.dtype));
-  size_t v = (size_t)(nkp * VP * dtype_bytes(a.dtype));
+  size_t v = kv_shared(a) ? 0 : (size_t)(nkp * VP * dtype_bytes(a.dtype));
   return ks + v + (size_t)(4 * 16 * NKP * dtype_bytes(a.dtype));
 }
 
@@ -183,7 +193,8 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   int VP = (int)dvp + (f32 ? 4 : 8);                  // V row pitch ([key][dim] in LDS)
   int NF = (int)(nkp / 16), OF = (int)(dvp / 16);
   size_t ks_bytes = (size_t)nkp * KSP * dtype_bytes(a.dtype);
-  size_t v_bytes = (size_t)nkp * VP * dtype_bytes(a.dtype);
+  const bool shareKV = kv_shared(a);  // then VP == KSP and Vs aliases Ks
+  size_t v_bytes = shareKV ? 0 : (size_t)nkp * VP * dtype_bytes(a.dtype);
   size_t p_bytes = (size_t)4 * 16 * NKP * dtype_bytes(a.dtype);
   size_t smem = ks_bytes + v_bytes + p_bytes;
   if (smem != attention_lds_bytes(a) || smem > 160 * 1024)
@@ -209,7 +220,10 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
   s << "  __shared__ __attribute__((aligned(16))) char smem[" << smem << "];\n";
   s << "  " << T << "* Ks = (" << T << "*)smem;\n";
-  s << "  " << T << "* Vs = (" << T << "*)(smem + " << ks_bytes << ");\n";
+  if (shareKV)
+    s << "  " << T << "* Vs = Ks;  // keys and values are one tensor\n";
+  else
+    s << "  " << T << "* Vs = (" << T << "*)(smem + " << ks_bytes << ");\n";
   s << "  " << T << "* Ps = (" << T << "*)(smem + " << ks_bytes + v_bytes << ");\n";
   s << "  const int tid = threadIdx.x, l = tid & 63, wave = tid >> 6;\n";
   s << "  const i64 bz = blockIdx.y;\n";
@@ -236,9 +250,9 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   }
   const bool vecK = !a.k_is_kt && a.d % VL == 0 && dpad % VL == 0;
   const bool vecV = a.dv % VL == 0 && dvp % VL == 0;
-  const int64_t NIK = (nkp * dpad / VL + 255) / 256, NIV = (nkp * dvp / VL + 255) / 256;
+  const int64_t NIK = (nkp * dpad / VL + 255) / 256, NIV = shareKV ? 0 : (nkp * dvp / VL + 255) / 256;
   if (vecK && vecV && NIK + NIV <= 24) {
-    s << "  " << VT << " kx_[" << NIK << "], vx_[" << NIV << "];\n";
+    s << "  " << VT << " kx_[" << NIK << "], vx_[" << std::max<int64_t>(NIV, 1) << "];\n";
     s << "#pragma unroll\n  for (int j = 0; j < " << NIK << "; ++j) {\n";
     s << "    const int i = tid + j * 256, key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
     s << "    kx_[j] = " << VT << "{};\n";
@@ -274,7 +288,9 @@ GenKernel gen_attention(const KInfo& ki, int index) {
           << "[koff + (i64)key * " << a.d << " + dim] : fromf<" << T << ">(0.0f);\n";
       s << "  }\n";
     }
-    if (vecV) {
+    if (shareKV) {
+      // the values are the keys already staged
+    } else if (vecV) {
       s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dvp / VL << "; i += 256) {\n";
       s << "    const int key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
       s << "    " << VT << " x_ = {};\n";
@@ -298,6 +314,28 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     else
       chain_expr = binary_expr(cn.op, chain_expr, flit(cn.attrs.scalar));
   }
+  // A score chain that only scales by a positive constant c (the 1/sqrt(d) of
+  // attention) commutes with the row maximum, so half-precision kernels take
+  // the maximum of the raw scores and evaluate exp(c (x - max)) as one base-2
+  // exponential of fma(x, c log2 e, -max c log2 e).
+  double fold_c = 0.0;
+  if (fast_math() && a.chain.size() == 1) {
+    const Node& cn = g.nodes[a.chain[0]];
+    if (cn.op == KORCH_MUL && cn.attrs.scalar > 0.0) fold_c = cn.attrs.scalar;
+    if (cn.op == KORCH_DIV && cn.attrs.scalar > 0.0) fold_c = 1.0 / cn.attrs.scalar;
+  }
+  const std::string CL = flit(fold_c * 1.4426950408889634);
+  const std::string score_expr = fold_c > 0.0 ? std::string("x") : chain_expr;
+  // exponentials of one row block after the maxima: sc[f][i] and sm[i]
+  auto exp_stmt = [&]() {
+    if (fold_c > 0.0)
+      return std::string("    sc[f][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[f][i], ") + CL + ", mcl[i]));\n";
+    return "    sc[f][i] = " + unary_expr(KORCH_EXP, "(sc[f][i] - mx[i])") + ";\n";
+  };
+  auto mcl_stmt = [&]() {
+    if (fold_c <= 0.0) return std::string();
+    return "  float mcl[4];\n#pragma unroll\n  for (int i = 0; i < 4; ++i) mcl[i] = -mx[i] * " + CL + ";\n";
+  };
   if (ksplit) {
     const int NFW = (int)(NKW / 16);
     s << "  const i64 q0 = (i64)blockIdx.x * 16;\n";
@@ -325,7 +363,7 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     s << "  float* red = (float*)(smem + " << red_off << ");  // [2][wave][16 rows]\n";
     s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = -__builtin_huge_valf();\n";
     s << "#pragma unroll\n  for (int f = 0; f < " << NFW << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
-    s << "    const float x = sc[f][i];\n    sc[f][i] = " << chain_expr << ";\n";
+    s << "    const float x = sc[f][i];\n    sc[f][i] = " << score_expr << ";\n";
     if (nkp != a.nk) s << "    if (kb + f * 16 + (l & 15) >= " << a.nk << ") sc[f][i] = -__builtin_huge_valf();\n";
     s << "    mx[i] = k_max(mx[i], sc[f][i]);\n  }\n";
     s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = group_max<16>(mx[i]);\n";
@@ -333,8 +371,9 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     s << "  __syncthreads();\n";
     s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n    const int r = (l >> 4) * 4 + i;\n";
     s << "    mx[i] = k_max(k_max(red[r], red[16 + r]), k_max(red[32 + r], red[48 + r]));\n    sm[i] = 0.0f;\n  }\n";
+    s << mcl_stmt();
     s << "#pragma unroll\n  for (int f = 0; f < " << NFW << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
-    s << "    sc[f][i] = " << unary_expr(KORCH_EXP, "(sc[f][i] - mx[i])") << ";\n    sm[i] += sc[f][i];\n  }\n";
+    s << exp_stmt() << "    sm[i] += sc[f][i];\n  }\n";
     s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = group_sum<16>(sm[i]);\n";
     s << "  if ((l & 15) == 0) {\n#pragma unroll\n    for (int i = 0; i < 4; ++i) red[64 + wave * 16 + (l >> 4) * 4 + i] = sm[i];\n  }\n";
     s << "  __syncthreads();\n";
@@ -403,13 +442,14 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   s << "  float mx[4], sm[4];\n";
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = -__builtin_huge_valf();\n";
   s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
-  s << "    const float x = sc[f][i];\n    sc[f][i] = " << chain_expr << ";\n";
+  s << "    const float x = sc[f][i];\n    sc[f][i] = " << score_expr << ";\n";
   if (nkp != a.nk) s << "    if (f * 16 + (l & 15) >= " << a.nk << ") sc[f][i] = -__builtin_huge_valf();\n";
   s << "    mx[i] = k_max(mx[i], sc[f][i]);\n  }\n";
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) mx[i] = group_max<16>(mx[i]);\n";
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = 0.0f;\n";
+  s << mcl_stmt();
   s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) {\n";
-  s << "    sc[f][i] = " << unary_expr(KORCH_EXP, "(sc[f][i] - mx[i])") << ";\n    sm[i] += sc[f][i];\n  }\n";
+  s << exp_stmt() << "    sm[i] += sc[f][i];\n  }\n";
   s << "#pragma unroll\n  for (int i = 0; i < 4; ++i) sm[i] = group_sum<16>(sm[i]);\n";
   s << "  " << T << "* Pw = Ps + wave * " << 16 * NKP << ";\n";
   s << "#pragma unroll\n  for (int f = 0; f < " << NF << "; ++f)\n#pragma unroll\n  for (int i = 0; i < 4; ++i) Pw[((l >> 4) * 4 + i) * "
