@@ -274,6 +274,23 @@ def main():
               "copy_us": round(per_launch_us(lambda: cdst.copy_(csrc)), 3), "copy_bytes_moved": 2 * csrc.numel()}
     del one, csrc, cdst
 
+    # context: the unfused plan of the same primitive graph (one kernel per
+    # primitive, contiguous reshapes as views), same inputs, back to back
+    ru = PlanRunner(graphs.build(args.workload), "unfused")
+    ru.set_inputs(W.inputs(args.workload))
+    for _ in range(5):
+        ru.launch()
+    ru.bind(stream)
+    n_unf = max(20, args.steps // 2)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(n_unf):
+        ru.launch_bound()
+    torch.cuda.synchronize()
+    unfused = {"us_per_step": round((time.perf_counter() - t1) * 1e6 / n_unf, 3),
+               "kernels": ru.plan.num_kernels(), "steps": n_unf}
+    del ru
+
     kernels = []
     for k in range(nk):
         f, b, fl = r.plan.kernel_info(k)
@@ -296,6 +313,7 @@ def main():
         "config": {"workload": DESCR[args.workload], "plan": "recorded" if args.kernels_json else args.plan,
                    "kernels": nk},
         "roofline": roof,
+        "unfused": unfused,
         "floors": floors,
         "kernels": kernels,
     }

@@ -163,9 +163,11 @@ __device__ __forceinline__ float f_rsqrt(float x) { return __builtin_amdgcn_rsqf
 // -2 sqrt(2/pi) / ln(2) * x (1 + 0.044715 x^2) and one reciprocal.  Large |x|
 // saturate to x and -0.
 __device__ __forceinline__ float f_gelu_tanh(float x) {
+  // k x (1 + 0.044715 x^2) = x * fma(x^2, 0.044715 k, k): five VALU operations
+  // and two transcendentals per element
   const float k = -2.302208198144325f;
-  const float t = x * __builtin_fmaf(0.044715f * x, x, 1.0f);
-  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(k * t));
+  const float t = x * __builtin_fmaf(x * x, 0.044715f * k, k);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(t));
 }
 __device__ __forceinline__ float f_mish(float x) {
   float ex = f_exp(k_min(x, 20.0f));
