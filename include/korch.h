@@ -215,7 +215,9 @@ int korch_kernel_source(const korch_graph* g, const korch_kernel_desc* k, char* 
    does not depend on the graph's lifetime. */
 int korch_plan_create(const korch_graph* g, int32_t n_kernels, const korch_kernel_desc* kernels, korch_plan** p);
 /* The unfused plan: one kernel per primitive, except reshapes of materialized
-   tensors, which are views and need no kernel. */
+   tensors, which are views and need no kernel.  Its kernel symbols are
+   korch_u<k>_<family> (a plan from korch_plan_create uses korch_k<k>_<family>),
+   so profiles of a run that executes both plans keep them apart. */
 int korch_plan_unfused(const korch_graph* g, korch_plan** p);
 void korch_plan_destroy(korch_plan* p);
 int korch_plan_num_kernels(const korch_plan* p, int32_t* n);

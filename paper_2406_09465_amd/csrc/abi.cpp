@@ -363,6 +363,7 @@ int korch_plan_unfused(const korch_graph* g, korch_plan** p) {
     auto* q = new korch_plan();
     q->p.g = g->g;
     q->p.kernels = ks;
+    q->p.name_prefix = "korch_u";
     *p = q;
   });
 }
