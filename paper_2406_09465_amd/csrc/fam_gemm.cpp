@@ -243,12 +243,15 @@ void choose_tiles(GemmSpec& sp, bool split) {
     // re-reading its operand panels (proportional to 1/BM + 1/BN).  192-wide
     // tiles (half precision, k-tiles of 32 so that two workgroups still share
     // a compute unit's LDS) serve products whose 128-wide tiles would leave a
-    // half-filled last round.
+    // half-filled last round.  256 x 192 tiles (half precision, eight waves of
+    // 64 x 96, k-tiles of 64, one workgroup per compute unit) re-read the
+    // operand panels least; they are taken when they fill whole rounds.
     double best = 1e300;
-    for (int bm : {128, 64}) {
+    for (int bm : {128, 64, 256}) {
       for (int bn : {128, 96, 64, 192}) {
         if (bn == 96 && sp.N % 96 != 0) continue;
-        if (bn == 192 && (sp.N % 192 != 0 || f32 || bm != 128)) continue;
+        if (bn == 192 && (sp.N % 192 != 0 || f32 || bm == 64)) continue;
+        if (bm == 256 && (bn != 192 || (sp.M + 255) / 256 * (sp.N / 192) * sp.batch < 256)) continue;
         int64_t tiles = (sp.M + bm - 1) / bm * ((sp.N + bn - 1) / bn) * sp.batch;
         double rounds = (double)((tiles + 255) / 256);
         double cost = rounds * bm * bn * (1.0 + 24.0 * (1.0 / bm + 1.0 / bn));
@@ -259,7 +262,7 @@ void choose_tiles(GemmSpec& sp, bool split) {
         }
       }
     }
-    if (sp.BN == 192) sp.BK = std::min(sp.BK, 32);
+    if (sp.BN == 192 && sp.BM != 256) sp.BK = std::min(sp.BK, 32);
   } else if (!split) {
     int64_t tiles = (sp.M + 127) / 128 * ((sp.N + sp.BN - 1) / sp.BN) * sp.batch;
     if (tiles < 240 && sp.M > 64) sp.BM = 64;
@@ -280,6 +283,11 @@ void choose_tiles(GemmSpec& sp, bool split) {
   }
   if (sp.BM / sp.WM < 16) sp.WM = std::max(1, sp.BM / 16);
   sp.NT = 256;
+  if (sp.BM == 256) {
+    sp.WM = 4;
+    sp.WN = 2;
+    sp.NT = 512;
+  }
   sp.NS = 2;
   if (const char* e = getenv("KORCH_GEMM_NS")) sp.NS = std::max(2, std::min(8, atoi(e)));
   // Explicit tile override "BM,BN,BK,WM,WN" (tile-configuration sweeps of the

@@ -51,6 +51,11 @@ GEMM_CASES = [
 # and a ragged contraction (176 = 5.5 k-tiles of 32).
 WIDE_TILE_CASE = dict(m=4000, d=176, h=1536)
 
+# An MLP block whose first product takes 256 x 192 tiles of eight waves
+# (16 x 16 = 256 tiles): ragged rows (4000 = 15.6 row tiles) and a ragged
+# contraction (720 = 11.25 k-tiles of 64).
+BIG_TILE_CASE = dict(m=4000, d=720, h=3072)
+
 # Attention shapes of the attention-kernel GPU tests (few query rows: the keys
 # are split over the waves; fp32 and fp16, padded keys), each run with the key
 # split and without it (KORCH_ATTN_NO_KEY_SPLIT=1).
@@ -87,6 +92,7 @@ def _jobs():
         for flag in ("", "1"):
             jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_NO_KSPLIT", flag)))
     jobs.append(("plans", "mlp", WIDE_TILE_CASE, None))
+    jobs.append(("plans", "mlp", BIG_TILE_CASE, None))
     for wl, sz in ATTN_CASES:
         for flag in ("", "1"):
             jobs.append(("env_plans", wl, sz, ("KORCH_ATTN_NO_KEY_SPLIT", flag)))

@@ -346,12 +346,13 @@ def test_gemm_k_split_selection():
 
 
 def test_gemm_wide_tile_selection():
-    """GEMM1 of the MLP block (4096 x 3072 output) takes 128 x 192 tiles with
-    k-tiles of 32: 512 tiles, two per compute unit in one round, where 128 x 128
-    tiles would leave a half-filled second round.  The ragged 4000 x 1536 shape
-    of the GPU test takes them too (32 x 8 tiles); a hidden width that 192 does
-    not divide keeps narrower tiles."""
-    from paper_2406_09465_amd.warm import WIDE_TILE_CASE
+    """GEMM1 of the MLP block (4096 x 3072 output) takes 256 x 192 tiles of
+    eight waves with k-tiles of 64: 256 tiles, one per compute unit, re-reading
+    the operand panels least.  The ragged 4000 x 3072 shape of the GPU test
+    takes them too (16 x 16 tiles); 4000 x 1536 (too few 256-row tiles for a
+    round) takes 128 x 192 tiles with k-tiles of 32 (32 x 8 tiles); a hidden
+    width that 192 does not divide keeps narrower tiles."""
+    from paper_2406_09465_amd.warm import BIG_TILE_CASE, WIDE_TILE_CASE
 
     def gemm1(sizes):
         p = graphs.build("mlp", **sizes).plan("layered")
@@ -359,10 +360,13 @@ def test_gemm_wide_tile_selection():
         return p.kernel_launch(1), p.kernel_source(1)
 
     (grid, block, _), src = gemm1({})
-    assert grid == (512, 1, 1) and block == (256, 1, 1)
+    assert grid == (256, 1, 1) and block == (512, 1, 1)
+    assert "* 72 + " in src  # A tile rows of 64 + 8 halves (k-tiles of 64)
+    (grid, block, _), _ = gemm1(BIG_TILE_CASE)
+    assert grid == (16 * 16, 1, 1) and block == (512, 1, 1)
+    (grid, block, _), src = gemm1(WIDE_TILE_CASE)
+    assert grid == (32 * 8, 1, 1) and block == (256, 1, 1)
     assert "* 40 + " in src  # A tile rows of 32 + 8 halves (k-tiles of 32)
-    (grid, _, _), _ = gemm1(WIDE_TILE_CASE)
-    assert grid == (32 * 8, 1, 1)
     (grid, _, _), _ = gemm1(dict(m=500, d=256, h=1056))
     assert grid[0] != 4 * 1056 // 192
 

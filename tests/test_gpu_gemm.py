@@ -43,12 +43,15 @@ def test_gemm_k_split(sizes, plan, no_split, monkeypatch):
 
 
 @pytest.mark.parametrize("plan", ["layered", "fused"])
-def test_gemm_wide_tiles(plan):
-    """128 x 192 tiles with k-tiles of 32 (ragged rows and contraction)."""
+@pytest.mark.parametrize("case", ["wide", "big"])
+def test_gemm_wide_tiles(plan, case):
+    """128 x 192 tiles with k-tiles of 32, and 256 x 192 tiles of eight waves
+    with k-tiles of 64 (ragged rows and contraction in both)."""
     from paper_2406_09465_amd import graphs
     from paper_2406_09465_amd.runner import PlanRunner
-    from paper_2406_09465_amd.warm import WIDE_TILE_CASE as sizes
-    print(f"\n[case] mlp {sizes} {plan} wide tiles", flush=True)
+    from paper_2406_09465_amd.warm import BIG_TILE_CASE, WIDE_TILE_CASE
+    sizes = WIDE_TILE_CASE if case == "wide" else BIG_TILE_CASE
+    print(f"\n[case] mlp {sizes} {plan} {case} tiles", flush=True)
     w = graphs.build("mlp", **sizes)
     raw, ref = reference("mlp", sizes)
     out = PlanRunner(w, plan).run(raw)
