@@ -273,7 +273,11 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   gk.args.push_back(scr);
   ArgRef cnt;
   cnt.kind = ArgRef::Counter;
-  cnt.bytes = (size_t)base * 4;
+  // Each tile's arrival counter sits on a 128-byte line of its own: device-scope
+  // atomics on one line are performed one after another at the point of
+  // coherence, and counters packed four bytes apart put every workgroup of the
+  // kernel in one queue.
+  cnt.bytes = (size_t)base * 128;
   int cnt_slot = (int)gk.args.size();
   gk.args.push_back(cnt);
   std::string T = ctype(sp.mtype);
@@ -340,9 +344,9 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are performed\n";
   s << "  __syncthreads();\n";
   s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
-  s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
+  s << "    const int old = __hip_atomic_fetch_add(cnt + tix * 32, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
   s << "    last_ = (old == " << S - 1 << ");\n";
-  s << "    if (last_) __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
+  s << "    if (last_) __hip_atomic_store(cnt + tix * 32, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
   s << "  __syncthreads();\n  if (!last_) return;\n";
   // deterministic sum of the partials, split 0 first
   if (vec4) {

@@ -624,7 +624,7 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     gk.args.push_back(scr);
     ArgRef cnt;
     cnt.kind = ArgRef::Counter;
-    cnt.bytes = (size_t)(A * ctiles) * 4;
+    cnt.bytes = (size_t)(A * ctiles) * 128;  // one 128-byte line per counter
     cnt_slot = (int)gk.args.size();
     gk.args.push_back(cnt);
   }
@@ -673,9 +673,9 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     s << "  __syncthreads();\n";
     s << "  const i64 tix = ay * " << ctiles << " + blockIdx.x;\n";
     s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
-    s << "    const int old = __hip_atomic_fetch_add(cnt + tix, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
+    s << "    const int old = __hip_atomic_fetch_add(cnt + tix * 32, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
     s << "    last_ = (old == " << SPLIT - 1 << ");\n";
-    s << "    if (last_) __hip_atomic_store(cnt + tix, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
+    s << "    if (last_) __hip_atomic_store(cnt + tix * 32, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
     s << "  __syncthreads();\n  if (!last_) return;\n";
     // every thread of the last workgroup sums a group of splits for one column
     // of the tile; the groups are then combined in order (deterministic)
