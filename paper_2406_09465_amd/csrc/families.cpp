@@ -624,7 +624,9 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     gk.args.push_back(scr);
     ArgRef cnt;
     cnt.kind = ArgRef::Counter;
-    cnt.bytes = (size_t)(A * ctiles) * 128;  // one 128-byte line per counter
+    // one 128-byte line per counter; with more than 32 splits a tile has a
+    // counter per group of 16 splits and one for the groups
+    cnt.bytes = (size_t)(A * ctiles) * (SPLIT > 32 ? (SPLIT + 15) / 16 + 1 : 1) * 128;
     cnt_slot = (int)gk.args.size();
     gk.args.push_back(cnt);
   }
@@ -673,9 +675,25 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     s << "  __syncthreads();\n";
     s << "  const i64 tix = ay * " << ctiles << " + blockIdx.x;\n";
     s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
-    s << "    const int old = __hip_atomic_fetch_add(cnt + tix * 32, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
-    s << "    last_ = (old == " << SPLIT - 1 << ");\n";
-    s << "    if (last_) __hip_atomic_store(cnt + tix * 32, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
+    if (SPLIT > 32) {
+      // Two-level arrival: atomics on one line are performed one after another,
+      // so the splits count in per group of 16 and the last of each group counts
+      // the group in; every split's partials are performed before its first
+      // increment, hence before the final one is observed.
+      const int64_t NG = (SPLIT + 15) / 16;
+      s << "    const int grp_ = blockIdx.z / 16, gsz_ = " << SPLIT << " - grp_ * 16 < 16 ? " << SPLIT << " - grp_ * 16 : 16;\n";
+      s << "    int* c1 = cnt + (tix * " << NG + 1 << " + 1 + grp_) * 32;\n";
+      s << "    int* c2 = cnt + tix * " << (NG + 1) * 32 << ";\n";
+      s << "    last_ = false;\n";
+      s << "    if (__hip_atomic_fetch_add(c1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gsz_ - 1) {\n";
+      s << "      __hip_atomic_store(c1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
+      s << "      last_ = __hip_atomic_fetch_add(c2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == " << NG - 1 << ";\n";
+      s << "      if (last_) __hip_atomic_store(c2, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n    }\n  }\n";
+    } else {
+      s << "    const int old = __hip_atomic_fetch_add(cnt + tix * 32, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
+      s << "    last_ = (old == " << SPLIT - 1 << ");\n";
+      s << "    if (last_) __hip_atomic_store(cnt + tix * 32, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
+    }
     s << "  __syncthreads();\n  if (!last_) return;\n";
     // every thread of the last workgroup sums a group of splits for one column
     // of the tile; the groups are then combined in order (deterministic)
