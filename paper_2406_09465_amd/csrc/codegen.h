@@ -144,8 +144,8 @@ std::string source_header(int nargs);
 // `src` (V = 0: the one float value `src`) at element offset `off` of its
 // storage `P` (a uniform base pointer): written
 // through to the device's point of coherence (`stv_out` / `st1_out`) unless the
-// tensor is 2 GiB or larger.
+// tensor is 2 GiB or larger or `plain` asks for ordinary stores.
 std::string out_store(const Graph& g, int node, const std::string& P, const std::string& off, int V,
-                      const std::string& src);
+                      const std::string& src, bool plain = false);
 
 }  // namespace korch

@@ -316,10 +316,10 @@ static bool uses_var(const std::string& e, const std::string& v) {
 }
 
 std::string out_store(const Graph& g, int node, const std::string& P, const std::string& off, int V,
-                      const std::string& src) {
+                      const std::string& src, bool plain_store) {
   const Node& n = g.nodes[node];
   static const bool plain = getenv("KORCH_OUT_PLAIN") && atoi(getenv("KORCH_OUT_PLAIN")) != 0;  // ablation switch
-  const bool big = plain || (double)numel(n.shape) * dtype_bytes(n.dtype) >= 2147483648.0;
+  const bool big = plain || plain_store || (double)numel(n.shape) * dtype_bytes(n.dtype) >= 2147483648.0;
   if (V == 0) return big ? "st1(" + P + " + " + off + ", " + src + ")" : "st1_out(" + P + ", " + off + ", " + src + ")";
   const std::string v = std::to_string(V);
   return big ? "stv<" + v + ">(" + P + " + " + off + ", " + src + ")" : "stv_out<" + v + ">(" + P + ", " + off + ", " + src + ")";

@@ -596,11 +596,16 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
         std::string arr = "_po" + std::to_string(o);
         pdecl << "    float " << arr << "[" << VB << "];\n";
         pe.body << "      " << arr << "[e] = " << v << ";\n";
+        // prologue values (the operand's shape, e.g. centered inputs) use plain
+        // stores: measured 0.4 us faster for instnorm's variance kernel than the
+        // write-through policy of the other outputs
         pafter << "    if (bv) "
-               << out_store(g, o, "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.b, VB, arr) << ";\n";
+               << out_store(g, o, "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.b, VB, arr, true)
+               << ";\n";
       } else {
         pe.body << "      if (bv) "
-                << out_store(g, o, "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.at(), 0, v) << ";\n";
+                << out_store(g, o, "((" + T + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.at(), 0, v, true)
+                << ";\n";
       }
     }
   for (int o : ki.k.outs) {
