@@ -343,3 +343,70 @@ def test_instnorm_shift_invariance():
     assert np.allclose(a, b, rtol=1e-12, atol=1e-12)
     c = _instnorm(2.0 * x, gamma, beta, eps=4e-5)
     assert np.allclose(a, c, rtol=1e-12, atol=1e-12)
+
+
+def _sra_direct(x, wsr, gamma, beta, r, eps=1e-5):
+    """Spatial-reduction attention written out from its definition, with no
+    primitive graph: patch matrix by loops in (ky, kx, c) order, the patch-merge
+    product, biased LayerNorm with eps inside the square root, K = V = that
+    result, scores scaled by 1/sqrt(c), SciPy's row softmax, then P V."""
+    from scipy.special import softmax
+    hh, ww, c = x.shape
+    ph, pw = hh // r, ww // r
+    a = np.zeros((ph * pw, r * r * c))
+    for py in range(ph):
+        for px in range(pw):
+            for ky in range(r):
+                for kx in range(r):
+                    for ch in range(c):
+                        a[py * pw + px, (ky * r + kx) * c + ch] = x[py * r + ky, px * r + kx, ch]
+    kvp = a @ wsr
+    kv = (kvp - kvp.mean(axis=1, keepdims=True)) / np.sqrt(kvp.var(axis=1, keepdims=True) + eps) * gamma + beta
+    q = np.array([[x[i, j, ch] for ch in range(c)] for i in range(hh) for j in range(ww)])
+    p = softmax(q @ kv.T / math.sqrt(c), axis=1)
+    return p @ kv
+
+
+@pytest.mark.parametrize("hh,ww,c,r", [(16, 16, 8, 2), (16, 24, 4, 4)])
+def test_sra_graph_against_direct_formula(hh, ww, c, r):
+    """The whole spatial-reduction attention graph (patch extraction, patch
+    merge, fissioned LayerNorm, scaled scores, fissioned softmax, P KV) equals
+    the attention formula computed directly, so a wrong permutation, scale,
+    eps placement or K != V in the builder fails here."""
+    g = rng(40 + r)
+    x = g.standard_normal((hh, ww, c))
+    wsr = g.standard_normal((r * r * c, c)) * 0.3
+    gamma = 1.0 + 0.1 * g.standard_normal(c)
+    beta = 0.1 * g.standard_normal(c)
+    got = run_unfused(configs.sra(hh=hh, ww=ww, c=c, r=r),
+                      {"X": x, "Wsr": wsr, "gamma": gamma, "beta": beta})["O"]
+    ref = _sra_direct(x, wsr, gamma, beta, r)
+    assert got.shape == (hh * ww, c)
+    assert np.max(np.abs(got - ref)) <= 1e-13 * np.max(np.abs(ref))
+    # the bound is tight enough to see even a 50 % change of eps
+    wrong = _sra_direct(x, wsr, gamma, beta, r, eps=1e-5 * 1.5)
+    assert np.max(np.abs(wrong - ref)) > 1e-9 * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("src,dst", [((3, 1), (2, 3, 4)), ((1,), (5,)), ((4,), (3, 4)), ((2, 1, 3), (2, 5, 3)),
+                                     ((1, 1), (1, 1))])
+def test_broadcast_against_loops(src, dst):
+    """Broadcast replicates along size-1 and missing leading dimensions: output
+    element x reads the input at x with the missing leading dimensions dropped
+    and every size-1 dimension indexed at 0."""
+    x = rng(50).standard_normal(src)
+    got = P.broadcast(x, dst)
+    assert got.shape == tuple(dst)
+    lead = len(dst) - len(src)
+    for idx in itertools.product(*[range(d) for d in dst]):
+        tail = idx[lead:]
+        sidx = tuple(0 if src[k] == 1 else tail[k] for k in range(len(src)))
+        assert got[idx] == x[sidx]
+    g = Graph()
+    xi = g.input("X", src)
+    b = g.op("broadcast", [xi], name="B", shape=dst)
+    g.output(b)
+    np.testing.assert_array_equal(run_unfused(g, {"X": x})["B"], got)
+    # the result owns its memory (a later in-place change to it does not reach x)
+    got.flat[0] += 1.0
+    assert x.flat[0] != got.flat[0]
