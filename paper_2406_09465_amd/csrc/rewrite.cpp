@@ -53,10 +53,18 @@ korch_attrs shape_attrs(const Shape& s) {
   return a;
 }
 
+// The bits of a double, so that two constants merge only when they are the
+// same value (a decimal rendering would round them to a few digits).
+uint64_t double_bits(double v) {
+  uint64_t b;
+  std::memcpy(&b, &v, sizeof(b));
+  return b;
+}
+
 std::string attrs_key(const korch_attrs& a) {
   std::ostringstream o;
   o << a.axis << ',' << a.keepdim << ',' << a.rank << ',' << a.has_scalar << ',' << a.stride << ',' << a.pad << ','
-    << a.pad_value << ',' << a.scalar;
+    << double_bits(a.pad_value) << ',' << double_bits(a.scalar);
   for (int d = 0; d < a.rank && d < KORCH_MAX_RANK; ++d)
     o << ';' << a.perm[d] << ':' << a.shape[d] << ':' << a.begin[d] << ':' << a.end[d];
   return o.str();

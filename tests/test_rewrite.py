@@ -221,3 +221,30 @@ def test_layout_variants_follow_product_operands():
     # graph inputs and outputs, layout nodes and row vectors never get variants
     assert graphs.build("conv", **SMALL["conv"]).graph.rewrite(K.RW_LAYOUT_VARIANTS)[1] == 0
     assert graphs.build("instnorm", **SMALL["instnorm"]).graph.rewrite(K.RW_LAYOUT_VARIANTS)[1] == 0
+
+
+def test_constants_that_differ_past_six_digits_stay_apart():
+    """The rebuilder merges identical nodes; two scalar products whose constants
+    agree to six significant digits are still different nodes, so
+    x*1.0000001 - x*1.0000004 keeps both products (it is not sub(n, n) = 0),
+    and both products can be graph outputs."""
+    for both_outputs in (False, True):
+        g = K.Graph()
+        x = g.input("f32", (4, 8))
+        a = g.op("mul", [x], "f32", scalar=1.0000001)
+        b = g.op("mul", [x], "f32", scalar=1.0000004)
+        if both_outputs:
+            g.output(a)
+            g.output(b)
+        else:
+            g.output(g.op("sub", [a, b], "f32"))
+        g.finalize()
+        for rules in (K.RW_ALL, K.RW_ALL | K.RW_LAYOUT_VARIANTS):
+            g2, _ = g.rewrite(rules)
+            muls = [v for v in range(g2.num_nodes()) if g2.node_info(v)[0] == "mul"]
+            assert sorted(g2.node_attrs(v)["scalar"] for v in muls) == [1.0000001, 1.0000004]
+            xv = np.random.default_rng(5).normal(size=(4, 8))
+            got = outputs_by_position(to_oracle(g2), [xv])
+            ref = [xv * 1.0000001, xv * 1.0000004] if both_outputs else [xv * 1.0000001 - xv * 1.0000004]
+            for y, r in zip(got, ref):
+                np.testing.assert_array_equal(y, r)
