@@ -224,13 +224,21 @@ int korch_plan_num_kernels(const korch_plan* p, int32_t* n);
 /* Family match, code generation and runtime compilation for gfx950 of every
    kernel (disk-cached).  Needs no GPU.  KORCH_E_UNSUPPORTED names the kernel. */
 int korch_plan_compile(korch_plan* p);
-/* Loads the compiled code objects on the current device and allocates the
-   plan's counter buffer (needs a GPU; korch_plan_execute calls it lazily). */
+/* Compiles the plan if needed, loads its code objects on the current device
+   and allocates and zeroes the plan's counter buffer (the arrival counters of
+   cross-workgroup hand-offs; each kernel leaves them at zero again).  Needs a
+   GPU; synchronizes the device once.  Required before any execute call on a
+   device; calling it again on the same device does nothing, on another device
+   it moves the plan there. */
 int korch_plan_load(korch_plan* p);
 int korch_plan_workspace_bytes(const korch_plan* p, size_t* bytes);
 /* Launches the plan's kernels in order on `stream` (a hipStream_t, NULL =
    default stream).  inputs[i] / outputs[i] follow graph input / output order.
-   Never allocates; never synchronizes. */
+   Never allocates, never compiles or loads, never synchronizes: a plan not
+   loaded on the current device (korch_plan_load) is KORCH_E_STATE.  The
+   plan's one counter buffer is shared by its executions, so one plan must not
+   execute on two streams at once (successive executions on one stream, or
+   streams ordered by events, are fine); use one plan per concurrent stream. */
 int korch_plan_execute(korch_plan* p, const void* const* inputs, void* const* outputs, void* workspace,
                        size_t workspace_bytes, void* stream);
 /* Same as korch_plan_execute but launches only kernels [first, first+count)

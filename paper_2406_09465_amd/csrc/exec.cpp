@@ -111,7 +111,14 @@ static bool aligned16(const void* q) { return ((uintptr_t)q & 15) == 0; }
 
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
                   hipStream_t stream, int first, int count, int timed, hipEvent_t ev_start, hipEvent_t ev_stop) {
-  load_plan(p);
+  // Execution only launches: loading (code objects, the counter buffer) is
+  // korch_plan_load's job, so nothing here allocates or synchronizes.
+  if (!p.loaded) fail(KORCH_E_STATE, "plan is not loaded: call korch_plan_load on this device first");
+  int dev = 0;
+  HIPCHECK(hipGetDevice(&dev));
+  if (dev != p.counter_device)
+    fail(KORCH_E_STATE, "plan is loaded on device " + std::to_string(p.counter_device) + ", not on the current device " +
+                            std::to_string(dev) + ": call korch_plan_load again");
   const Graph& g = p.g;
   for (size_t i = 0; i < g.inputs.size(); ++i) {
     if (!inputs || !inputs[i]) fail(KORCH_E_ARG, "input " + std::to_string(i) + " is NULL");

@@ -67,6 +67,16 @@ class _B:
         return self.ids[name]
 
 
+def _finish(b, name, outputs, sizes, extra_outputs=()):
+    """Marks the outputs (then any extra named nodes, so that a test can read
+    an intermediate tensor of the unfused plan) and finalizes the graph."""
+    names = list(outputs) + [x for x in extra_outputs if x not in outputs]
+    for o in names:
+        b.g.output(b.ids[o])
+    b.g.finalize()
+    return Workload(name, b.dtype, b.g, b.ids, b.inputs, names, sizes=sizes)
+
+
 def _softmax(b, s):
     b.op("m", "reduce_max", [s], axis=-1, keepdim=True)
     b.op("Z", "sub", [s, "m"])
@@ -88,7 +98,7 @@ def _layernorm(b, x, eps, p=""):
     return p + "Y"
 
 
-def attention(n=128, d=64, nk=None, dtype="f32"):
+def attention(n=128, d=64, nk=None, dtype="f32", extra_outputs=()):
     nk = n if nk is None else nk
     b = _B(dtype)
     b.inp("Q", (n, d))
@@ -99,15 +109,13 @@ def attention(n=128, d=64, nk=None, dtype="f32"):
     b.op("S", "mul", ["S0"], scalar=1.0 / math.sqrt(d))
     _softmax(b, "S")
     b.op("O", "matmul", ["P", "V"])
-    b.g.output(b.ids["O"])
-    b.g.finalize()
-    w = Workload("attention", dtype, b.g, b.ids, b.inputs, ["O"], sizes=dict(n=n, d=d, nk=nk))
+    w = _finish(b, "attention", ["O"], dict(n=n, d=d, nk=nk), extra_outputs)
     w.plans["fused"] = [(["KT", "S0", "S", "m", "Z", "E", "s", "P", "O"], ["O"])]
     w.plans["layered"] = [(["KT", "S0", "S"], ["S"]), (["m", "Z", "E", "s", "P"], ["P"]), (["O"], ["O"])]
     return w
 
 
-def mlp(m=4096, d=768, h=3072, dtype="f16", eps=1e-5):
+def mlp(m=4096, d=768, h=3072, dtype="f16", eps=1e-5, extra_outputs=()):
     b = _B(dtype)
     b.inp("X", (m, d))
     b.inp("W1", (d, h))
@@ -119,9 +127,7 @@ def mlp(m=4096, d=768, h=3072, dtype="f16", eps=1e-5):
     b.op("Hg", "gelu_tanh", ["H0"])
     b.op("Zo", "matmul", ["Hg", "W2"])
     b.op("out", "add", ["Zo", "X"])
-    b.g.output(b.ids["out"])
-    b.g.finalize()
-    w = Workload("mlp", dtype, b.g, b.ids, b.inputs, ["out"], sizes=dict(m=m, d=d, h=h))
+    w = _finish(b, "mlp", ["out"], dict(m=m, d=d, h=h), extra_outputs)
     # The statistics kernel materializes the centred rows D and the row scale
     # r (two outputs); normalization and affine run in the first product's
     # operand prologue, GELU in its epilogue, the residual in the second
@@ -140,7 +146,7 @@ def mlp(m=4096, d=768, h=3072, dtype="f16", eps=1e-5):
     return w
 
 
-def sra(hh=128, ww=128, c=64, r=8, dtype="f16", eps=1e-5):
+def sra(hh=128, ww=128, c=64, r=8, dtype="f16", eps=1e-5, extra_outputs=()):
     b = _B(dtype)
     b.inp("X", (hh, ww, c))
     b.inp("Wsr", (r * r * c, c))
@@ -157,9 +163,7 @@ def sra(hh=128, ww=128, c=64, r=8, dtype="f16", eps=1e-5):
     b.op("S", "mul", ["S0"], scalar=1.0 / math.sqrt(c))
     _softmax(b, "S")
     b.op("O", "matmul", ["P", kv])
-    b.g.output(b.ids["O"])
-    b.g.finalize()
-    w = Workload("sra", dtype, b.g, b.ids, b.inputs, ["O"], sizes=dict(hh=hh, ww=ww, c=c, r=r))
+    w = _finish(b, "sra", ["O"], dict(hh=hh, ww=ww, c=c, r=r), extra_outputs)
     ln = ["ln_mu", "ln_D", "ln_D2", "ln_var", "ln_ve", "ln_r", "ln_Xh", "ln_Yg", "ln_Y"]
     w.plans["fused"] = [
         (["Xt", "A", "KVp"] + ln, ["ln_Y"]),
@@ -175,7 +179,7 @@ def sra(hh=128, ww=128, c=64, r=8, dtype="f16", eps=1e-5):
     return w
 
 
-def conv(hh=416, ww=416, cin=32, cout=64, k=3, dtype="f16"):
+def conv(hh=416, ww=416, cin=32, cout=64, k=3, dtype="f16", extra_outputs=()):
     b = _B(dtype)
     b.inp("X", (hh, ww, cin))
     b.inp("W", (k, k, cin, cout))
@@ -189,15 +193,13 @@ def conv(hh=416, ww=416, cin=32, cout=64, k=3, dtype="f16"):
     b.op("SP", "log", ["E1"])
     b.op("T", "tanh", ["SP"])
     b.op("Y", "mul", ["B", "T"])
-    b.g.output(b.ids["Y"])
-    b.g.finalize()
-    w = Workload("conv", dtype, b.g, b.ids, b.inputs, ["Y"], sizes=dict(hh=hh, ww=ww, cin=cin, cout=cout, k=k))
+    w = _finish(b, "conv", ["Y"], dict(hh=hh, ww=ww, cin=cin, cout=cout, k=k), extra_outputs)
     w.plans["fused"] = [(["C", "B1", "B", "E", "E1", "SP", "T", "Y"], ["Y"])]
     w.plans["layered"] = [(["C", "B1", "B"], ["B"]), (["E", "E1", "SP", "T", "Y"], ["Y"])]
     return w
 
 
-def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6):
+def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6, extra_outputs=()):
     b = _B(dtype)
     b.inp("Q", (heads, n, d))
     b.inp("K", (heads, n, d))
@@ -212,9 +214,7 @@ def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6):
     b.op("den0", "matmul", ["Qr", "sKT"])
     b.op("den", "add", ["den0"], scalar=eps)
     b.op("out", "div", ["num", "den"])
-    b.g.output(b.ids["out"])
-    b.g.finalize()
-    w = Workload("linattn", dtype, b.g, b.ids, b.inputs, ["out"], sizes=dict(heads=heads, n=n, d=d))
+    w = _finish(b, "linattn", ["out"], dict(heads=heads, n=n, d=d), extra_outputs)
     w.plans["fused"] = [
         (["Kr", "KrT", "KVm", "sK"], ["KVm", "sK"]),
         (["Qr", "num", "sKT", "den0", "den", "out"], ["out"]),
@@ -227,7 +227,7 @@ def linattn(heads=16, n=4096, d=16, dtype="bf16", eps=1e-6):
     return w
 
 
-def instnorm(hh=224, ww=224, c=32, dtype="f16", eps=1e-5):
+def instnorm(hh=224, ww=224, c=32, dtype="f16", eps=1e-5, extra_outputs=()):
     b = _B(dtype)
     b.inp("X", (hh, ww, c))
     b.inp("gamma", (c,))
@@ -245,9 +245,7 @@ def instnorm(hh=224, ww=224, c=32, dtype="f16", eps=1e-5):
     b.op("R", "relu", ["Y"])
     b.op("Ri", "reshape", ["R"], shape=(hh, ww, c))
     b.op("out", "pad", ["Ri"], begin=(1, 1, 0), end=(1, 1, 0))
-    b.g.output(b.ids["out"])
-    b.g.finalize()
-    w = Workload("instnorm", dtype, b.g, b.ids, b.inputs, ["out"], sizes=dict(hh=hh, ww=ww, c=c))
+    w = _finish(b, "instnorm", ["out"], dict(hh=hh, ww=ww, c=c), extra_outputs)
     # operator per kernel (InstanceNorm as mean, variance and normalize; ReLU; Pad).
     # D feeds both the variance and the normalization, and a kernel holding D
     # and Xh but not the variance chain would not be convex, so the variance
@@ -258,6 +256,29 @@ def instnorm(hh=224, ww=224, c=32, dtype="f16", eps=1e-5):
     w.plans["fused"] = [(["mu"], ["mu"]), (["D", "D2", "var", "ve", "r"], ["D", "r"]),
                         (["Xh", "Yg", "Y", "R", "Ri", "out"], ["out"])]
     return w
+
+
+def layout_probe(op, dtype, shapes, **attrs):
+    """A graph of one layout primitive (transpose, slice, pad or concat) on
+    graph inputs of the given shapes; a concat whose ``fill`` attribute is set
+    appends a constant operand of that value (as the product-merging
+    transformation does).  Its unfused plan is one kernel per primitive, the
+    same generated kernels as the layout nodes of a workload's unfused plan."""
+    b = _B(dtype)
+    names = []
+    for i, sh in enumerate(shapes):
+        b.inp(f"in{i}", sh)
+        names.append(f"in{i}")
+    fill = attrs.pop("fill", None)
+    if fill is not None:
+        last = list(shapes[-1])
+        last[attrs.get("axis", -1)] = 1
+        b.op("ones", "fill", [], shape=tuple(last), scalar=fill)
+        names.append("ones")
+    if op == "pad":
+        attrs = dict(begin=attrs["lo"], end=attrs["hi"], pad_value=attrs.get("value", 0.0))
+    b.op("out", op, names, **attrs)
+    return _finish(b, f"layout_{op}", ["out"], dict(shapes=[tuple(s) for s in shapes]))
 
 
 BUILDERS = {"attention": attention, "mlp": mlp, "sra": sra, "conv": conv, "linattn": linattn, "instnorm": instnorm}

@@ -40,6 +40,7 @@ class PlanRunner:
         self.device = device
         self.plan = Plan(workload.graph, kernels) if kernels is not None else workload.plan(plan)
         self.plan.compile()
+        self.plan.load()  # code objects and the counter buffer on the current device
         self.ws_bytes = self.plan.workspace_bytes()
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=device)
         g = workload.graph

@@ -66,6 +66,45 @@ ATTN_CASES = [
     ("sra", dict(hh=8, ww=56, c=16, r=2)),
 ]
 
+# Bit-exact layout GPU tests.  In place: the unfused plan of a workload with
+# each listed layout node and its operand (when computed) as extra graph
+# outputs, at the full and a ragged size.
+LAYOUT_IN_PLACE = {
+    "attention": [("KT", "K")],
+    "sra": [("Xt", "X"), ("KT", "ln_Y")],
+    "linattn": [("KrT", "Kr"), ("sKT", "sK")],
+    "instnorm": [("out", "R")],
+}
+LAYOUT_SIZES = {w: SIZES[w][:2] for w in LAYOUT_IN_PLACE}
+# Stand-alone layout primitives (graphs.layout_probe): (op, dtype, input shapes, attributes).
+LAYOUT_STANDALONE = [
+    # the product-merging transformation at full workload sizes
+    ("concat", "f16", [(256, 64)], dict(axis=1, fill=1.0)),
+    ("concat", "bf16", [(16, 4096, 16)], dict(axis=2, fill=1.0)),
+    ("concat", "f32", [(128, 64)], dict(axis=1, fill=1.0)),
+    ("slice", "f16", [(16384, 65)], dict(begin=(0, 0), end=(16384, 64))),
+    ("slice", "f16", [(16384, 65)], dict(begin=(0, 64), end=(16384, 65))),
+    ("slice", "bf16", [(16, 4096, 17)], dict(begin=(0, 0, 0), end=(16, 4096, 16))),
+    ("slice", "bf16", [(16, 4096, 17)], dict(begin=(0, 0, 16), end=(16, 4096, 17))),
+    ("slice", "bf16", [(16, 16, 17)], dict(begin=(0, 0, 0), end=(16, 16, 16))),
+    ("slice", "f32", [(128, 65)], dict(begin=(0, 64), end=(128, 65))),
+    # layout variants of product operands (transposes of the last two axes)
+    ("transpose", "f16", [(4096, 768)], dict(perm=(1, 0))),
+    ("transpose", "f16", [(16384, 256)], dict(perm=(1, 0))),
+    ("transpose", "bf16", [(16, 16, 4096)], dict(perm=(0, 2, 1))),
+    # ragged shapes, several axes, two inputs, a non-zero pad value
+    ("transpose", "f16", [(37, 29, 8)], dict(perm=(2, 0, 1))),
+    ("transpose", "f32", [(50, 24)], dict(perm=(1, 0))),
+    ("transpose", "bf16", [(3, 5, 7, 9)], dict(perm=(3, 1, 0, 2))),
+    ("slice", "f16", [(33, 17, 5)], dict(begin=(3, 2, 1), end=(30, 17, 4))),
+    ("pad", "f16", [(13, 11, 24)], dict(lo=(1, 2, 0), hi=(2, 1, 0), value=0.0)),
+    ("pad", "bf16", [(7, 9)], dict(lo=(0, 3), hi=(5, 0), value=-2.5)),
+    ("pad", "f32", [(5, 6, 3)], dict(lo=(1, 1, 1), hi=(1, 1, 1), value=7.0)),
+    ("concat", "f16", [(9, 5), (9, 3)], dict(axis=1)),
+    ("concat", "bf16", [(4, 6, 2), (3, 6, 2)], dict(axis=0)),
+]
+
+
 # Workloads whose computed product operands get layout variants.
 LAYOUT_WORKLOADS = ("attention", "mlp", "sra", "linattn")
 
@@ -96,6 +135,11 @@ def _jobs():
     for wl, sz in ATTN_CASES:
         for flag in ("", "1"):
             jobs.append(("env_plans", wl, sz, ("KORCH_ATTN_NO_KEY_SPLIT", flag)))
+    for w, sizes in LAYOUT_SIZES.items():
+        for sz in sizes:
+            jobs.append(("layout_in_place", w, sz, None))
+    for i in range(len(LAYOUT_STANDALONE)):
+        jobs.append(("layout_probe", None, {}, i))
     for w, sizes in CHOOSER.items():
         for sz in sizes:
             jobs.append(("candidates", w, sz, None))
@@ -108,8 +152,22 @@ def _jobs():
 def _run_job(job, part=0, parts=1):
     """Compiles this process's share of one job; returns the failures."""
     kind, w, sz, extra = job
-    wl = graphs.build(w, **sz)
     failures = []
+    if kind in ("layout_in_place", "layout_probe"):
+        if kind == "layout_probe":
+            op, dt, shapes, attrs = LAYOUT_STANDALONE[extra]
+            wl = graphs.layout_probe(op, dt, shapes, **attrs)
+        else:
+            names = [n for pair in LAYOUT_IN_PLACE[w] for n in pair]
+            wl = graphs.build(w, **sz)
+            names = [n for n in names if n not in wl.input_names]
+            wl = graphs.build(w, extra_outputs=names, **sz)
+        try:
+            wl.plan("unfused").compile()
+        except KorchError as e:
+            failures.append((w, sz, f"{kind} {extra}", str(e)[:200]))
+        return failures
+    wl = graphs.build(w, **sz)
     if kind == "plans":
         for pn in ("unfused", "layered", "fused"):
             try:

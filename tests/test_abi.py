@@ -255,7 +255,25 @@ def test_execute_without_gpu_fails_loudly():
         pytest.skip("a GPU is present")
     w = graphs.attention(n=16, d=16)
     p = w.plan("fused")
-    assert code(lambda: p.execute([16, 16, 16], [16])) == -30
+    p.compile()
+    assert code(p.load) == -30  # KORCH_E_HIP: no device to load on
+
+
+def test_execute_of_an_unloaded_plan_is_a_state_error():
+    """Execution never compiles, loads or allocates: a plan that was not
+    loaded on the device is refused with KORCH_E_STATE before any HIP call
+    (so this runs without a GPU), compiled or not."""
+    w = graphs.attention(n=16, d=16)
+    p = w.plan("fused")
+    assert code(lambda: p.execute([16, 16, 16], [16])) == -4
+    p.compile()
+    assert code(lambda: p.execute([16, 16, 16], [16])) == -4
+    assert code(lambda: p.execute_kernels(0, 1, [16, 16, 16], [16])) == -4
+    try:
+        p.execute([16, 16, 16], [16])
+    except K.KorchError as e:
+        assert "korch_plan_load" in str(e)
+    assert code(lambda: p.execute_timed(0, 1, [16, 16, 16], [16], 0, 0, 0, 0, 0, 0)) == -4
 
 
 def test_unsupported_kernel_reports_infinite_cost():

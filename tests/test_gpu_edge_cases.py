@@ -1,0 +1,74 @@
+"""GPU parity on the degenerate inputs of each workload (synthetic.edge):
+Mish arguments beyond +-20 (the clamp of tanh(softplus(x)) and exp(x)
+underflow), zero-variance LayerNorm rows and InstanceNorm channels, score
+ranges of several tens in both softmaxes, and ReLU linear attention rows and
+heads whose exact result is 0.  Every plan (one kernel per primitive,
+layered, fused) at full size against the float64 oracle on the same inputs,
+with the standard tolerance rule, plus the exact or tighter checks each case
+allows.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import configs as OC
+from oracle.graph import run_unfused
+from synthetic import storage_to_f64
+from synthetic import workloads as W
+from synthetic.edge import CASES, edge_inputs
+from tests.helpers import TOL, close, close_elementwise
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+PLANS = ["unfused", "layered", "fused"]
+_ref = {}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def reference(workload):
+    if workload not in _ref:
+        _ref.clear()
+        raw = edge_inputs(workload)
+        dt = W.DEFAULT_DTYPE[workload]
+        x = {k: storage_to_f64(v, dt) for k, v in raw.items()}
+        _ref[workload] = (raw, x, run_unfused(OC.build(workload), x, keep_all=True))
+    return _ref[workload]
+
+
+@pytest.mark.parametrize("plan", PLANS)
+@pytest.mark.parametrize("workload", list(CASES))
+def test_edge_case(workload, plan):
+    from paper_2406_09465_amd import graphs
+    from paper_2406_09465_amd.runner import PlanRunner
+    print(f"\n[case] edge {workload} {CASES[workload]} {plan}", flush=True)
+    raw, x, ref = reference(workload)
+    w = graphs.build(workload)
+    out = PlanRunner(w, plan).run(raw)
+    tol = TOL[w.dtype]
+    name = w.output_names[0]
+    g, r = out[name], ref[name]
+    ok, mx, rel = close(g, r, tol)
+    assert ok, f"{workload}.{name}: max abs err {mx:.3e}, normwise rel {rel:.3e} > tol {tol}"
+    if workload == "conv":
+        # per element with an absolute floor of about one fp16 unit at 1.0
+        # (the standard rule's floor is tol * max|r| ~ 2.4 here)
+        ok, mx, rel = close_elementwise(g, r, tol, 1e-3)
+        assert ok, f"conv elementwise: max abs {mx:.3e}, max rel {rel:.3e}"
+        b = ref["B"]
+        assert np.all(g[b < -100] == 0.0)  # Mish of an argument below -100 rounds to zero in fp16
+    elif workload == "mlp":
+        ok, mx, rel = close_elementwise(g[:18], r[:18], tol, 1e-3)
+        assert ok, f"mlp flat rows: max abs {mx:.3e}, max rel {rel:.3e}"
+    elif workload == "instnorm":
+        beta = np.maximum(x["beta"][:4], 0.0)
+        assert np.max(np.abs(g[1:-1, 1:-1, :4] - beta)) <= 1e-3
+        assert np.all(g[0] == 0) and np.all(g[:, 0] == 0)
+    elif workload == "linattn":
+        assert np.all(g[:, ::7, :] == 0.0), "all-negative query rows must give exactly 0"
+        assert np.all(g[2] == 0.0), "a head with all-negative keys must give exactly 0"

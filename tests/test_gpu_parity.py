@@ -12,7 +12,7 @@ import pytest
 
 from oracle import configs as OC
 from oracle.graph import run_unfused
-from tests.helpers import TOL, close, inputs_f64
+from tests.helpers import TOL, close, close_elementwise, inputs_f64
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -62,6 +62,11 @@ def check(workload, w, out, ref):
     tol = TOL[w.dtype]
     for name in w.output_names:
         ok, mx, rel = close(out[name], ref[name], tol)
+        # also reported: the per-element rule with a fixed absolute floor
+        floor = 1e-6 if w.dtype == "f32" else 1e-3
+        _, _, erel = close_elementwise(out[name], ref[name], tol, floor)
+        print(f"[err] {workload}.{name}: max abs {mx:.3e}, normwise rel {rel:.3e}, "
+              f"max rel where |ref| > {floor / tol:.0e}: {erel:.3e}", flush=True)
         assert ok, f"{workload}.{name}: max abs err {mx:.3e}, normwise rel {rel:.3e} > tol {tol}"
 
 
