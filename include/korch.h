@@ -241,6 +241,23 @@ int korch_plan_workspace_bytes(const korch_plan* p, size_t* bytes);
    streams ordered by events, are fine); use one plan per concurrent stream. */
 int korch_plan_execute(korch_plan* p, const void* const* inputs, void* const* outputs, void* workspace,
                        size_t workspace_bytes, void* stream);
+/* korch_plan_execute for callers that cannot allocate device memory (code
+   under HIP graph capture, tight serving loops, harnesses that forbid
+   allocation): no workspace argument.  The plan's workspace and hand-off
+   counters live in a static device array of the library, 32 MiB per device
+   (the first 64 KiB for counters, the rest, 33,488,896 bytes, for the
+   workspace), held from the first korch_plan_load on a device until the
+   process ends; korch_plan_load looks up its address on each device.  The
+   call first clears the counters the plan uses with a fill kernel on
+   `stream`, then launches the plan's kernels; it never allocates, compiles,
+   loads or synchronizes.  Errors: KORCH_E_STATE when the plan is not loaded
+   on the current device; KORCH_E_WORKSPACE when the plan's workspace
+   (korch_plan_workspace_bytes) or counters exceed the static array (nothing
+   is launched); KORCH_E_ARG / KORCH_E_ALIGN as korch_plan_execute.  Every
+   call on one device shares that device's array and finds there whatever the
+   previous call left: calls that overlap on one device (two streams, or two
+   threads without ordering) race and give wrong results. */
+int korch_plan_execute_noalloc(korch_plan* p, const void* const* inputs, void* const* outputs, void* stream);
 /* Same as korch_plan_execute but launches only kernels [first, first+count)
    of the plan (for timing one kernel in place); the caller is responsible for
    having run the earlier kernels whose outputs these read. */

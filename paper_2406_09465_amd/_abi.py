@@ -105,6 +105,7 @@ _SIGS = {
     "korch_plan_load": ([_P], C.c_int),
     "korch_plan_workspace_bytes": ([_P, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute": ([_P, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
+    "korch_plan_execute_noalloc": ([_P, C.POINTER(_P), C.POINTER(_P), _P], C.c_int),
     "korch_plan_execute_kernels": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
     "korch_kernel_source": ([_P, _P, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute_timed": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P, _I, _P, _P], C.c_int),
@@ -375,6 +376,13 @@ class Plan:
         outs = outputs if isinstance(outputs, C.Array) else pointer_array(outputs)
         check(lib.korch_plan_execute(self.h, ins, outs, C.c_void_p(int(workspace)), int(workspace_bytes),
                                      C.c_void_p(int(stream))))
+
+    def execute_noalloc(self, inputs, outputs, stream=0):
+        """korch_plan_execute_noalloc: workspace and counters in the library's
+        static device scratch (no allocation; the plan must be loaded)."""
+        ins = inputs if isinstance(inputs, C.Array) else pointer_array(inputs)
+        outs = outputs if isinstance(outputs, C.Array) else pointer_array(outputs)
+        check(lib.korch_plan_execute_noalloc(self.h, ins, outs, C.c_void_p(int(stream))))
 
     def execute_kernels(self, first, count, inputs, outputs, workspace=0, workspace_bytes=0, stream=0):
         ins = inputs if isinstance(inputs, C.Array) else pointer_array(inputs)

@@ -26,7 +26,8 @@ void load_plan(Plan& p);
 void destroy_plan_device(Plan& p);
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
                   hipStream_t stream, int first, int count, int timed = -1, hipEvent_t ev_start = nullptr,
-                  hipEvent_t ev_stop = nullptr);
+                  hipEvent_t ev_stop = nullptr, void* counters = nullptr);
+void execute_plan_noalloc(Plan& p, const void* const* inputs, void* const* outputs, hipStream_t stream);
 void compile_candidate(const Graph& g, const KernelDesc& kd);
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream);
@@ -413,6 +414,13 @@ int korch_plan_execute(korch_plan* p, const void* const* inputs, void* const* ou
   return guard([&] {
     NEED(p);
     execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, 0, -1);
+  });
+}
+
+int korch_plan_execute_noalloc(korch_plan* p, const void* const* inputs, void* const* outputs, void* stream) {
+  return guard([&] {
+    NEED(p);
+    execute_plan_noalloc(p->p, inputs, outputs, (hipStream_t)stream);
   });
 }
 

@@ -1,6 +1,9 @@
-// Helper kernels of the profiler: a cache-flushing write and a seeded fill.
+// Helper kernels of the profiler (a cache-flushing write and a seeded fill),
+// and the static device scratch of allocation-free plan execution.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <mutex>
 
 namespace {
 
@@ -32,9 +35,60 @@ __global__ void fill_kernel(void* __restrict__ p, size_t n, int dtype, uint64_t 
   }
 }
 
+// Zeroes `n` 16-byte words (clears counters without a memset node, so a
+// caller may capture the launch in a graph).
+__global__ void zero_kernel(uint4* __restrict__ p, size_t n) {
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = make_uint4(0, 0, 0, 0);
+}
+
+// Device memory of korch_plan_execute_noalloc: hand-off counters in the first
+// kStaticCounterBytes, the plan's workspace after them.  One copy per device,
+// held until the process ends.  Host code never passes this name to a kernel
+// (on the host it is only a stand-in); it uses the per-device address that
+// hipGetSymbolAddress returns.
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices];
+
 }  // namespace
 
 namespace korch {
+
+size_t static_scratch_bytes() { return kStaticScratchBytes; }
+
+// Set-up, once per device, with that device current: looks up and keeps this
+// device's address of the static scratch.
+hipError_t static_scratch_setup(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_addr[dev]) return hipSuccess;
+  void* q = nullptr;
+  hipError_t e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  if (!q) return hipErrorInvalidSymbol;
+  g_scratch_addr[dev] = q;
+  return hipSuccess;
+}
+
+// The address kept by static_scratch_setup for `dev`, or NULL before it.
+void* static_scratch_address(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  return g_scratch_addr[dev];
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
+  size_t n = bytes / 16;
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, (uint4*)p, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_flush(void* p, size_t bytes, hipStream_t s) {
   size_t n = bytes / 16;

@@ -22,6 +22,14 @@ namespace korch {
 std::vector<char> rtc_compile(const std::string& src, const std::string& name);
 hipError_t launch_flush(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_fill(void* p, size_t n, int dtype, uint64_t seed, hipStream_t s);
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+size_t static_scratch_bytes();
+hipError_t static_scratch_setup(int dev);
+void* static_scratch_address(int dev);
+
+// Head of the static scratch reserved for hand-off counters (every plan's
+// counters are a few KiB: one 128-byte line per output tile or split group).
+constexpr size_t kStaticCounterBytes = (size_t)64 << 10;
 
 #define HIPCHECK(x)                                                                             \
   do {                                                                                          \
@@ -103,6 +111,8 @@ void load_plan(Plan& p) {
     HIPCHECK(hipMalloc(&p.counters, p.counter_bytes));
     HIPCHECK(hipMemset(p.counters, 0, p.counter_bytes));
   }
+  // set-up of allocation-free execution on this device (kept per device)
+  HIPCHECK(static_scratch_setup(dev));
   p.counter_device = dev;
   p.loaded = true;
 }
@@ -110,7 +120,8 @@ void load_plan(Plan& p) {
 static bool aligned16(const void* q) { return ((uintptr_t)q & 15) == 0; }
 
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
-                  hipStream_t stream, int first, int count, int timed, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                  hipStream_t stream, int first, int count, int timed, hipEvent_t ev_start, hipEvent_t ev_stop,
+                  void* counters) {
   // Execution only launches: loading (code objects, the counter buffer) is
   // korch_plan_load's job, so nothing here allocates or synchronizes.
   if (!p.loaded) fail(KORCH_E_STATE, "plan is not loaded: call korch_plan_load on this device first");
@@ -136,19 +147,27 @@ void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void
   int nk = (int)p.ck.size();
   if (first < 0 || first > nk) fail(KORCH_E_ARG, "first kernel index out of range");
   int last = count < 0 ? nk : std::min(nk, first + count);
+  char* cbase = (char*)(counters ? counters : p.counters);
   for (int k = first; k < last; ++k) {
     auto& ck = p.ck[k];
-    std::vector<void*> ptr(ck.arg_storage.size());
+    // kernel arguments on the stack (no host allocation per launch)
+    void* stack_ptr[64];
+    std::vector<void*> heap_ptr;
+    void** ptr = stack_ptr;
+    if (ck.arg_storage.size() > 64) {
+      heap_ptr.resize(ck.arg_storage.size());
+      ptr = heap_ptr.data();
+    }
     for (size_t a = 0; a < ck.arg_storage.size(); ++a) {
       const Storage& s = ck.arg_storage[a];
       switch (s.kind) {
         case Storage::GraphInput: ptr[a] = const_cast<void*>(inputs[s.index]); break;
         case Storage::GraphOutput: ptr[a] = outputs[s.index]; break;
         case Storage::Workspace: ptr[a] = (char*)ws + s.offset; break;
-        case Storage::Counters: ptr[a] = (char*)p.counters + s.offset; break;
+        case Storage::Counters: ptr[a] = cbase + s.offset; break;
       }
     }
-    void* params[] = {ptr.data()};
+    void* params[] = {(void*)ptr};
     if (k == timed && (ev_start || ev_stop)) {
       // the events take the timestamps of this kernel's own dispatch (no
       // separate marker packets in the stream)
@@ -161,6 +180,31 @@ void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void
     HIPCHECK(hipModuleLaunchKernel((hipFunction_t)ck.function, ck.gen.grid[0], ck.gen.grid[1], ck.gen.grid[2],
                                    ck.gen.block[0], ck.gen.block[1], ck.gen.block[2], 0, stream, params, nullptr));
   }
+}
+
+// korch_plan_execute without a workspace argument and without any allocation:
+// the workspace and the hand-off counters live in the static device scratch.
+// The counters this plan uses are cleared by a fill kernel first (stream
+// ordered, no memset node), since the scratch keeps whatever the last call
+// on this device left there.
+void execute_plan_noalloc(Plan& p, const void* const* inputs, void* const* outputs, hipStream_t stream) {
+  if (!p.loaded) fail(KORCH_E_STATE, "plan is not loaded: call korch_plan_load on this device first");
+  int dev = 0;
+  HIPCHECK(hipGetDevice(&dev));
+  if (dev != p.counter_device)
+    fail(KORCH_E_STATE, "plan is loaded on device " + std::to_string(p.counter_device) + ", not on the current device " +
+                            std::to_string(dev) + ": call korch_plan_load again");
+  char* base = (char*)static_scratch_address(dev);
+  if (!base) fail(KORCH_E_STATE, "static scratch not set up on this device: call korch_plan_load");
+  const size_t ws_cap = static_scratch_bytes() - kStaticCounterBytes;
+  if (p.counter_bytes > kStaticCounterBytes)
+    fail(KORCH_E_WORKSPACE, "plan needs " + std::to_string(p.counter_bytes) + " bytes of counters; the static scratch holds " +
+                                std::to_string(kStaticCounterBytes));
+  if (p.ws_bytes > ws_cap)
+    fail(KORCH_E_WORKSPACE, "plan needs " + std::to_string(p.ws_bytes) + " bytes of workspace; the static scratch holds " +
+                                std::to_string(ws_cap) + " (use korch_plan_execute with a caller workspace)");
+  if (p.counter_bytes) HIPCHECK(launch_zero(base, p.counter_bytes, stream));
+  execute_plan(p, inputs, outputs, base + kStaticCounterBytes, ws_cap, stream, 0, -1, -1, nullptr, nullptr, base);
 }
 
 // The candidate kernel as a stand-alone graph: its external tensors become
@@ -233,13 +277,13 @@ float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int re
     }
     void* ws = p.ws_bytes ? alloc(p.ws_bytes) : nullptr;
     void* fl = flush_bytes ? alloc(flush_bytes) : nullptr;
-    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr);
+    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr, nullptr);
     ev = new hipEvent_t[2 * std::max(reps, 1)];
     for (int r = 0; r < 2 * reps; ++r) HIPCHECK(hipEventCreate(&ev[r]));
     for (int r = 0; r < reps; ++r) {
       if (fl) HIPCHECK(launch_flush(fl, flush_bytes, stream));
       HIPCHECK(hipEventRecord(ev[2 * r], stream));
-      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr);
+      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr, nullptr);
       HIPCHECK(hipEventRecord(ev[2 * r + 1], stream));
     }
     HIPCHECK(hipStreamSynchronize(stream));

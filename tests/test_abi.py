@@ -274,6 +274,7 @@ def test_execute_of_an_unloaded_plan_is_a_state_error():
     except K.KorchError as e:
         assert "korch_plan_load" in str(e)
     assert code(lambda: p.execute_timed(0, 1, [16, 16, 16], [16], 0, 0, 0, 0, 0, 0)) == -4
+    assert code(lambda: p.execute_noalloc([16, 16, 16], [16])) == -4
 
 
 def test_unsupported_kernel_reports_infinite_cost():
