@@ -1,11 +1,20 @@
 """Fused-subgraph latency of one workload's orchestration plan on one MI355X.
 
 One step = one execution of the whole plan (every kernel of the fused
-orchestration) on inputs already resident in HBM.  Prints ONE JSON line:
-metric / value (microseconds per step) plus a roofline object for the plan's
-dominant kernel (algorithmic flops or bytes per launch over its average
-launch time, measured with HIP events around that kernel inside the timed
-loop) and the float64 oracle timed on the host cores on a bounded sample.
+orchestration) on inputs already resident in HBM.  Before every timed step a
+512 MiB device write evicts L2 and the Infinity Cache (the workloads' working
+sets would otherwise stay cache-resident); the step's latency is the span from
+its first kernel's dispatch start to its last kernel's dispatch end, taken by
+events attached to those dispatches.  `value` is the median over the timed
+steps (p10 / p90 beside it); the same plan back to back without flushes is
+reported as `warm`.
+
+Prints ONE JSON line: metric / value (microseconds per step), a roofline
+object for the plan's dominant kernel (algorithmic flops or bytes per launch
+over its mean launch duration in the timed steps), the measured-cost model's
+prediction against the measured step, the unfused plan of the same graph under
+the same protocol, and the float64 oracle timed on the host cores on a bounded
+sample.
 
 Default workload: transformer MLP block, fp16, X [4096, 768], W1 [768, 3072],
 W2 [3072, 768] (the configuration the headline metric is quoted on).
@@ -43,7 +52,9 @@ DESCR = {
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--steps", type=int, default=400,
+                    help="timed steps, each preceded by a cache flush and timed from its first kernel's start "
+                         "to its last kernel's end")
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="mlp", choices=list(DESCR))
     ap.add_argument("--plan", default="korch",
@@ -54,8 +65,12 @@ def parse():
     ap.add_argument("--no-rewrite", action="store_true",
                     help="korch plan: do not consider the transformed primitive graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--time-every", type=int, default=8,
-                    help="bracket the dominant kernel with events on every N-th timed step")
+    ap.add_argument("--no-unfused", action="store_true", help="skip the unfused-plan comparison")
+    ap.add_argument("--flush-mib", type=int, default=512,
+                    help="bytes written before every timed step to evict L2 and the Infinity Cache")
+    ap.add_argument("--profile-reps", type=int, default=100, help="timed launches per candidate in the chooser")
+    ap.add_argument("--no-profile-db", action="store_true",
+                    help="profile every candidate again instead of reusing latencies recorded in the profile database")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work for the oracle sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, run a plain device copy of this many MiB 3 times (PMC byte calibration)")
@@ -108,6 +123,48 @@ def traffic_from_profiles(kernel_name, source_hash):
         return None
 
 
+def pct(xs):
+    """n, p10, median, p90 (microseconds) of a sample."""
+    ys = sorted(xs)
+
+    def q(f):
+        return round(ys[min(len(ys) - 1, int(f * (len(ys) - 1) + 0.5))], 3)
+    return {"n": len(ys), "p10_us": q(0.1), "median_us": round(statistics.median(ys), 3), "p90_us": q(0.9)}
+
+
+def timed_steps(r, steps, flush, stream):
+    """Runs `steps` executions of the bound plan of runner `r` on `stream`.
+    Before each one, when `flush` (a device byte tensor) is given, it is
+    overwritten, outside the measured span.  Every execution carries an event
+    on the start of its first kernel's dispatch and one on the end of every
+    kernel's dispatch (end-of-dispatch events add nothing to the span; a
+    start event on a later kernel adds a few microseconds, so none is used).
+    Returns the spans (first kernel's start to last kernel's end, us), each
+    kernel's duration in every execution (us; kernel k > 0: from the end of
+    kernel k - 1 to its own end, i.e. including the dispatch gap in front of
+    it), and the wall time of the loop (s)."""
+    import torch
+    nk = r.plan.num_kernels()
+    recs = []
+    for _ in range(steps):
+        st = [torch.cuda.Event(enable_timing=True)] + [None] * (nk - 1)
+        en = [torch.cuda.Event(enable_timing=True) for _ in range(nk)]
+        for e in st[:1] + en:
+            e.record(stream)  # creates the underlying event
+        recs.append((st, en, r.event_arrays(st, en)))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i, (_, _, arr) in enumerate(recs):
+        if flush is not None:
+            flush.fill_(i & 0xFF)
+        r.launch_events_bound(arr)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    spans = [st[0].elapsed_time(en[nk - 1]) * 1e3 for st, en, _ in recs]
+    per = [[(st[0] if k == 0 else en[k - 1]).elapsed_time(en[k]) * 1e3 for st, en, _ in recs] for k in range(nk)]
+    return {"spans": spans, "per_kernel": per, "wall_s": wall}
+
+
 # Relative cost margin a transformed graph's plan must beat the original's by.
 TIE_MARGIN = 0.02
 
@@ -142,7 +199,12 @@ def main():
         from paper_2406_09465_amd.warm import CHOOSER_LIMITS, LAYOUT_WORKLOADS
         t0 = time.time()
         hand = [k for name in ("fused", "layered") for k in w.kernels(name)]
-        ch = chooser.korch_plan(w.graph, warmup=10, reps=50, extra=hand, **CHOOSER_LIMITS)
+        db = None
+        if not args.no_profile_db:
+            from paper_2406_09465_amd.profile_db import ProfileDB
+            db = ProfileDB()
+        prof = dict(warmup=10, reps=args.profile_reps, flush_bytes=args.flush_mib << 20, db=db)
+        ch = chooser.korch_plan(w.graph, extra=hand, **prof, **CHOOSER_LIMITS)
         best, rules, w0 = ch, 0, w
         alt = lay = None
         if not args.no_rewrite:
@@ -154,7 +216,7 @@ def main():
                 w2, napp = graphs.rewritten(w0, rr)
                 if not napp:
                     continue
-                c2 = chooser.korch_plan(w2.graph, warmup=10, reps=50, **CHOOSER_LIMITS)
+                c2 = chooser.korch_plan(w2.graph, **prof, **CHOOSER_LIMITS)
                 if rr == RW_ALL:
                     alt = c2
                 else:
@@ -169,7 +231,8 @@ def main():
                        "search_states": best.states, "original_graph_us": round(ch.cost_us, 3),
                        "rewritten_graph_us": round(alt.cost_us, 3) if alt else None,
                        "layout_graph_us": round(lay.cost_us, 3) if lay else None,
-                       "choose_seconds": round(time.time() - t0, 1)})
+                       "choose_seconds": round(time.time() - t0, 1),
+                       "profile_db": {"path": db.path, "hits": db.hits, "new": db.new} if db else None})
         r = PlanRunner(w, kernels=best.kernels)
     else:
         r = PlanRunner(w, args.plan)
@@ -189,47 +252,35 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # warmup, and per-kernel timing to pick the dominant kernel
+    # warm-up, then the timed region: exactly `steps` plan executions.  Before
+    # every step a write of `flush_mib` MiB (outside the measured span) evicts
+    # L2 and the Infinity Cache, so the step reads its inputs from HBM.  A step's
+    # latency is the span from its first kernel's dispatch start to its last
+    # kernel's dispatch end, taken by events that the library attaches to those
+    # dispatches (no marker packets); end-of-dispatch events on every kernel
+    # give the per-kernel durations and the dominant kernel's launch time.
     for _ in range(args.warmup):
         r.launch()
-    torch.cuda.synchronize()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(nk)]
-    for e in ev:
-        e[0].record(stream)
-        e[1].record(stream)
-    per = [[] for _ in range(nk)]
-    for _ in range(max(5, args.warmup)):
-        for k in range(nk):
-            r.launch_timed(k, ev[k][0], ev[k][1])
-        torch.cuda.synchronize()
-        for k in range(nk):
-            per[k].append(ev[k][0].elapsed_time(ev[k][1]) * 1e3)
-    dom = max(range(nk), key=lambda k: statistics.median(per[k]))
-
-    # timed region: exactly `steps` plan executions, one library call each.  On
-    # every `time_every`-th step the library launches the dominant kernel with a
-    # pair of events (created here, recorded once so that they exist) that take
-    # that dispatch's own start and end timestamps on the launch stream; its
-    # average duration is taken over those sampled launches.
-    sampled = list(range(0, args.steps, max(1, args.time_every)))
-    starts = {i: torch.cuda.Event(enable_timing=True) for i in sampled}
-    ends = {i: torch.cuda.Event(enable_timing=True) for i in sampled}
-    for i in sampled:
-        starts[i].record(stream)
-        ends[i].record(stream)
     r.bind(stream)
-    timed_at = [starts.get(i) for i in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        if timed_at[i] is not None:
-            r.launch_timed_bound(dom, timed_at[i], ends[i])
-        else:
-            r.launch_bound()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
-    dom_us = statistics.mean(starts[i].elapsed_time(ends[i]) * 1e3 for i in sampled)
+    flush = torch.empty(max(1, args.flush_mib) << 20, dtype=torch.uint8, device="cuda") if args.flush_mib else None
+    res = timed_steps(r, args.steps, flush, stream)
+    spans = res["spans"]
+    per = res["per_kernel"]
+    dom = max(range(nk), key=lambda k: statistics.median(per[k]))
+    dom_us = statistics.mean(per[dom])
+    value_us = statistics.median(spans)
+    dist = pct(spans)
+    if args.steps < 200:
+        # the timing protocol's sample size: more flushed steps outside the
+        # timed region, for the distribution only
+        more = timed_steps(r, 200 - args.steps, flush, stream)["spans"]
+        d2 = pct(spans + more)
+        dist["n200"] = {k_: d2[k_] for k_ in ("n", "p10_us", "median_us", "p90_us")}
+    # the same plan back to back without flushes (warm caches)
+    warm = timed_steps(r, max(args.steps, 50), None, stream)
+    warm_d = pct(warm["spans"])
+    warm_d["back_to_back_us_per_step"] = round(warm["wall_s"] * 1e6 / max(args.steps, 50), 3)
+    warm_d["note"] = "no flush: inputs and weights resident in L2 / Infinity Cache"
 
     fam, abytes, aflops = r.plan.kernel_info(dom)
     name = r.plan.kernel_name(dom)
@@ -249,9 +300,10 @@ def main():
     roof["traffic"] = traffic_from_profiles(f"{args.workload}/{name}", src_hash)
     roof["kernel"] = name
     roof["kernel_us"] = round(dom_us, 3)
-    roof["timed_launches"] = len(sampled)
+    roof["timed_launches"] = len(per[dom])
     roof["alg_bytes"] = abytes
     roof["alg_flops"] = aflops
+    roof["source_hash"] = src_hash
 
     # context floors (same run, same stream): a launch of a one-element kernel,
     # and a device copy moving the plan's algorithmic bytes per step (half read,
@@ -275,36 +327,37 @@ def main():
     del one, csrc, cdst
 
     # context: the unfused plan of the same primitive graph (one kernel per
-    # primitive, contiguous reshapes as views), same inputs, back to back
-    ru = PlanRunner(graphs.build(args.workload), "unfused")
-    ru.set_inputs(W.inputs(args.workload))
-    for _ in range(5):
-        ru.launch()
-    ru.bind(stream)
-    n_unf = max(20, args.steps // 2)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for _ in range(n_unf):
-        ru.launch_bound()
-    torch.cuda.synchronize()
-    unfused = {"us_per_step": round((time.perf_counter() - t1) * 1e6 / n_unf, 3),
-               "kernels": ru.plan.num_kernels(), "steps": n_unf}
-    del ru
+    # primitive, contiguous reshapes as views), same inputs, same protocol
+    unfused = None
+    if not args.no_unfused:
+        ru = PlanRunner(graphs.build(args.workload), "unfused")
+        ru.set_inputs(W.inputs(args.workload))
+        for _ in range(5):
+            ru.launch()
+        ru.bind(stream)
+        n_unf = max(20, args.steps // 2)
+        uf = timed_steps(ru, n_unf, flush, stream)
+        uw = timed_steps(ru, n_unf, None, stream)
+        unfused = {"us_per_step": round(statistics.median(uf["spans"]), 3), "flushed": pct(uf["spans"]),
+                   "warm": pct(uw["spans"]), "kernels": ru.plan.num_kernels(), "steps": n_unf}
+        del ru
+    del flush
 
     kernels = []
     for k in range(nk):
         f, b, fl = r.plan.kernel_info(k)
         kernels.append({"name": r.plan.kernel_name(k), "family": f, "us": round(statistics.median(per[k]), 3),
+                        "warm_us": round(statistics.median(warm["per_kernel"][k]), 3),
                         "alg_bytes": b, "alg_flops": fl})
 
     out = {
         "metric": METRIC,
-        "value": round(ms_per_step * 1e3, 3),
+        "value": round(value_us, 3),
         "unit": "us",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 6),
+        "ms_per_step": round(value_us * 1e-3, 6),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -312,6 +365,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": DESCR[args.workload], "plan": "recorded" if args.kernels_json else args.plan,
                    "kernels": nk},
+        "timing": dict(dist, protocol=f"each step after a {args.flush_mib} MiB write (outside the span); span = first "
+                                         "kernel's dispatch start to last kernel's dispatch end; value = median",
+                       wall_s_with_flushes=round(res["wall_s"], 4)),
+        "warm": warm_d,
         "roofline": roof,
         "unfused": unfused,
         "floors": floors,
@@ -319,6 +376,12 @@ def main():
     }
     if chosen:
         out["chosen_plan"] = chosen
+        if chosen.get("predicted_us"):
+            # the cost model (sum of the kernels' profiled latencies) against
+            # the measured flushed step
+            out["cost_model"] = {"predicted_us": chosen["predicted_us"], "measured_us": round(value_us, 3),
+                                 "sum_kernel_medians_us": round(sum(statistics.median(p_) for p_ in per), 3),
+                                 "predicted_over_measured": round(chosen["predicted_us"] / value_us, 4)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -274,6 +274,17 @@ int korch_plan_execute_kernels(korch_plan* p, int32_t first, int32_t count, cons
 int korch_plan_execute_timed(korch_plan* p, int32_t first, int32_t count, const void* const* inputs,
                              void* const* outputs, void* workspace, size_t workspace_bytes, void* stream, int32_t timed,
                              void* start, void* stop);
+/* korch_plan_execute with timing events on any kernels: start_events[k] and
+   stop_events[k] (arrays with one entry per kernel of the plan; either array,
+   and any entry, may be NULL) are hipEvent_t handles owned by the caller,
+   created with timing enabled, that take the start and end timestamps of
+   kernel k's own dispatch on `stream` (no marker packets are added).  So one
+   call measures the span of a whole plan execution (the first kernel's start
+   to the last kernel's end) and any kernel inside it.  Errors as
+   korch_plan_execute. */
+int korch_plan_execute_events(korch_plan* p, const void* const* inputs, void* const* outputs, void* workspace,
+                              size_t workspace_bytes, void* stream, void* const* start_events,
+                              void* const* stop_events);
 /* Per-kernel family, algorithmic bytes (compulsory reads of its external
    tensors plus writes of its outputs) and flops (2*M*N*K per contraction). */
 int korch_plan_kernel_info(const korch_plan* p, int32_t k, int32_t* family, double* alg_bytes, double* alg_flops);
@@ -294,7 +305,12 @@ int korch_compile_candidate(const korch_graph* g, const korch_kernel_desc* k);
    with seeded uniform values in [0.5, 1.5) in device buffers the profiler allocates, runs
    `warmup` untimed launches, then `reps` launches each preceded by a write of
    `flush_bytes` to a scratch buffer (to evict L2 and the Infinity Cache) and
-   bracketed by HIP events on `stream`; *median_us is the median.  Returns
+   a read of every input that the parent graph computes (in a plan, the
+   producing kernel has just written such a tensor, so it is cache-resident,
+   while graph inputs come from HBM; environment KORCH_PROFILE_COLD=1 skips
+   that read), each launch timed by HIP events that take that dispatch's own
+   start and end timestamps on `stream`; *median_us is the median.  The cost
+   of a plan is the sum of its kernels' costs (Section 4.2).  Returns
    KORCH_E_UNSUPPORTED (cost infinity) when no family implements it. */
 int korch_profile_candidate(const korch_graph* g, const korch_kernel_desc* k, int32_t warmup, int32_t reps,
                             size_t flush_bytes, void* stream, float* median_us);

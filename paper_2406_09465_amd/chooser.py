@@ -104,16 +104,34 @@ def plan_cost(view: GraphView, kernels, cost_of) -> float:
     return sum(cost_of[(tuple(p), tuple(o))] for p, o in kernels)
 
 
-def profile_candidates(graph, cands, warmup=10, reps=50, flush_bytes=512 << 20, log=None, failures=None):
+def profile_candidates(graph, cands, warmup=10, reps=100, flush_bytes=512 << 20, log=None, failures=None, db=None):
     """Measured latency (us) of every candidate on the current device, None when
     no family implements it.  A candidate whose generated kernel fails to
-    compile also costs infinity; it is appended to ``failures`` when given."""
+    compile also costs infinity; it is appended to ``failures`` when given.
+    With a ``ProfileDB`` (``db``), candidates measured before under the same
+    protocol on the same kind of device are looked up instead of profiled, and
+    new measurements are recorded."""
     from ._abi import E_COMPILE, KorchError
     costs = []
     t0 = time.time()
+    dev = None
+    if db is not None:
+        from .profile_db import device_tag
+        dev = device_tag()
     for i, (p, o) in enumerate(cands):
+        key = None
+        if db is not None:
+            key = db.key(graph.kernel_source(p, o) if graph.family(p, o) != "none" else f"unsupported {p} {o}",
+                         warmup, reps, flush_bytes, dev)
+            found, val = db.get(key)
+            if found:
+                costs.append(val)
+                continue
         try:
-            costs.append(graph.profile(p, o, warmup=warmup, reps=reps, flush_bytes=flush_bytes))
+            c = graph.profile(p, o, warmup=warmup, reps=reps, flush_bytes=flush_bytes)
+            costs.append(c)
+            if db is not None:
+                db.put(key, c)
         except KorchError as e:
             if e.code != E_COMPILE:
                 raise
@@ -122,11 +140,13 @@ def profile_candidates(graph, cands, warmup=10, reps=50, flush_bytes=512 << 20, 
                 failures.append(((tuple(p), tuple(o)), str(e)[:300]))
         if log and (i + 1) % 50 == 0:
             log(f"profiled {i + 1}/{len(cands)} candidates ({time.time() - t0:.1f} s)")
+    if db is not None:
+        db.save()
     return costs
 
 
-def korch_plan(graph, max_prims=64, max_outs=3, warmup=10, reps=50, flush_bytes=512 << 20, log=None,
-               extra=()) -> Choice:
+def korch_plan(graph, max_prims=64, max_outs=3, warmup=10, reps=100, flush_bytes=512 << 20, log=None,
+               extra=(), db=None) -> Choice:
     """Enumerates the supported candidates of ``graph``, profiles them on the
     current device and returns the cheapest ordered plan.  ``extra`` adds
     kernels (e.g. those of hand-written plans) to the candidate set."""
@@ -138,7 +158,7 @@ def korch_plan(graph, max_prims=64, max_outs=3, warmup=10, reps=50, flush_bytes=
             seen.add(k)
             cands.append(k)
     failures = []
-    costs = profile_candidates(graph, cands, warmup, reps, flush_bytes, log, failures)
+    costs = profile_candidates(graph, cands, warmup, reps, flush_bytes, log, failures, db)
     ch = choose(GraphView(graph), cands, costs)
     ch.costs = {(tuple(p), tuple(o)): c for (p, o), c in zip(cands, costs) if c is not None}
     ch.failures = failures

@@ -25,8 +25,8 @@ void generate_plan(Plan& p);
 void load_plan(Plan& p);
 void destroy_plan_device(Plan& p);
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
-                  hipStream_t stream, int first, int count, int timed = -1, hipEvent_t ev_start = nullptr,
-                  hipEvent_t ev_stop = nullptr, void* counters = nullptr);
+                  hipStream_t stream, int first, int count, void* const* starts = nullptr,
+                  void* const* stops = nullptr, void* counters = nullptr);
 void execute_plan_noalloc(Plan& p, const void* const* inputs, void* const* outputs, hipStream_t stream);
 void compile_candidate(const Graph& g, const KernelDesc& kd);
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
@@ -440,8 +440,23 @@ int korch_plan_execute_timed(korch_plan* p, int32_t first, int32_t count, const 
     NEED(p);
     if (count < 0) fail(KORCH_E_ARG, "negative kernel count");
     if (timed < first || timed >= first + count) fail(KORCH_E_ARG, "timed kernel outside the launched range");
-    execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, first, count, timed,
-                 (hipEvent_t)start, (hipEvent_t)stop);
+    std::vector<void*> starts(p->p.kernels.size(), nullptr), stops(p->p.kernels.size(), nullptr);
+    if (timed >= 0 && timed < (int)starts.size()) {
+      starts[timed] = start;
+      stops[timed] = stop;
+    }
+    execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, first, count, starts.data(),
+                 stops.data());
+  });
+}
+
+int korch_plan_execute_events(korch_plan* p, const void* const* inputs, void* const* outputs, void* workspace,
+                              size_t workspace_bytes, void* stream, void* const* start_events,
+                              void* const* stop_events) {
+  return guard([&] {
+    NEED(p);
+    execute_plan(p->p, inputs, outputs, workspace, workspace_bytes, (hipStream_t)stream, 0, -1, start_events,
+                 stop_events);
   });
 }
 

@@ -35,6 +35,27 @@ __global__ void fill_kernel(void* __restrict__ p, size_t n, int dtype, uint64_t 
   }
 }
 
+// Reads `n` 16-byte words of `p` (bringing them into L2 and the Infinity
+// Cache, as a producing kernel leaves its output) without changing them; each
+// workgroup stores the XOR of what it read in sink[blockIdx.x], so the loads
+// are not dead.
+__global__ void touch_kernel(const uint4* __restrict__ p, size_t n, uint4* __restrict__ sink) {
+  __shared__ uint32_t red[256];
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  uint32_t acc = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    uint4 v = p[i];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t a = 0;
+    for (int t = 0; t < (int)blockDim.x; ++t) a ^= red[t];
+    sink[blockIdx.x] = make_uint4(a, 0, 0, 0);
+  }
+}
+
 // Zeroes `n` 16-byte words (clears counters without a memset node, so a
 // caller may capture the launch in a graph).
 __global__ void zero_kernel(uint4* __restrict__ p, size_t n) {
@@ -94,6 +115,17 @@ hipError_t launch_flush(void* p, size_t bytes, hipStream_t s) {
   size_t n = bytes / 16;
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(flush_kernel, dim3(4096), dim3(256), 0, s, (uint4*)p, n, 0x5a5a5a5au);
+  return hipGetLastError();
+}
+
+// `sink` holds kTouchBlocks 16-byte words.
+constexpr unsigned kTouchBlocks = 1024;
+size_t touch_sink_bytes() { return (size_t)kTouchBlocks * 16; }
+
+hipError_t launch_touch(const void* p, size_t bytes, void* sink, hipStream_t s) {
+  size_t n = bytes / 16;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(touch_kernel, dim3(kTouchBlocks), dim3(256), 0, s, (const uint4*)p, n, (uint4*)sink);
   return hipGetLastError();
 }
 

@@ -23,6 +23,8 @@ std::vector<char> rtc_compile(const std::string& src, const std::string& name);
 hipError_t launch_flush(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_fill(void* p, size_t n, int dtype, uint64_t seed, hipStream_t s);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_touch(const void* p, size_t bytes, void* sink, hipStream_t s);
+size_t touch_sink_bytes();
 size_t static_scratch_bytes();
 hipError_t static_scratch_setup(int dev);
 void* static_scratch_address(int dev);
@@ -119,8 +121,12 @@ void load_plan(Plan& p) {
 
 static bool aligned16(const void* q) { return ((uintptr_t)q & 15) == 0; }
 
+// Launches kernels [first, first + count) of the plan (count < 0: to the end).
+// starts[k] / stops[k] (arrays over all kernels of the plan, or NULL) are
+// events that take the start / end timestamps of kernel k's own dispatch.
+// `counters` replaces the plan's counter buffer when not NULL.
 void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void* ws, size_t ws_bytes,
-                  hipStream_t stream, int first, int count, int timed, hipEvent_t ev_start, hipEvent_t ev_stop,
+                  hipStream_t stream, int first, int count, void* const* starts, void* const* stops,
                   void* counters) {
   // Execution only launches: loading (code objects, the counter buffer) is
   // korch_plan_load's job, so nothing here allocates or synchronizes.
@@ -168,7 +174,9 @@ void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void
       }
     }
     void* params[] = {(void*)ptr};
-    if (k == timed && (ev_start || ev_stop)) {
+    hipEvent_t ev_start = starts ? (hipEvent_t)starts[k] : nullptr;
+    hipEvent_t ev_stop = stops ? (hipEvent_t)stops[k] : nullptr;
+    if (ev_start || ev_stop) {
       // the events take the timestamps of this kernel's own dispatch (no
       // separate marker packets in the stream)
       HIPCHECK(hipExtModuleLaunchKernel((hipFunction_t)ck.function, (uint32_t)(ck.gen.grid[0] * ck.gen.block[0]),
@@ -204,7 +212,7 @@ void execute_plan_noalloc(Plan& p, const void* const* inputs, void* const* outpu
     fail(KORCH_E_WORKSPACE, "plan needs " + std::to_string(p.ws_bytes) + " bytes of workspace; the static scratch holds " +
                                 std::to_string(ws_cap) + " (use korch_plan_execute with a caller workspace)");
   if (p.counter_bytes) HIPCHECK(launch_zero(base, p.counter_bytes, stream));
-  execute_plan(p, inputs, outputs, base + kStaticCounterBytes, ws_cap, stream, 0, -1, -1, nullptr, nullptr, base);
+  execute_plan(p, inputs, outputs, base + kStaticCounterBytes, ws_cap, stream, 0, -1, nullptr, nullptr, base);
 }
 
 // The candidate kernel as a stand-alone graph: its external tensors become
@@ -238,8 +246,21 @@ void compile_candidate(const Graph& g, const KernelDesc& kd) {
   compile_plan(p);
 }
 
+// True when node u is computed by a kernel (not a graph input, nor a view of one).
+static bool computed_in(const Graph& g, int u) {
+  while (g.is_view(u)) u = g.nodes[u].in[0];
+  return g.is_prim(u);
+}
+
+// With KORCH_PROFILE_COLD=1 intermediate inputs are left cold like graph inputs.
+static bool profile_warm_intermediates() {
+  const char* e = getenv("KORCH_PROFILE_COLD");
+  return !(e && e[0] == '1');
+}
+
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream) {
+  const bool warm_intermediates = profile_warm_intermediates();
   Plan p;
   p.name_prefix = "korch_cand";
   p.g = extract_subgraph(g, kd);
@@ -265,26 +286,41 @@ float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int re
   std::vector<float> times;
   try {
     uint64_t seed = 1;
-    for (int i : p.g.inputs) {
-      const Node& n = p.g.nodes[i];
-      void* q = alloc((size_t)numel(n.shape) * dtype_bytes(n.dtype));
+    // The stand-alone graph's inputs are the candidate's external producers,
+    // in order; those that are computed in the parent graph (not its inputs)
+    // are the tensors a preceding kernel of a plan has just written.
+    std::vector<int> ext = external_inputs(g, kd);
+    std::vector<std::pair<const void*, size_t>> warm_bufs;
+    for (size_t j = 0; j < p.g.inputs.size(); ++j) {
+      const Node& n = p.g.nodes[p.g.inputs[j]];
+      size_t bytes = (size_t)numel(n.shape) * dtype_bytes(n.dtype);
+      void* q = alloc(bytes);
       HIPCHECK(launch_fill(q, (size_t)numel(n.shape), n.dtype, seed++, stream));
       in.push_back(q);
+      if (warm_intermediates && j < ext.size() && computed_in(g, ext[j])) warm_bufs.push_back({q, bytes});
     }
+    void* sink = warm_bufs.empty() ? nullptr : alloc(touch_sink_bytes());
     for (int o : p.g.outputs) {
       const Node& n = p.g.nodes[o];
       out.push_back(alloc((size_t)numel(n.shape) * dtype_bytes(n.dtype)));
     }
     void* ws = p.ws_bytes ? alloc(p.ws_bytes) : nullptr;
     void* fl = flush_bytes ? alloc(flush_bytes) : nullptr;
-    for (int w = 0; w < warmup; ++w) execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr, nullptr);
-    ev = new hipEvent_t[2 * std::max(reps, 1)];
+    for (int w = 0; w < warmup; ++w)
+      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, nullptr, nullptr, nullptr);
+    ev = new hipEvent_t[2 * std::max(reps, 1)]();
     for (int r = 0; r < 2 * reps; ++r) HIPCHECK(hipEventCreate(&ev[r]));
+    // Each rep: the flush (evicts L2 and the Infinity Cache), a read of every
+    // intermediate input (in a plan its producer has just written it, so it
+    // sits in the caches while graph inputs come from HBM), then the kernel
+    // launched with a start and a stop event that take its own dispatch's
+    // timestamps (no marker packets, whose serialization would add a few
+    // microseconds to every candidate and bias the choice toward fewer kernels).
     for (int r = 0; r < reps; ++r) {
       if (fl) HIPCHECK(launch_flush(fl, flush_bytes, stream));
-      HIPCHECK(hipEventRecord(ev[2 * r], stream));
-      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, -1, nullptr, nullptr, nullptr);
-      HIPCHECK(hipEventRecord(ev[2 * r + 1], stream));
+      for (auto& b : warm_bufs) HIPCHECK(launch_touch(b.first, b.second, sink, stream));
+      execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, (void* const*)&ev[2 * r],
+                   (void* const*)&ev[2 * r + 1], nullptr);
     }
     HIPCHECK(hipStreamSynchronize(stream));
     for (int r = 0; r < reps; ++r) {

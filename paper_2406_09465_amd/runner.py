@@ -91,6 +91,23 @@ class PlanRunner:
         if rc:
             check(rc)
 
+    def event_arrays(self, starts, stops):
+        """C arrays (one entry per kernel) of the hipEvent_t handles of torch
+        events (each recorded once before, so that it exists) or None."""
+        n = self._nk if hasattr(self, "_nk") else self.plan.num_kernels()
+        a = (C.c_void_p * n)(*[e.cuda_event if e is not None else None for e in starts])
+        b = (C.c_void_p * n)(*[e.cuda_event if e is not None else None for e in stops])
+        return a, b
+
+    def launch_events_bound(self, arrays):
+        """One execution on the bound arguments with per-kernel dispatch events
+        (``arrays`` from ``event_arrays``): korch_plan_execute_events."""
+        h, ins, outs, ws, wsb, st = self._bound
+        rc = lib.korch_plan_execute_events(h, ins, outs, ws, wsb, st, C.cast(arrays[0], C.POINTER(C.c_void_p)),
+                                           C.cast(arrays[1], C.POINTER(C.c_void_p)))
+        if rc:
+            check(rc)
+
     def launch_timed_bound(self, timed, start, stop):
         """``launch_timed`` on the bound arguments (``start`` / ``stop``: torch events, each recorded once before)."""
         h, ins, outs, ws, wsb, st = self._bound

@@ -125,3 +125,49 @@ def test_cross_workgroup_handoff_repeats_bitwise(workload, plan):
         r.launch()
         torch.cuda.synchronize()
         assert all(torch.equal(a.view(it), b.view(it)) for a, b in zip(ref, r.outs))
+
+
+def test_execute_with_events_on_every_kernel():
+    """korch_plan_execute_events launches the same kernels as korch_plan_execute
+    (identical bytes); events on every kernel give positive durations that lie
+    inside the span from the first kernel's start to the last kernel's end, and
+    NULL entries are allowed."""
+    from paper_2406_09465_amd import graphs
+    from paper_2406_09465_amd.runner import PlanRunner
+    from synthetic import workloads as W
+    sizes = SIZES["mlp"]
+    w = graphs.build("mlp", **sizes)
+    print("\n[case] per-kernel events, mlp layered", flush=True)
+    r = PlanRunner(w, "layered")
+    r.set_inputs(W.inputs("mlp", **sizes))
+    r.launch()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in r.outs]
+    s = torch.cuda.current_stream()
+    r.bind(s)
+    nk = r.plan.num_kernels()
+    assert nk >= 2
+    st = [torch.cuda.Event(enable_timing=True) for _ in range(nk)]
+    en = [torch.cuda.Event(enable_timing=True) for _ in range(nk)]
+    for e in st + en:
+        e.record(s)
+    for t in r.outs:
+        t.zero_()
+    r.launch_events_bound(r.event_arrays(st, en))
+    torch.cuda.synchronize()
+    assert all(torch.equal(x, y) for x, y in zip(ref, r.outs))
+    span = st[0].elapsed_time(en[-1])
+    durs = [st[k].elapsed_time(en[k]) for k in range(nk)]
+    assert all(d > 0.0 for d in durs)
+    assert span >= max(durs) and span >= 0.9 * sum(durs)
+    for k in range(1, nk):
+        assert st[k - 1].elapsed_time(st[k]) >= 0.0  # kernels start in plan order
+    # only the first start and the last stop
+    a = [st[0]] + [None] * (nk - 1)
+    b = [None] * (nk - 1) + [en[-1]]
+    for t in r.outs:
+        t.zero_()
+    r.launch_events_bound(r.event_arrays(a, b))
+    torch.cuda.synchronize()
+    assert all(torch.equal(x, y) for x, y in zip(ref, r.outs))
+    assert st[0].elapsed_time(en[-1]) > 0.0
