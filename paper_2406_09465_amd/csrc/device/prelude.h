@@ -121,6 +121,12 @@ __device__ __forceinline__ void stv_out(T* base, i64 off, const float* s) {
     *reinterpret_cast<VT*>(base + off) = v;
   }
 }
+// 16 bytes already in the storage dtype, at byte offset `boff` of a kernel
+// output, with the same write-through policy.
+__device__ __forceinline__ void st16_out(void* base, i64 boff, uint4 v) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4o_, v), r, (unsigned)boff, 0, 16);
+}
 template <typename T> __device__ __forceinline__ void st1_out(T* base, i64 off, float v) {
   stv_out<1, T>(base, off, &v);
 }

@@ -904,7 +904,8 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
       s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) bf[j] = *(const " << V8 << "*)(Bb + (wn * "
         << sp.WTN << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
     s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n      for (int j = 0; j < "
-      << sp.FN << "; ++j) acc[i][j] = " << fn << "(af[i], bf[j], acc[i][j], 0, 0, 0);\n";
+      << sp.FN << "; ++j) acc[i][j] = " << fn << (sp.acc_t ? "(bf[j], af[i]" : "(af[i], bf[j]")
+      << ", acc[i][j], 0, 0, 0);\n";
   }
   s << "    }\n  };\n";
   // Register pipeline of NS stages over two LDS buffers: while tile t is
@@ -994,8 +995,90 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
 size_t gemm_smem_bytes(const GemmSpec& sp) {
   size_t bbuf = (size_t)b_buf_elems(sp);
   size_t ab = (size_t)2 * ((size_t)sp.BM * sp.BKP + bbuf) * dtype_bytes(sp.mtype);
+  if (sp.acc_t) return std::max(ab, (size_t)sp.OSB);
   size_t c = (size_t)(sp.CROWS ? sp.CROWS : sp.BM) * sp.LDC * 4;
   return std::max(ab, c);
+}
+
+int reg_epilogue_output(const KInfo& ki, const GemmSpec& sp) {
+  if (getenv("KORCH_GEMM_NO_REG_EPI") && atoi(getenv("KORCH_GEMM_NO_REG_EPI")) != 0) return -1;
+  const Graph& g = ki.g;
+  if (sp.conv || sp.mms.size() != 1 || sp.mtype == KORCH_F32 || sp.nmdims != 1 || !sp.rowred.empty() ||
+      !sp.side.empty() || (int)sp.OUT.size() != sp.nb + 2 || ki.k.outs.size() != 1)
+    return -1;
+  const int o = ki.k.outs[0];
+  const Node& on = g.nodes[o];
+  if (on.shape != sp.OUT || dtype_bytes(on.dtype) != 2 || sp.N % 8 || sp.BN % 8) return -1;
+  if (o != sp.mms[0] && !sp.epi.count(o)) return -1;
+  // every value the epilogue reads other than the product is the same along
+  // the rows (its dimension of the product's M axis is 1 or absent)
+  const size_t mdim = (size_t)sp.nb;
+  for (int v : sp.epi)
+    for (int u : g.nodes[v].in) {
+      if (sp.epi.count(u) || in_vec(sp.mms, u)) continue;
+      const Shape& s = g.nodes[u].shape;
+      const size_t lead = sp.OUT.size() - s.size();
+      if (s.size() >= sp.OUT.size() - mdim && s[mdim - lead] != 1) return -1;
+    }
+  return o;
+}
+
+std::string gemm_reg_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot, int o) {
+  const Graph& g = ki.g;
+  const Node& on = g.nodes[o];
+  const std::string OT = ctype(on.dtype);
+  Emitter em(g);
+  em.inset = sp.epi;
+  em.inset.insert(sp.mms[0]);
+  em.argslot = slot;
+  em.vec = 4;
+  std::vector<Ix> it;
+  for (int d = 0; d < sp.nb; ++d) it.push_back(Ix::var("z" + std::to_string(d)));
+  it.push_back(Ix::var("m"));
+  it.push_back(Ix::var("n", 1, 4));
+  const std::string pkey = Emitter::key(sp.mms[0], broadcast_index(g.nodes[sp.mms[0]].shape, sp.OUT, it));
+  em.provide = [&](int node, const std::vector<Ix>& idx, std::string* out) {
+    if (node != sp.mms[0]) return false;
+    if (Emitter::key(node, idx) != pkey) fail(KORCH_E_UNSUPPORTED, "gemm: epilogue reads the product at another index");
+    *out = "acc[i][j][e]";
+    return true;
+  };
+  const std::string v = em.value(o, broadcast_index(on.shape, sp.OUT, it));
+  // element offset of (z.., m, n) in the contiguous output
+  std::string zoff = "0";
+  for (int d = 0; d < sp.nb; ++d) zoff = "(" + zoff + ") * " + std::to_string(sp.OUT[d]) + "LL + z" + std::to_string(d);
+  std::ostringstream s;
+  s << "  " << OT << "* Os = (" << OT << "*)smem;  // output tile in its storage dtype\n";
+  // waves beyond WM x WN only stage operands and hold no accumulators
+  if (sp.WM * sp.WN < sp.NT / 64) s << "  if (wave < " << sp.WM * sp.WN << ")\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
+    << "; ++j) {\n";
+  s << "    const int ml = wm * " << sp.WTM << " + i * 16 + (l & 15), nl = wn * " << sp.WTN << " + j * 16 + 4 * (l >> 4);\n";
+  s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
+  s << "    float _o[4] = {0.0f, 0.0f, 0.0f, 0.0f};\n";
+  s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n" << em.pre.str();
+  s << "#pragma unroll\n      for (int e = 0; e < 4; ++e) {\n" << em.body.str() << "        _o[e] = " << v << ";\n      }\n";
+  s << "    }\n";
+  s << "    typedef " << OT << " OT4 __attribute__((ext_vector_type(4)));\n";
+  s << "    *(OT4*)(Os + ml * " << sp.OSP << " + nl) = OT4{(" << OT << ")_o[0], (" << OT << ")_o[1], (" << OT << ")_o[2], ("
+    << OT << ")_o[3]};\n";
+  s << "  }\n  __syncthreads();\n";
+  const int vr = sp.BN / 8;  // 16-byte vectors per tile row
+  const bool big = (double)numel(on.shape) * 2 >= 2147483648.0 ||
+                   (getenv("KORCH_OUT_PLAIN") && atoi(getenv("KORCH_OUT_PLAIN")) != 0);
+  s << "  for (int s_ = tid; s_ < " << sp.BM * vr << "; s_ += " << sp.NT << ") {\n";
+  s << "    const int ml = s_ / " << vr << ", nl = (s_ % " << vr << ") * 8;\n";
+  s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
+  s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n";
+  s << "      const uint4 v_ = *(const uint4*)(Os + ml * " << sp.OSP << " + nl);\n";
+  s << "      const i64 off = ((" << zoff << ") * " << sp.M << "LL + m) * " << sp.N << "LL + n;\n";
+  std::string P = "((" + OT + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])";
+  if (big)
+    s << "      *(uint4*)(" << P << " + off) = v_;\n";
+  else
+    s << "      st16_out(" << P << ", off * 2, v_);\n";
+  s << "    }\n  }\n";
+  return s.str();
 }
 
 // Pointwise epilogue over the C tile: every kernel output at (batch, m, n).
@@ -1152,6 +1235,12 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   const bool ksplit = !sp.conv && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 && sp.NT == 256 &&
                       ksplit_lds <= 160 * 1024 && !getenv("KORCH_GEMM_NO_KSPLIT");
   const int64_t KH = (KT + 1) / 2;
+  const int repi_out = ksplit ? -1 : reg_epilogue_output(ki, sp);
+  if (repi_out >= 0) {
+    sp.acc_t = true;
+    sp.OSP = sp.BN + 8;
+    sp.OSB = sp.BM * sp.OSP * 2;
+  }
   std::ostringstream s;
   s << source_header((int)gk.args.size());
   if (ksplit) {
@@ -1219,6 +1308,9 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
     ep.NT = 512;
     s << gemm_epilogue(ki, ep, slot, "ml * " + std::to_string(sp.LDC));
     s << "  }\n";
+  } else if (sp.acc_t) {
+    s << mfma_mainloop(sp, "", KT, true, false);
+    s << gemm_reg_epilogue(ki, sp, slot, repi_out);
   } else if (sp.CROWS && sp.CROWS < sp.BM) {
     // The C tile passes through LDS one band of wave rows at a time (waves
     // with wm == p write rows [p*WTM, (p+1)*WTM), then every thread runs the

@@ -48,6 +48,13 @@ struct GemmSpec {
   // branch-free buffer loads): LDS writes and global loads per thread and
   // k-tile; 0 leaves the instruction order to the compiler.
   int sched_w = 0, sched_g = 0;
+  // Transposed accumulators: the MFMAs take the right operand's fragment as
+  // their first source, so lane l of 16 x 16 block (i, j) holds row l % 16 and
+  // the four consecutive columns 4 (l / 16) .. + 3 (the register epilogue).
+  bool acc_t = false;
+  // Register epilogue: output staging tile in LDS (elements per row; 0 = none).
+  int OSP = 0;
+  int OSB = 0;  // its bytes
 };
 
 // LDS element offset of row k of the [k][n] right-operand tile.
@@ -90,6 +97,14 @@ bool conv_direct_fits(const GemmSpec& sp, std::string* why);
 bool conv_uses_direct(const GemmSpec& sp, std::string* why);
 GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index);
 std::string gemm_prologue_common(const GemmSpec& sp);
+// Register epilogue of a single product whose kernel has one output of the
+// product's shape in a 16-bit dtype and whose epilogue reads, besides the
+// product, only values that are the same along the product's rows (per-column
+// vectors, scalars): the output is evaluated on the accumulators themselves
+// (transposed layout), staged once in LDS in its storage dtype and stored as
+// 16-byte rows.  Returns the output node, or -1 when the case does not apply.
+int reg_epilogue_output(const KInfo& ki, const GemmSpec& sp);
+std::string gemm_reg_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot, int out);
 size_t gemm_smem_bytes(const GemmSpec& sp);
 
 }  // namespace korch
