@@ -2,8 +2,8 @@
 
 One step = one execution of the whole plan (every kernel of the fused
 orchestration) on inputs already resident in HBM.  Before every timed step a
-512 MiB device write evicts L2 and the Infinity Cache (the workloads' working
-sets would otherwise stay cache-resident); the step's latency is the span from
+read of a 512 MiB device buffer evicts L2 and the Infinity Cache (the
+workloads' working sets would otherwise stay cache-resident); the step's latency is the span from
 its first kernel's dispatch start to its last kernel's dispatch end, taken by
 events attached to those dispatches.  `value` is the median over the timed
 steps (p10 / p90 beside it); the same plan back to back without flushes is
@@ -67,7 +67,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused-plan comparison")
     ap.add_argument("--flush-mib", type=int, default=512,
-                    help="bytes written before every timed step to evict L2 and the Infinity Cache")
+                    help="MiB streamed through before every timed step to evict L2 and the Infinity Cache")
+    ap.add_argument("--flush-write", action="store_true",
+                    help="the flush writes its buffer (leaving dirty lines) instead of reading it")
     ap.add_argument("--profile-reps", type=int, default=100, help="timed launches per candidate in the chooser")
     ap.add_argument("--no-profile-db", action="store_true",
                     help="profile every candidate again instead of reusing latencies recorded in the profile database")
@@ -132,17 +134,39 @@ def pct(xs):
     return {"n": len(ys), "p10_us": q(0.1), "median_us": round(statistics.median(ys), 3), "p90_us": q(0.9)}
 
 
+class Flush:
+    """Cold-cache precondition: korch_flush_caches over a device buffer (a
+    read by default; a write with write=True), enqueued on the stream."""
+
+    def __init__(self, mib, stream, write=False):
+        import ctypes as C
+
+        import torch
+
+        from paper_2406_09465_amd._abi import lib
+        self.buf = torch.empty(max(1, mib) << 20, dtype=torch.uint8, device="cuda")
+        self.args = (C.c_void_p(self.buf.data_ptr()), C.c_size_t(self.buf.numel()), C.c_int32(1 if write else 0),
+                     C.c_void_p(stream.cuda_stream))
+        self.lib = lib
+
+    def __call__(self):
+        rc = self.lib.korch_flush_caches(*self.args)
+        if rc:
+            from paper_2406_09465_amd._abi import check
+            check(rc)
+
+
 def timed_steps(r, steps, flush, stream):
     """Runs `steps` executions of the bound plan of runner `r` on `stream`.
-    Before each one, when `flush` (a device byte tensor) is given, it is
-    overwritten, outside the measured span.  Every execution carries an event
-    on the start of its first kernel's dispatch and one on the end of every
-    kernel's dispatch (end-of-dispatch events add nothing to the span; a
-    start event on a later kernel adds a few microseconds, so none is used).
-    Returns the spans (first kernel's start to last kernel's end, us), each
-    kernel's duration in every execution (us; kernel k > 0: from the end of
-    kernel k - 1 to its own end, i.e. including the dispatch gap in front of
-    it), and the wall time of the loop (s)."""
+    Before each one, when `flush` (a Flush) is given, it runs, outside the
+    measured span.  Every execution carries an event on the start of its first
+    kernel's dispatch and one on the end of every kernel's dispatch
+    (end-of-dispatch events add nothing to the span; a start event on a later
+    kernel adds a few microseconds, so none is used).  Returns the spans (first
+    kernel's start to last kernel's end, us), each kernel's duration in every
+    execution (us; kernel k > 0: from the end of kernel k - 1 to its own end,
+    i.e. including the dispatch gap in front of it), and the wall time of the
+    loop (s)."""
     import torch
     nk = r.plan.num_kernels()
     recs = []
@@ -154,9 +178,9 @@ def timed_steps(r, steps, flush, stream):
         recs.append((st, en, r.event_arrays(st, en)))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i, (_, _, arr) in enumerate(recs):
+    for _, _, arr in recs:
         if flush is not None:
-            flush.fill_(i & 0xFF)
+            flush()
         r.launch_events_bound(arr)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -184,6 +208,8 @@ def main():
     from synthetic import workloads as W
 
     torch.cuda.set_device(0)
+    if args.flush_write:
+        os.environ["KORCH_FLUSH_WRITE"] = "1"  # the profiler's flush then writes too
     w = graphs.build(args.workload)
     chosen = None
     if args.kernels_json:
@@ -253,8 +279,9 @@ def main():
         del src, dst
 
     # warm-up, then the timed region: exactly `steps` plan executions.  Before
-    # every step a write of `flush_mib` MiB (outside the measured span) evicts
-    # L2 and the Infinity Cache, so the step reads its inputs from HBM.  A step's
+    # every step a read of `flush_mib` MiB of a scratch buffer (outside the
+    # measured span) evicts L2 and the Infinity Cache, so the step reads its
+    # inputs from HBM.  A step's
     # latency is the span from its first kernel's dispatch start to its last
     # kernel's dispatch end, taken by events that the library attaches to those
     # dispatches (no marker packets); end-of-dispatch events on every kernel
@@ -262,7 +289,7 @@ def main():
     for _ in range(args.warmup):
         r.launch()
     r.bind(stream)
-    flush = torch.empty(max(1, args.flush_mib) << 20, dtype=torch.uint8, device="cuda") if args.flush_mib else None
+    flush = Flush(args.flush_mib, stream, args.flush_write) if args.flush_mib else None
     res = timed_steps(r, args.steps, flush, stream)
     spans = res["spans"]
     per = res["per_kernel"]
@@ -276,6 +303,15 @@ def main():
         more = timed_steps(r, 200 - args.steps, flush, stream)["spans"]
         d2 = pct(spans + more)
         dist["n200"] = {k_: d2[k_] for k_ in ("n", "p10_us", "median_us", "p90_us")}
+    # the other cold precondition: a flush that writes (the step's misses then
+    # also write back the flush buffer's dirty lines)
+    other = None
+    if args.flush_mib:
+        oflush = Flush(args.flush_mib, stream, not args.flush_write)
+        o = timed_steps(r, 100, oflush, stream)
+        other = dict(pct(o["spans"]), flush="write" if not args.flush_write else "read",
+                     kernels_median_us=[round(statistics.median(x), 3) for x in o["per_kernel"]])
+        del oflush
     # the same plan back to back without flushes (warm caches)
     warm = timed_steps(r, max(args.steps, 50), None, stream)
     warm_d = pct(warm["spans"])
@@ -365,9 +401,12 @@ def main():
         "data": "synthetic",
         "config": {"workload": DESCR[args.workload], "plan": "recorded" if args.kernels_json else args.plan,
                    "kernels": nk},
-        "timing": dict(dist, protocol=f"each step after a {args.flush_mib} MiB write (outside the span); span = first "
-                                         "kernel's dispatch start to last kernel's dispatch end; value = median",
+        "timing": dict(dist, protocol=f"each step after a {args.flush_mib} MiB "
+                                         f"{'write' if args.flush_write else 'read'} of a scratch buffer (outside the "
+                                         "span; evicts L2 and the Infinity Cache); span = first kernel's dispatch start "
+                                         "to last kernel's dispatch end; value = median",
                        wall_s_with_flushes=round(res["wall_s"], 4)),
+        "timing_other_flush": other,
         "warm": warm_d,
         "roofline": roof,
         "unfused": unfused,

@@ -303,9 +303,9 @@ int korch_compile_candidate(const korch_graph* g, const korch_kernel_desc* k);
 
 /* Times the single kernel (P', O) in isolation: compiles it, fills its inputs
    with seeded uniform values in [0.5, 1.5) in device buffers the profiler allocates, runs
-   `warmup` untimed launches, then `reps` launches each preceded by a write of
-   `flush_bytes` to a scratch buffer (to evict L2 and the Infinity Cache) and
-   a read of every input that the parent graph computes (in a plan, the
+   `warmup` untimed launches, then `reps` launches each preceded by a read of
+   `flush_bytes` of a scratch buffer (korch_flush_caches; environment
+   KORCH_FLUSH_WRITE=1 writes it instead) and a read of every input that the parent graph computes (in a plan, the
    producing kernel has just written such a tensor, so it is cache-resident,
    while graph inputs come from HBM; environment KORCH_PROFILE_COLD=1 skips
    that read), each launch timed by HIP events that take that dispatch's own
@@ -314,6 +314,17 @@ int korch_compile_candidate(const korch_graph* g, const korch_kernel_desc* k);
    KORCH_E_UNSUPPORTED (cost infinity) when no family implements it. */
 int korch_profile_candidate(const korch_graph* g, const korch_kernel_desc* k, int32_t warmup, int32_t reps,
                             size_t flush_bytes, void* stream, float* median_us);
+
+/* Cold-cache precondition of a measurement (Section 5.2 times kernels in
+   isolation; here they must find their inputs in HBM).  Enqueues on `stream`
+   one kernel that streams through the first `bytes` (rounded down to 16) of
+   the caller's device buffer `buffer` (16-byte aligned, at least 512 MiB to
+   cover L2 and the 256 MB Infinity Cache): a read when write = 0, after which
+   the caches hold clean lines of `buffer` (dirty lines present before are
+   written back during this kernel), else a write, after which they hold dirty
+   lines that a following kernel's misses must write back.  Asynchronous;
+   KORCH_E_ALIGN for a misaligned buffer. */
+int korch_flush_caches(void* buffer, size_t bytes, int32_t write, void* stream);
 
 #ifdef __cplusplus
 }

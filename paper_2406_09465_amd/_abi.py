@@ -106,6 +106,7 @@ _SIGS = {
     "korch_plan_workspace_bytes": ([_P, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute": ([_P, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
     "korch_plan_execute_noalloc": ([_P, C.POINTER(_P), C.POINTER(_P), _P], C.c_int),
+    "korch_flush_caches": ([_P, C.c_size_t, _I, _P], C.c_int),
     "korch_plan_execute_events": ([_P, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P, C.POINTER(_P), C.POINTER(_P)],
                                   C.c_int),
     "korch_plan_execute_kernels": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),

@@ -29,6 +29,7 @@ void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void
                   void* const* stops = nullptr, void* counters = nullptr);
 void execute_plan_noalloc(Plan& p, const void* const* inputs, void* const* outputs, hipStream_t stream);
 void compile_candidate(const Graph& g, const KernelDesc& kd);
+void flush_caches(void* buf, size_t bytes, int write, hipStream_t stream);
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream);
 }  // namespace korch
@@ -545,6 +546,14 @@ int korch_compile_candidate(const korch_graph* g, const korch_kernel_desc* k) {
     std::string why;
     if (match_family(g->g, kd, &why) == KORCH_FAM_NONE) fail(KORCH_E_UNSUPPORTED, why);
     compile_candidate(g->g, kd);
+  });
+}
+
+int korch_flush_caches(void* buffer, size_t bytes, int32_t write, void* stream) {
+  return guard([&] {
+    if (bytes && !buffer) fail(KORCH_E_ARG, "null flush buffer");
+    if (((uintptr_t)buffer & 15) != 0) fail(KORCH_E_ALIGN, "flush buffer must be 16-byte aligned");
+    flush_caches(buffer, bytes, write ? 1 : 0, (hipStream_t)stream);
   });
 }
 

@@ -7,10 +7,25 @@
 
 namespace {
 
-// Streams `n` 16-byte words into `p`, evicting L2 and the Infinity Cache.
+// Streams `n` 16-byte words into `p`, evicting L2 and the Infinity Cache
+// (and leaving them full of dirty lines of `p`).
 __global__ void flush_kernel(uint4* __restrict__ p, size_t n, uint32_t v) {
   size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = make_uint4(v, i, v, i);
+}
+
+// Reads `n` 16-byte words of `p`, evicting L2 and the Infinity Cache (whose
+// dirty lines are written back during this kernel) and leaving them full of
+// clean lines.  The loaded words are folded into one value that is stored
+// (into p[0]) only when it equals an arbitrary constant, so the loads stay live.
+__global__ void read_flush_kernel(uint4* __restrict__ p, size_t n) {
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  uint32_t a = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint4 v = p[i];
+    a ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  if (a == 0x9e3779b9u) p[0] = make_uint4(a, a, a, a);
 }
 
 __device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
@@ -111,10 +126,15 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_flush(void* p, size_t bytes, hipStream_t s) {
+// Evicts L2 and the Infinity Cache through `bytes` of the device buffer `p`:
+// a read of it (write = 0), after which the caches hold clean lines, or a write.
+hipError_t launch_flush(void* p, size_t bytes, int write, hipStream_t s) {
   size_t n = bytes / 16;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(flush_kernel, dim3(4096), dim3(256), 0, s, (uint4*)p, n, 0x5a5a5a5au);
+  if (write)
+    hipLaunchKernelGGL(flush_kernel, dim3(4096), dim3(256), 0, s, (uint4*)p, n, 0x5a5a5a5au);
+  else
+    hipLaunchKernelGGL(read_flush_kernel, dim3(4096), dim3(256), 0, s, (uint4*)p, n);
   return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ extern "C" hipError_t hipExtModuleLaunchKernel(hipFunction_t f, uint32_t globalW
 namespace korch {
 
 std::vector<char> rtc_compile(const std::string& src, const std::string& name);
-hipError_t launch_flush(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_flush(void* p, size_t bytes, int write, hipStream_t s);
 hipError_t launch_fill(void* p, size_t n, int dtype, uint64_t seed, hipStream_t s);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_touch(const void* p, size_t bytes, void* sink, hipStream_t s);
@@ -195,6 +195,10 @@ void execute_plan(Plan& p, const void* const* inputs, void* const* outputs, void
 // The counters this plan uses are cleared by a fill kernel first (stream
 // ordered, no memset node), since the scratch keeps whatever the last call
 // on this device left there.
+void flush_caches(void* buf, size_t bytes, int write, hipStream_t stream) {
+  HIPCHECK(launch_flush(buf, bytes, write, stream));
+}
+
 void execute_plan_noalloc(Plan& p, const void* const* inputs, void* const* outputs, hipStream_t stream) {
   if (!p.loaded) fail(KORCH_E_STATE, "plan is not loaded: call korch_plan_load on this device first");
   int dev = 0;
@@ -252,6 +256,14 @@ static bool computed_in(const Graph& g, int u) {
   return g.is_prim(u);
 }
 
+// With KORCH_FLUSH_WRITE=1 the flush before each timed launch writes its
+// buffer instead of reading it (the caches are then full of dirty lines,
+// whose write-back the timed kernel pays for).
+int profile_flush_write() {
+  const char* e = getenv("KORCH_FLUSH_WRITE");
+  return e && e[0] == '1' ? 1 : 0;
+}
+
 // With KORCH_PROFILE_COLD=1 intermediate inputs are left cold like graph inputs.
 static bool profile_warm_intermediates() {
   const char* e = getenv("KORCH_PROFILE_COLD");
@@ -261,6 +273,7 @@ static bool profile_warm_intermediates() {
 float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int reps, size_t flush_bytes,
                         hipStream_t stream) {
   const bool warm_intermediates = profile_warm_intermediates();
+  const int flush_write = profile_flush_write();
   Plan p;
   p.name_prefix = "korch_cand";
   p.g = extract_subgraph(g, kd);
@@ -317,7 +330,7 @@ float profile_candidate(const Graph& g, const KernelDesc& kd, int warmup, int re
     // timestamps (no marker packets, whose serialization would add a few
     // microseconds to every candidate and bias the choice toward fewer kernels).
     for (int r = 0; r < reps; ++r) {
-      if (fl) HIPCHECK(launch_flush(fl, flush_bytes, stream));
+      if (fl) HIPCHECK(launch_flush(fl, flush_bytes, flush_write, stream));
       for (auto& b : warm_bufs) HIPCHECK(launch_touch(b.first, b.second, sink, stream));
       execute_plan(p, in.data(), out.data(), ws, p.ws_bytes, stream, 0, -1, (void* const*)&ev[2 * r],
                    (void* const*)&ev[2 * r + 1], nullptr);

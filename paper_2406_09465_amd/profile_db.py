@@ -47,13 +47,14 @@ class ProfileDB:
 
     # Version of the measurement protocol (korch_profile_candidate): a change in
     # how a candidate is timed invalidates every record.
-    PROTOCOL = "dispatch-timestamps/flush-each-rep/warm-intermediates/median/v2"
+    PROTOCOL = "dispatch-timestamps/flush-each-rep/warm-intermediates/median/v3"
 
     @staticmethod
     def key(source, warmup, reps, flush_bytes, device):
         h = hashlib.sha256()
         cold = os.environ.get("KORCH_PROFILE_COLD", "") == "1"
-        for part in (ProfileDB.PROTOCOL, "cold" if cold else "warm", source, str(warmup), str(reps),
+        wflush = os.environ.get("KORCH_FLUSH_WRITE", "") == "1"
+        for part in (ProfileDB.PROTOCOL, "cold" if cold else "warm", "wflush" if wflush else "rflush", source, str(warmup), str(reps),
                      str(flush_bytes), device):
             h.update(part.encode())
             h.update(b"\0")

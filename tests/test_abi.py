@@ -435,3 +435,13 @@ def test_runtime_compiler_helper(tmp_path):
     r = subprocess.run([helper, str(bad), "k", str(tmp_path / "bad.co"), str(tmp_path / "bad.log"), *opts],
                        capture_output=True, text=True, timeout=300)
     assert r.returncode == 1 and "undeclared_name" in (tmp_path / "bad.log").read_text()
+
+
+def test_flush_rejects_bad_buffers_before_any_device_call():
+    """korch_flush_caches checks its arguments on the host: a null buffer
+    (with a size) and a misaligned one are refused without launching."""
+    import ctypes as C
+
+    from paper_2406_09465_amd._abi import lib
+    assert lib.korch_flush_caches(None, C.c_size_t(1 << 20), 0, None) == -1  # KORCH_E_ARG
+    assert lib.korch_flush_caches(C.c_void_p(0x1008), C.c_size_t(1 << 20), 1, None) == -21  # KORCH_E_ALIGN

@@ -171,3 +171,22 @@ def test_execute_with_events_on_every_kernel():
     torch.cuda.synchronize()
     assert all(torch.equal(x, y) for x, y in zip(ref, r.outs))
     assert st[0].elapsed_time(en[-1]) > 0.0
+
+
+def test_cache_flush_read_and_write():
+    """korch_flush_caches: the read flush leaves its buffer unchanged, the
+    write flush overwrites it; both run on the caller's stream."""
+    import ctypes as C
+
+    from paper_2406_09465_amd._abi import lib
+    print("\n[case] cache flush", flush=True)
+    buf = torch.arange(1 << 20, dtype=torch.int32, device="cuda")  # 4 MiB
+    ref = buf.clone()
+    s = torch.cuda.current_stream()
+    nb = buf.numel() * 4
+    assert lib.korch_flush_caches(C.c_void_p(buf.data_ptr()), C.c_size_t(nb), 0, C.c_void_p(s.cuda_stream)) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(buf, ref)
+    assert lib.korch_flush_caches(C.c_void_p(buf.data_ptr()), C.c_size_t(nb), 1, C.c_void_p(s.cuda_stream)) == 0
+    torch.cuda.synchronize()
+    assert not torch.equal(buf, ref)
