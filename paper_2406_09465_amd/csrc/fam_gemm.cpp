@@ -926,6 +926,63 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
   };
   const bool unrolled = kconst > 0 && kconst <= 128;
   const int NS = unrolled ? sp.NS : 2;
+  // Split k-steps across the barrier: the fragments of a tile's last k-step
+  // are read before the barrier that publishes the next tile's staging, and
+  // that k-step's MFMAs run after it while the next tile's first fragments are
+  // read, so no wave waits on LDS reads with the matrix cores idle after the
+  // barrier.  Two fragment register sets alternate (even k-steps per tile).
+  const int nkk = sp.BK / sp.kstep;
+  const bool split_steps = unrolled && !f32 && hook.empty() && nkk >= 2 && nkk % 2 == 0 && sp.split_steps;
+  if (split_steps) {
+    const std::string V8 = sp.mtype == KORCH_F16 ? "f16x8" : "bf16x8";
+    const std::string fn = sp.mtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16"
+                                                 : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
+    s << "  " << V8 << " af0[" << sp.FM << "], bf0[" << sp.FN << "], af1[" << sp.FM << "], bf1[" << sp.FN << "];\n";
+    for (int h = 0; h < 2; ++h) {
+      const std::string H = std::to_string(h);
+      s << "  auto frag" << H << " = [&](const int buf, const int kk) {\n";
+      s << "    const " << T << "* Ab = As + buf * " << sp.BM * sp.BKP << ";\n";
+      s << "    const " << T << "* Bb = Bs + buf * " << bbuf << ";\n";
+      s << "#pragma unroll\n    for (int i = 0; i < " << sp.FM << "; ++i) af" << H << "[i] = *(const " << V8 << "*)(Ab + (wm * "
+        << sp.WTM << " + i * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
+      if (sp.b_kn)
+        s << "#pragma unroll\n    for (int j = 0; j < " << sp.FN << "; ++j) bf" << H << "[j] = __builtin_bit_cast(" << V8
+          << ", lds_tr_k8(Bb + (kk * 32 + (l >> 4) * 8 + ((l & 15) >> 2)) * " << sp.BNP
+          << (sp.BSH ? " + (kk * 4 + (l >> 4)) * " + std::to_string(sp.BSH) : std::string()) << " + wn * " << sp.WTN
+          << " + j * 16 + 4 * (l & 3), " << sp.BNP << "));\n";
+      else
+        s << "#pragma unroll\n    for (int j = 0; j < " << sp.FN << "; ++j) bf" << H << "[j] = *(const " << V8
+          << "*)(Bb + (wn * " << sp.WTN << " + j * 16 + (l & 15)) * " << sp.BKP << " + kk * 32 + (l >> 4) * 8);\n";
+      s << "  };\n";
+      s << "  auto mma" << H << " = [&]() {\n#pragma unroll\n    for (int i = 0; i < " << sp.FM
+        << "; ++i)\n#pragma unroll\n    for (int j = 0; j < " << sp.FN << "; ++j) acc[i][j] = " << fn
+        << (sp.acc_t ? "(bf" + H + "[j], af" + H + "[i]" : "(af" + H + "[i], bf" + H + "[j]") << ", acc[i][j], 0, 0, 0);\n  };\n";
+    }
+    for (int st = 0; st < NS; ++st)
+      s << "  fetchA(" << clampk("kt0 + " + std::to_string(st)) << ", " << st << "); fetchB("
+        << clampk("kt0 + " + std::to_string(st)) << ", " << st << ");\n";
+    s << "  stashA(0, 0, " << clampk("kt0") << "); stashB(0, 0, " << clampk("kt0") << ");\n  __syncthreads();\n";
+    s << "  " << wguard << "frag0(0, 0);\n";
+    std::string live = kconst_exact ? "" : "if (kt < kt1) ";
+    s << "#pragma unroll\n  for (int j = 0; j < " << kconst << "; ++j) {\n";
+    s << "    const int kt = kt0 + j, b_ = j & 1, s_ = j % " << NS << ", sn_ = (j + 1) % " << NS << ";\n";
+    s << "    fetchA(" << clampk("kt + " + std::to_string(NS)) << ", s_); fetchB(" << clampk("kt + " + std::to_string(NS))
+      << ", s_);\n";
+    s << "    " << live << wguard << "{\n";
+    for (int kk = 0; kk + 1 < nkk; ++kk) {
+      const int cur = kk % 2, nxt = (kk + 1) % 2;
+      s << "      frag" << nxt << "(b_, " << kk + 1 << ");\n      mma" << cur << "();\n";
+    }
+    s << "    }\n";
+    s << "    stashA(1 - b_, sn_, " << clampk("kt + 1") << "); stashB(1 - b_, sn_, " << clampk("kt + 1") << ");\n";
+    s << "    __syncthreads();\n";
+    // after the barrier: the next tile's first fragments, then this tile's last k-step
+    s << "    " << wguard << "{\n";
+    s << "      if (j + 1 < " << kconst << ") frag0(1 - b_, 0);\n";
+    s << "      " << live << "mma" << (nkk - 1) % 2 << "();\n";
+    s << "    }\n";
+    s << "  }\n";
+  } else {
   for (int st = 0; st < NS; ++st)
     s << "  fetchA(" << clampk("kt0 + " + std::to_string(st)) << ", " << st << "); fetchB("
       << clampk("kt0 + " + std::to_string(st)) << ", " << st << ");\n";
@@ -981,6 +1038,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
     s << "    if (kt + 1 >= kt1) break;\n";
     s << step("1", "(kt + 1)");
     s << "  }\n";
+  }
   }
   if (!ctile) return s.str();
   // accumulators -> LDS C tile (fp32)
@@ -1235,6 +1293,10 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   const bool ksplit = !sp.conv && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 && sp.NT == 256 &&
                       ksplit_lds <= 160 * 1024 && !getenv("KORCH_GEMM_NO_KSPLIT");
   const int64_t KH = (KT + 1) / 2;
+  {
+    const char* e = getenv("KORCH_GEMM_SPLIT_STEPS");
+    sp.split_steps = !(e && atoi(e) == 0);
+  }
   const int repi_out = ksplit ? -1 : reg_epilogue_output(ki, sp);
   if (repi_out >= 0) {
     sp.acc_t = true;

@@ -52,6 +52,8 @@ struct GemmSpec {
   // their first source, so lane l of 16 x 16 block (i, j) holds row l % 16 and
   // the four consecutive columns 4 (l / 16) .. + 3 (the register epilogue).
   bool acc_t = false;
+  // Main loop with each tile's last k-step after the barrier (see mfma_mainloop).
+  bool split_steps = false;
   // Register epilogue: output staging tile in LDS (elements per row; 0 = none).
   int OSP = 0;
   int OSB = 0;  // its bytes
