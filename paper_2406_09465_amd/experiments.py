@@ -73,7 +73,7 @@ def fewest_kernels(view, cands, costs):
     return n, ch.cost_us - n * big
 
 
-def shapes(workload, out, warmup=10, reps=50):
+def shapes(workload, out, warmup=10, reps=100):
     jobs = [(workload, sz) for sz in SWEEPS[workload]]
     t0 = time.time()
     precompile(jobs)
@@ -81,7 +81,8 @@ def shapes(workload, out, warmup=10, reps=50):
              "Command:", "", "```", f"python -m paper_2406_09465_amd.experiments shapes --workload {workload} "
              f"--out {out}", "```", "",
              f"Candidates compiled in {time.time() - t0:.0f} s. Costs are medians of {reps} launches after "
-             f"{warmup} warm-up launches, each after a 512 MiB cache flush.", "",
+             f"{warmup} warm-up launches, each timed by its own dispatch after a read of 512 MiB (cold caches) and "
+             "a read of its computed inputs (cache-resident, as a producing kernel leaves them).", "",
              "| sizes | candidates | chosen kernels | chosen cost (us) | fewest kernels | their cost (us) | chosen plan |",
              "|---|---|---|---|---|---|---|"]
     for sz in SWEEPS[workload]:
@@ -99,14 +100,14 @@ def shapes(workload, out, warmup=10, reps=50):
     open(out, "w").write("\n".join(lines) + "\n")
 
 
-def layouts(out, workloads=None, warmup=10, reps=50):
+def layouts(out, workloads=None, warmup=10, reps=100):
     from ._abi import RW_LAYOUT_VARIANTS
     from .warm import LAYOUT_WORKLOADS
     wls = list(workloads or LAYOUT_WORKLOADS)
     lines = ["# Data layout as a plan variable", "", "Command:", "", "```",
              f"python -m paper_2406_09465_amd.experiments layouts --out {out}", "```", "",
-             f"Full-size workloads; costs are medians of {reps} launches after {warmup} warm-up launches, each after a "
-             "512 MiB cache flush.  `x^T` is tensor x stored with its last two axes swapped.", "",
+             f"Full-size workloads; costs are medians of {reps} launches after {warmup} warm-up launches, each timed "
+             "by its own dispatch after a read of 512 MiB (cold caches) and a read of its computed inputs.  `x^T` is tensor x stored with its last two axes swapped.", "",
              "| workload | original graph (us, kernels) | variant graph (us, kernels) | layouts chosen | "
              "cheapest plan storing only x^T, per variant (us) |", "|---|---|---|---|---|"]
     for wl in wls:

@@ -3,6 +3,10 @@
   python -m paper_2406_09465_amd.profsum stats <rocprof dir> <out.md> --cmd "<command>"
       kernel-trace statistics (*_kernel_stats.csv) as a markdown table.
 
+  python -m paper_2406_09465_amd.profsum counters <pmc dir>... --out <out.md> --cmd "<command>"...
+      MFMA / LDS counters (SQ_VALU_MFMA_BUSY_CYCLES, SQ_LDS_BANK_CONFLICT, ...)
+      of a plan's kernels with the derived utilisations.
+
   python -m paper_2406_09465_amd.profsum pmc --workload mlp --fetch <dir> --write <dir>
          --calib-mib 256 --out profiles/pmc_traffic.json --cmd-fetch "..." --cmd-write "..."
       FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of every kernel of the
@@ -105,6 +109,67 @@ def pmc(args):
     open(md, "w").write("\n".join(lines) + "\n")
 
 
+def _dispatches(d):
+    """{(dispatch id, kernel name): {counter: value, "_ns": duration}} of a --pmc run."""
+    out = {}
+    for r in _rows(d, "*counter_collection.csv"):
+        k = (r["Dispatch_Id"], r["Kernel_Name"])
+        e = out.setdefault(k, {})
+        e[r["Counter_Name"]] = float(r["Counter_Value"])
+        e["_ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    return out
+
+
+def counters(args):
+    """MFMA and LDS counters of a plan's kernels (medians over dispatches) from
+    --pmc runs, with the derived utilisations.  SQ counters are totals over
+    the whole GPU; SQ_VALU_MFMA_BUSY_CYCLES counts 16 cycles per 16x16x32 MFMA
+    on its SIMD; GRBM_GUI_ACTIVE sums the busy cycles of the 8 XCDs."""
+    per = {}
+    for d in args.dirs:
+        for (_, name), e in _dispatches(d).items():
+            if not name.startswith(args.prefix):
+                continue
+            for c, v in e.items():
+                per.setdefault(name, {}).setdefault(c, []).append(v)
+    med = {k: {c: statistics.median(v) for c, v in cs.items()} for k, cs in per.items()}
+    lines = [f"# {args.title}", "", "Commands (one rocprofv3 pass per counter group):", "", "```"] + args.cmd + ["```", "",
+             f"Medians over the dispatches of each kernel (durations are those under counter collection, longer "
+             f"than in the timed bench).  `MFMA busy` = SQ_VALU_MFMA_BUSY_CYCLES / ({args.simds} SIMDs x "
+             f"{args.ghz} GHz x duration), the matrix cores' busy fraction against the nominal clock of the "
+             "published peak; `MFMA TFLOP/s` = SQ_INSTS_VALU_MFMA_MOPS_F16 (+ _BF16) x 512 / duration.  `LDS "
+             "conflict` = SQ_LDS_BANK_CONFLICT / SQ_ACTIVE_INST_LDS (stall cycles per LDS-instruction cycle).  `wait "
+             "LDS`, `wait any`, `VALU active` = SQ_WAIT_INST_LDS, SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_VALU / "
+             "SQ_WAVE_CYCLES (shares of the waves' lifetime).", ""]
+    cols = ["kernel", "duration us", "MFMA busy", "MFMA TFLOP/s", "LDS conflict", "wait LDS", "wait any",
+            "VALU active"]
+    lines += ["| " + " | ".join(cols) + " |", "|" + "---|" * len(cols)]
+    for k in sorted(med):
+        m = med[k]
+        dur = m.get("_ns", 0.0) / 1e3
+        busy = m.get("SQ_VALU_MFMA_BUSY_CYCLES")
+        mops = m.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) + m.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+        wave = m.get("SQ_WAVE_CYCLES")
+
+        def f(x, fmt="{:.3f}"):
+            return fmt.format(x) if x is not None else ""
+
+        def share(c):
+            return m[c] / wave if wave and c in m else None
+        row = [k, f(dur, "{:.2f}"),
+               f(busy / (args.simds * args.ghz * 1e3 * dur) if busy is not None and dur else None),
+               f(mops * 512 / (dur * 1e-6) / 1e12 if mops and dur else None, "{:.0f}"),
+               f(m["SQ_LDS_BANK_CONFLICT"] / m["SQ_ACTIVE_INST_LDS"] if m.get("SQ_ACTIVE_INST_LDS") else None),
+               f(share("SQ_WAIT_INST_LDS")), f(share("SQ_WAIT_INST_ANY")), f(share("SQ_ACTIVE_INST_VALU"))]
+        lines.append("| " + " | ".join(row) + " |")
+    lines += ["", "Raw medians:", "", "| kernel | counter | value |", "|---|---|---|"]
+    for k in sorted(med):
+        for c in sorted(med[k]):
+            if c != "_ns":
+                lines.append(f"| {k} | {c} | {med[k][c]:.0f} |")
+    open(args.out, "w").write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="mode", required=True)
@@ -123,8 +188,16 @@ def main():
     p.add_argument("--cmd-fetch", default="")
     p.add_argument("--cmd-write", default="")
     p.add_argument("--bench-json", default="", help="bench.py output line whose chosen_plan to use")
+    c = sub.add_parser("counters")
+    c.add_argument("dirs", nargs="+")
+    c.add_argument("--out", required=True)
+    c.add_argument("--title", default="MFMA and LDS counters")
+    c.add_argument("--prefix", default="korch_k")
+    c.add_argument("--simds", type=int, default=1024)
+    c.add_argument("--ghz", type=float, default=2.4)
+    c.add_argument("--cmd", action="append", default=[])
     a = ap.parse_args()
-    stats(a) if a.mode == "stats" else pmc(a)
+    {"stats": stats, "pmc": pmc, "counters": counters}[a.mode](a)
 
 
 if __name__ == "__main__":
