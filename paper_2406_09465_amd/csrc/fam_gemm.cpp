@@ -1113,13 +1113,20 @@ std::string gemm_reg_epilogue(const KInfo& ki, const GemmSpec& sp, const std::ma
     << "; ++j) {\n";
   s << "    const int ml = wm * " << sp.WTM << " + i * 16 + (l & 15), nl = wn * " << sp.WTN << " + j * 16 + 4 * (l >> 4);\n";
   s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
+  // tiles that divide the problem need no bounds checks; without the
+  // per-block branch the compiler interleaves the blocks' epilogue chains
+  const bool full = sp.M % sp.BM == 0 && sp.N % sp.BN == 0;
+  const std::string inb = full ? "true" : "m < " + std::to_string(sp.M) + "LL && n < " + std::to_string(sp.N) + "LL";
   s << "    float _o[4] = {0.0f, 0.0f, 0.0f, 0.0f};\n";
-  s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n" << em.pre.str();
+  s << "    if (" << inb << ") {\n" << em.pre.str();
   s << "#pragma unroll\n      for (int e = 0; e < 4; ++e) {\n" << em.body.str() << "        _o[e] = " << v << ";\n      }\n";
   s << "    }\n";
   s << "    typedef " << OT << " OT4 __attribute__((ext_vector_type(4)));\n";
   s << "    *(OT4*)(Os + ml * " << sp.OSP << " + nl) = OT4{(" << OT << ")_o[0], (" << OT << ")_o[1], (" << OT << ")_o[2], ("
     << OT << ")_o[3]};\n";
+  // one block at a time: hoisting every block's chain (no branch separates
+  // them) would need more registers than a wave has and spill
+  s << "    __builtin_amdgcn_sched_barrier(0);\n";
   s << "  }\n  __syncthreads();\n";
   const int vr = sp.BN / 8;  // 16-byte vectors per tile row
   const bool big = (double)numel(on.shape) * 2 >= 2147483648.0 ||
@@ -1127,7 +1134,7 @@ std::string gemm_reg_epilogue(const KInfo& ki, const GemmSpec& sp, const std::ma
   s << "  for (int s_ = tid; s_ < " << sp.BM * vr << "; s_ += " << sp.NT << ") {\n";
   s << "    const int ml = s_ / " << vr << ", nl = (s_ % " << vr << ") * 8;\n";
   s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
-  s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n";
+  s << "    if (" << inb << ") {\n";
   s << "      const uint4 v_ = *(const uint4*)(Os + ml * " << sp.OSP << " + nl);\n";
   s << "      const i64 off = ((" << zoff << ") * " << sp.M << "LL + m) * " << sp.N << "LL + n;\n";
   std::string P = "((" + OT + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])";
@@ -1150,6 +1157,8 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
   while (VE > 1 && (sp.N % VE || sp.BN % VE)) VE /= 2;
   int cols = (int)std::min<int64_t>(sp.BN, sp.mms.size() > 1 ? sp.N : sp.BN);
   cols = (cols + VE - 1) / VE * VE;
+  // every column a tile covers lies inside the product (no check needed)
+  const bool n_full = sp.mms.size() > 1 ? cols == sp.N : sp.N % sp.BN == 0;
   Emitter em(g);
   em.inset = sp.epi;
   for (int m : sp.mms) em.inset.insert(m);
@@ -1239,10 +1248,17 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
   if (conv_tw > 0) {
     // C tile row ml is pixel (ml / conv_tw, ml % conv_tw) of a 2-D output tile at (ty0, tx0)
     s << "    const i64 oy = ty0 + ml / " << conv_tw << ", ox = tx0 + ml % " << conv_tw << ", n = n0 + nl;\n";
-    s << "    if (oy < " << sp.Ho << "LL && ox < " << sp.Wo << "LL && n < " << sp.N << "LL) {\n";
+    std::string c;
+    if (sp.Ho % (rows / conv_tw)) c += "oy < " + std::to_string(sp.Ho) + "LL";
+    if (sp.Wo % conv_tw) c += std::string(c.empty() ? "" : " && ") + "ox < " + std::to_string(sp.Wo) + "LL";
+    if (!n_full) c += std::string(c.empty() ? "" : " && ") + "n < " + std::to_string(sp.N) + "LL";
+    s << "    if (" << (c.empty() ? "true" : c) << ") {\n";
   } else {
     s << "    const i64 m = m0 + ml, n = n0 + nl;\n";
-    s << "    if (m < " << sp.M << "LL && n < " << sp.N << "LL) {\n";
+    std::string c;
+    if (sp.M % sp.BM) c += "m < " + std::to_string(sp.M) + "LL";
+    if (!n_full) c += std::string(c.empty() ? "" : " && ") + "n < " + std::to_string(sp.N) + "LL";
+    s << "    if (" << (c.empty() ? "true" : c) << ") {\n";
     if (sp.conv) s << "      const i64 oy = m / " << sp.Wo << "LL, ox = m % " << sp.Wo << "LL;\n";
   }
   s << cvload.str() << em.pre.str() << decl.str();
