@@ -291,6 +291,11 @@ int korch_plan_kernel_info(const korch_plan* p, int32_t k, int32_t* family, doub
 /* Generated HIP source and kernel symbol name of kernel k (after compile). */
 int korch_plan_kernel_source(const korch_plan* p, int32_t k, char* buf, size_t cap, size_t* len);
 int korch_plan_kernel_name(const korch_plan* p, int32_t k, char* buf, size_t cap);
+/* The gfx950 code object (ELF) of kernel k after korch_plan_compile: copies
+   min(cap, size) bytes to `buf` (may be NULL) and stores the size in *len (may
+   be NULL).  Its AMDGPU metadata note states the kernel's registers, LDS and
+   private (scratch) segment.  KORCH_E_STATE before compilation. */
+int korch_plan_kernel_code(const korch_plan* p, int32_t k, void* buf, size_t cap, size_t* len);
 /* Launch geometry of kernel k (after compile). */
 int korch_plan_kernel_launch(const korch_plan* p, int32_t k, int32_t grid[3], int32_t block[3], int32_t* lds_bytes);
 

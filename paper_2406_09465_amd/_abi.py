@@ -111,6 +111,7 @@ _SIGS = {
                                   C.c_int),
     "korch_plan_execute_kernels": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P], C.c_int),
     "korch_kernel_source": ([_P, _P, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
+    "korch_plan_kernel_code": ([_P, _I, _P, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
     "korch_plan_execute_timed": ([_P, _I, _I, C.POINTER(_P), C.POINTER(_P), _P, C.c_size_t, _P, _I, _P, _P], C.c_int),
     "korch_plan_kernel_info": ([_P, _I, C.POINTER(_I), C.POINTER(C.c_double), C.POINTER(C.c_double)], C.c_int),
     "korch_plan_kernel_source": ([_P, _I, C.c_char_p, C.c_size_t, C.POINTER(C.c_size_t)], C.c_int),
@@ -414,6 +415,14 @@ class Plan:
         buf = C.create_string_buffer(n.value + 1)
         check(lib.korch_plan_kernel_source(self.h, int(k), buf, n.value + 1, None))
         return buf.value.decode()
+
+    def kernel_code(self, k):
+        """The compiled gfx950 code object (ELF bytes) of kernel k."""
+        n = C.c_size_t()
+        check(lib.korch_plan_kernel_code(self.h, int(k), None, 0, C.byref(n)))
+        buf = C.create_string_buffer(max(n.value, 1))
+        check(lib.korch_plan_kernel_code(self.h, int(k), buf, n.value, None))
+        return buf.raw[:n.value]
 
     def kernel_name(self, k):
         buf = C.create_string_buffer(256)

@@ -509,6 +509,17 @@ int korch_plan_kernel_source(const korch_plan* p, int32_t k, char* buf, size_t c
   });
 }
 
+int korch_plan_kernel_code(const korch_plan* p, int32_t k, void* buf, size_t cap, size_t* len) {
+  return guard([&] {
+    NEED(p);
+    if (!p->p.compiled) fail(KORCH_E_STATE, "plan is not compiled");
+    if (k < 0 || k >= (int)p->p.ck.size()) fail(KORCH_E_ARG, "kernel index out of range");
+    const std::vector<char>& c = p->p.ck[k].code;
+    if (len) *len = c.size();
+    if (buf && cap) memcpy(buf, c.data(), std::min(cap, c.size()));
+  });
+}
+
 int korch_plan_kernel_name(const korch_plan* p, int32_t k, char* buf, size_t cap) {
   return guard([&] {
     NEED(p);

@@ -76,6 +76,12 @@ std::string binary_expr(int op, const std::string& x, const std::string& y);
 // variants (set per generated kernel; thread-local).
 void set_fast_math(bool on);
 bool fast_math();
+// Register relief (thread-local, set while a kernel is regenerated because
+// its first code object spilled registers to scratch): families that can
+// trade speed for fewer live registers do so at levels 1, 2, ...
+void set_reg_relief(int level);
+int reg_relief();
+constexpr int kMaxRegRelief = 2;
 // The fissioned Mish pattern rooted at `node` (a product); returns its input or -1.
 int mish_operand(const Graph& g, const std::set<int>& inset, int node);
 

@@ -168,6 +168,9 @@ std::string flit(double v) {
 thread_local bool g_fast_math = false;
 
 void set_fast_math(bool on) { g_fast_math = on; }
+thread_local int g_reg_relief = 0;
+void set_reg_relief(int level) { g_reg_relief = level; }
+int reg_relief() { return g_reg_relief; }
 bool fast_math() { return g_fast_math; }
 
 std::string unary_expr(int op, const std::string& x) {

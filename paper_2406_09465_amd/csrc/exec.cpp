@@ -60,19 +60,57 @@ void generate_plan(Plan& p) {
 // Kernels are compiled on the calling thread: hipRTC runs in a link namespace
 // of its own with its own C library, whose per-thread state does not cover
 // threads created by the process's main C library.
+// Bytes of private (scratch) memory per lane that a single-kernel code object
+// declares: the value of ".private_segment_fixed_size" in its AMDGPU metadata
+// note (a msgpack map; the key is a 27-byte fixstr, the value a msgpack
+// unsigned integer).  Registers spilled by the compiler live there.
+int64_t code_scratch_bytes(const std::vector<char>& code) {
+  static const std::string key = std::string(1, (char)0xbb) + ".private_segment_fixed_size";
+  auto it = std::search(code.begin(), code.end(), key.begin(), key.end());
+  if (it == code.end()) return 0;
+  size_t i = (size_t)(it - code.begin()) + key.size();
+  auto byte = [&](size_t j) -> uint64_t { return j < code.size() ? (uint8_t)code[j] : 0; };
+  const uint64_t b = byte(i);
+  if (b < 0x80) return (int64_t)b;
+  int n = b == 0xcc ? 1 : b == 0xcd ? 2 : b == 0xce ? 4 : b == 0xcf ? 8 : 0;
+  uint64_t v = 0;
+  for (int j = 1; j <= n; ++j) v = v << 8 | byte(i + j);
+  return (int64_t)v;
+}
+
 void compile_plan(Plan& p) {
   if (p.compiled) return;
   generate_plan(p);
   int n = (int)p.ck.size();
+  bool regenerated = false;
   for (int k = 0; k < n; ++k) {
     try {
       p.ck[k].code = rtc_compile(p.ck[k].gen.source, p.ck[k].gen.name);
+      // A kernel that spills registers to scratch is generated again with
+      // more register relief (its family's cheaper configuration) until it
+      // fits or the levels run out.
+      for (int level = 1; level <= kMaxRegRelief && code_scratch_bytes(p.ck[k].code) > 0; ++level) {
+        set_kernel_prefix(p.name_prefix);
+        set_reg_relief(level);
+        try {
+          p.ck[k].gen = generate_kernel(p.g, p.ck[k].desc, k);
+        } catch (...) {
+          set_reg_relief(0);
+          set_kernel_prefix("korch_k");
+          throw;
+        }
+        set_reg_relief(0);
+        set_kernel_prefix("korch_k");
+        p.ck[k].code = rtc_compile(p.ck[k].gen.source, p.ck[k].gen.name);
+        regenerated = true;
+      }
     } catch (Error& e) {
       fail(e.code, "kernel " + std::to_string(k) + ": " + e.what());
     } catch (std::exception& e) {
       fail(KORCH_E_COMPILE, "kernel " + std::to_string(k) + ": " + e.what());
     }
   }
+  if (regenerated) plan_workspace(p);  // a regenerated kernel may take other scratch arguments
   p.compiled = true;
 }
 

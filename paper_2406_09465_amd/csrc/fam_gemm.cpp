@@ -251,7 +251,9 @@ void choose_tiles(GemmSpec& sp, bool split) {
       for (int bn : {128, 96, 64, 192}) {
         if (bn == 96 && sp.N % 96 != 0) continue;
         if (bn == 192 && (sp.N % 192 != 0 || f32 || bm == 64)) continue;
-        if (bm == 256 && (bn != 192 || (sp.M + 255) / 256 * (sp.N / 192) * sp.batch < 256)) continue;
+        // register relief 2: no 256-row tiles (eight waves of 64 x 96 accumulators)
+        if (bm == 256 && (bn != 192 || (sp.M + 255) / 256 * (sp.N / 192) * sp.batch < 256 || reg_relief() >= 2))
+          continue;
         int64_t tiles = (sp.M + bm - 1) / bm * ((sp.N + bn - 1) / bn) * sp.batch;
         double rounds = (double)((tiles + 255) / 256);
         double cost = rounds * bm * bn * (1.0 + 24.0 * (1.0 / bm + 1.0 / bn));
@@ -1310,8 +1312,10 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
                       ksplit_lds <= 160 * 1024 && !getenv("KORCH_GEMM_NO_KSPLIT");
   const int64_t KH = (KT + 1) / 2;
   {
+    // register relief 1: a tile's k-steps all before the barrier (one set of
+    // fragment registers)
     const char* e = getenv("KORCH_GEMM_SPLIT_STEPS");
-    sp.split_steps = !(e && atoi(e) == 0);
+    sp.split_steps = !(e && atoi(e) == 0) && reg_relief() < 1;
   }
   const int repi_out = ksplit ? -1 : reg_epilogue_output(ki, sp);
   if (repi_out >= 0) {

@@ -445,3 +445,38 @@ def test_flush_rejects_bad_buffers_before_any_device_call():
     from paper_2406_09465_amd._abi import lib
     assert lib.korch_flush_caches(None, C.c_size_t(1 << 20), 0, None) == -1  # KORCH_E_ARG
     assert lib.korch_flush_caches(C.c_void_p(0x1008), C.c_size_t(1 << 20), 1, None) == -21  # KORCH_E_ALIGN
+
+
+@pytest.mark.parametrize("workload", list(graphs.BUILDERS))
+def test_standard_plan_kernels_do_not_spill(workload):
+    """No generated kernel of a workload's hand-written and unfused plans keeps
+    registers in scratch memory (its code object's private segment is empty):
+    a kernel whose first build spills is generated again with register relief."""
+    from paper_2406_09465_amd import codeobj
+    w = graphs.build(workload)
+    for plan in ("fused", "layered", "unfused"):
+        p = w.plan(plan)
+        p.compile()
+        for k in range(p.num_kernels()):
+            for name, r in codeobj.kernel_resources(p.kernel_code(k)).items():
+                assert r["scratch"] == 0 and r["vgpr_spill"] == 0, (workload, plan, name, r)
+                assert r["vgpr"] <= 512 and r["lds"] <= 160 * 1024
+
+
+def test_spilling_kernel_is_regenerated_with_register_relief():
+    """The MLP's fused plan puts LayerNorm's apply step in the first product's
+    operand prologue; with 256 x 192 tiles and two fragment register sets that
+    kernel spills, so compilation regenerates it (one fragment set, then
+    smaller tiles) until its code object needs no scratch."""
+    import re
+
+    from paper_2406_09465_amd import codeobj
+    w = graphs.build("mlp")
+    p = w.plan("fused")
+    first = p.kernel_source(1)  # generated, not yet compiled
+    p.compile()
+    final = p.kernel_source(1)
+    assert "frag1(" in first and final != first
+    (r,) = codeobj.kernel_resources(p.kernel_code(1)).values()
+    assert r["scratch"] == 0
+    assert re.search(r"__launch_bounds__\((\d+)\)", final).group(1) == "256"  # 128-row tiles, four waves
