@@ -80,7 +80,7 @@ bool plan_direct(const GemmSpec& sp, Direct& d, std::string* why) {
   d.TH = 128 / d.TW;
   d.HR = d.TH + (int)sp.KH - 1;
   d.HC = d.TW + (int)sp.KW - 1;
-  d.CPP = d.CP + 8;  // odd number of 16-byte slots per pixel: 16 consecutive pixels hit distinct banks
+  d.CPP = d.CP + 16;  // pitch an odd multiple of 32 bytes: a 16-byte read of 16 pixels is free of bank conflicts
   d.CV = d.CP / 8;
   d.HV = d.HR * d.HC * d.CV;
   d.HPT = (d.HV + 255) / 256;

@@ -313,7 +313,11 @@ void choose_tiles(GemmSpec& sp, bool split) {
   sp.FN = sp.WTN / 16;
   sp.VA = 16 / dtype_bytes(sp.mtype);
   sp.VB = sp.VA;
-  sp.BKP = sp.BK + (f32 ? 4 : 8);
+  // Row pitch of k-contiguous operand tiles.  A fragment read (16 rows x four
+  // consecutive 16-byte slots, one 16-byte vector per lane) is free of bank
+  // conflicts on gfx950 when the pitch is an odd multiple of 32 bytes; odd
+  // multiples of 16 bytes cost four extra cycles per read (measured).
+  sp.BKP = sp.BK + (f32 ? 4 : 16);
   sp.LDC = sp.BN + 4;
 }
 
@@ -865,6 +869,239 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
   return s.str();
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS staging.
+//
+// A wave's `global_load_lds_dwordx4` moves 16 bytes per lane from global
+// memory into 1 KiB of LDS at a wave-uniform address (lane i at +16 i), with
+// no register round trip and no LDS write instruction; it is counted by
+// vmcnt.  Measured on this part: a stream of LDS writes (ds_write_b128 of
+// staged registers) runs at about 75 bytes per clock per compute unit
+// whatever the lane-to-address mapping, and competes with the fragment reads;
+// the same data staged by direct loads leaves the reads almost undisturbed.
+//
+// Layouts (16-bit operands, k-tiles of 64, one stage = A then B):
+//   A [BM rows][64 k]: row r's 16-byte chunk c at position c ^ (r & 7).  One
+//     load covers 8 rows, each lane fetching the chunk its position holds;
+//     every 4 lanes still cover one aligned 64-byte segment of a row.  A
+//     fragment read (16 rows x 4 chunks, 16 bytes per lane) then touches 16
+//     distinct 16-byte bank groups per half-wave pair of lane octets.
+//   B [64 k][BN n]: row k's chunk c at c ^ f(k), f chosen below; rows are BN
+//     elements apart with no padding, so the stage is contiguous.
+// The loads are issued from inline assembly (M0 holds the LDS address; no
+// other code in these kernels uses M0): the compiler cannot tell the two
+// stages apart and would otherwise wait for the next tile's loads before
+// every fragment read of the current tile.  The waits are explicit (see
+// dma_mainloop).
+
+// XOR masks of the right operand's chunk index: f keeps every chunk inside its
+// row and puts the two 16-byte chunks that each row of a half-wave of
+// transposing reads touches (rows {0..3, 8..11} + 4 h of a 16-row block, the
+// same chunk pair for all of them) on 16 distinct 16-byte bank groups of the
+// 256-byte bank cycle.  f may not use bit 2 of k: the two reads of one
+// fragment are 4 rows apart and share f.
+static bool dma_b_swizzle(int P, int& x0, int& x1, int& x3) {
+  static const int vals[] = {0, 2, 4, 6, 8, 10, 12, 14};
+  for (int a : vals)
+    for (int b : vals)
+      for (int c : vals) {
+        auto f = [&](int k) { return a * (k & 1) + b * ((k >> 1) & 1) + c * ((k >> 3) & 1); };
+        bool ok = true;
+        for (int k = 0; k < 16 && ok; ++k)
+          for (int ch = 0; ch < P && ok; ++ch)
+            if ((ch ^ f(k)) >= P) ok = false;
+        for (int h = 0; h < 2 && ok; ++h)
+          for (int c0 = 0; c0 + 1 < P && ok; c0 += 2) {
+            bool used[16] = {};
+            for (int r : {0, 1, 2, 3, 8, 9, 10, 11}) {
+              const int k = r + 4 * h, u = (k * P + (c0 ^ f(k))) % 16;
+              for (int d = 0; d < 2 && ok; ++d) {
+                const int uu = (u + d) % 16;
+                if (used[uu]) ok = false;
+                used[uu] = true;
+              }
+            }
+          }
+        if (ok) {
+          x0 = a, x1 = b, x3 = c;
+          return true;
+        }
+      }
+  return false;
+}
+
+static std::string dma_fk(const GemmSpec& sp, const std::string& k) {
+  std::string r;
+  auto term = [&](int x, const std::string& bit) {
+    if (!x) return;
+    r += std::string(r.empty() ? "" : " + ") + std::to_string(x) + " * " + bit;
+  };
+  term(sp.dx0, "((" + k + ") & 1)");
+  term(sp.dx1, "(((" + k + ") >> 1) & 1)");
+  term(sp.dx3, "(((" + k + ") >> 3) & 1)");
+  return r.empty() ? "0" : "(" + r + ")";
+}
+
+void plan_dma(const KInfo& ki, GemmSpec& sp, bool ksplit) {
+  sp.dma = false;
+  const char* e = getenv("KORCH_GEMM_DMA");
+  if (e && atoi(e) == 0) return;
+  if (sp.conv || ksplit || sp.mms.size() != 1 || sp.Bs.size() != 1 || !sp.b_kn) return;
+  if (sp.mtype != KORCH_F16 && sp.mtype != KORCH_BF16) return;
+  if (ki.in.count(sp.A) || ki.in.count(sp.Bs[0])) return;  // operands computed in the kernel
+  if (sp.BK != 64 || sp.K % 64 || sp.M % sp.BM || sp.N % sp.BN || sp.BN % 16) return;
+  if (sp.WM * sp.WN * 64 != sp.NT) return;  // every wave multiplies
+  const int NW = sp.NT / 64;
+  // a third right-operand stage (loaded two k-tiles ahead by wave groups of
+  // their own) when it fits and the waves split into the three loading groups
+  sp.dsb = (size_t)(2 * sp.BM + 3 * sp.BN) * 64 * 2 <= 160 * 1024 && sp.K / 64 >= 3 && NW % 4 == 0 &&
+                   (sp.BM / 8) % (NW / 2) == 0 && (sp.BN / 8) % (NW / 4) == 0 && !getenv("KORCH_GEMM_DMA_2STAGE")
+               ? 3
+               : 2;
+  if (sp.dsb == 2 && ((sp.BM / 8) % NW || (sp.BN / 8) % NW)) return;  // equal load counts per wave
+  if ((size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * 2 > 160 * 1024) return;
+  int x0 = 0, x1 = 0, x3 = 0;
+  if (!dma_b_swizzle(sp.BN / 8, x0, x1, x3)) return;
+  sp.dx0 = x0, sp.dx1 = x1, sp.dx3 = x3;
+  sp.dma = true;
+}
+
+// Which waves load what.  With two right-operand stages every wave loads
+// blocks of both operands for the next k-tile (wave w: blocks w, w + NW, ...)
+// and waits for all its loads before the barrier that ends the tile.  With
+// three, the right operand is loaded two k-tiles ahead: waves [0, NW/2) load
+// the left operand (one tile ahead), waves [NW/2, 3NW/4) the right operand's
+// even k-tiles and waves [3NW/4, NW) its odd ones.  Each wave then waits
+// (vmcnt 0) only at the end of a tile whose successor it loaded, when every
+// load it has in flight is needed.  Partial waits (vmcnt > 0) are never used:
+// direct-to-LDS loads were seen to complete out of issue order (a partial
+// wait let a tile be read before its last loads had landed).
+struct DmaRoles {
+  int NW, ga, gb;   // waves; waves loading A; waves per B parity group
+  int PA, PB;       // blocks per loading wave
+};
+static DmaRoles dma_roles(const GemmSpec& sp) {
+  DmaRoles r;
+  r.NW = sp.NT / 64;
+  if (sp.dsb == 3) {
+    r.ga = r.NW / 2, r.gb = r.NW / 4;
+  } else {
+    r.ga = r.NW, r.gb = r.NW;
+  }
+  r.PA = sp.BM / 8 / r.ga;
+  r.PB = sp.BN / 8 / r.gb;
+  return r;
+}
+
+// Per-wave load offsets and the staging lambdas `dmaA_(kt, st)` and
+// `dmaB_(kt, st)` (each called only by the waves that load that operand).
+static std::string dma_loader(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot) {
+  const Graph& g = ki.g;
+  const std::string T = ctype(sp.mtype);
+  const DmaRoles R = dma_roles(sp);
+  const int P = sp.BN / 8;
+  const int64_t SAE = (int64_t)sp.BM * 64, SBE = (int64_t)sp.BN * 64, BOFF = 2 * SAE;
+  auto boff = [&](int node) {
+    const Shape& sh = g.nodes[node].shape;
+    Shape ob(sp.OUT.begin(), sp.OUT.begin() + sp.nb);
+    Shape nbsh(sh.begin(), sh.end() - 2);
+    std::vector<Ix> zc;
+    for (int d = 0; d < sp.nb; ++d) zc.push_back(Ix::var("z" + std::to_string(d)));
+    auto bi = broadcast_index(nbsh, ob, zc);
+    auto st = strides_of(sh);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], st[d], 1));
+    return off.at();
+  };
+  std::ostringstream s;
+  s << "  // direct-to-LDS staging: " << sp.BM / 8 << " A blocks and " << sp.BN / 8 << " B blocks of 1 KiB per k-tile, "
+    << "2 A stages and " << sp.dsb << " B stages\n";
+  s << "  const int wv_ = __builtin_amdgcn_readfirstlane(wave);\n";
+  if (sp.dsb == 3) {
+    s << "  const int wa_ = wv_, wb_ = (wv_ - " << R.ga << ") % " << R.gb << ", par_ = (wv_ - " << R.ga << ") / " << R.gb
+      << ";  // A loader index; B loader index and k-tile parity\n";
+  } else {
+    s << "  const int wa_ = wv_, wb_ = wv_;\n";
+  }
+  s << "  const unsigned lds0_ = (unsigned)(size_t)(__attribute__((address_space(3))) void*)smem;\n";
+  s << "  const " << T << "* Ag_ = (const " << T << "*)a.p[" << slot.at(sp.A) << "] + (" << boff(sp.A) << ");\n";
+  s << "  const " << T << "* Bg_ = (const " << T << "*)a.p[" << slot.at(sp.Bs[0]) << "] + (" << boff(sp.Bs[0]) << ");\n";
+  s << "  i64 doffA_[" << R.PA << "], doffB_[" << R.PB << "];  // element offset of this lane's chunk at k-tile 0\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << R.PA << "; ++i) {\n";
+  s << "    const int r = 8 * (wa_ + i * " << R.ga << ") + (l >> 3);\n";
+  s << "    doffA_[i] = (m0 + r) * " << sp.K << "LL + (((l & 7) ^ (l >> 3)) * 8);\n  }\n";
+  s << "#pragma unroll\n  for (int i = 0; i < " << R.PB << "; ++i) {\n";
+  s << "    const int q = (wb_ + i * " << R.gb << ") * 64 + l, k = q / " << P << ", p = q % " << P << ";\n";
+  s << "    doffB_[i] = (i64)k * " << sp.N << "LL + n0 + ((p ^ " << dma_fk(sp, "k") << ") * 8);\n  }\n";
+  const char* ld = "      asm volatile(\"s_mov_b32 m0, %1\\n\\tglobal_load_lds_dwordx4 %0, off\" :: \"v\"(src), \"s\"(la) : \"memory\", \"m0\");\n";
+  s << "  auto dmaA_ = [&](const int kt, const int st) {\n#pragma unroll\n    for (int i = 0; i < " << R.PA << "; ++i) {\n";
+  s << "      const " << T << "* src = Ag_ + (i64)kt * 64 + doffA_[i];\n";
+  s << "      const unsigned la = lds0_ + (unsigned)((st * " << SAE << " + (wa_ + i * " << R.ga << ") * 512) * 2);\n" << ld;
+  s << "    }\n  };\n";
+  s << "  auto dmaB_ = [&](const int kt, const int st) {\n#pragma unroll\n    for (int i = 0; i < " << R.PB << "; ++i) {\n";
+  s << "      const " << T << "* src = Bg_ + (i64)kt * " << 64 * sp.N << "LL + doffB_[i];\n";
+  s << "      const unsigned la = lds0_ + (unsigned)((" << BOFF << " + st * " << SBE << " + (wb_ + i * " << R.gb
+    << ") * 512) * 2);\n" << ld;
+  s << "    }\n  };\n";
+  return s.str();
+}
+
+// Main loop over the k-tiles with direct-to-LDS staging.  A tile j + 1 goes to
+// the A stage tile j - 1 used and B tile j + dsb - 1 to the B stage tile j - 1
+// used; both are issued as tile j's products start.
+static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
+  std::ostringstream s;
+  const std::string T = ctype(sp.mtype);
+  const std::string V8 = sp.mtype == KORCH_F16 ? "f16x8" : "bf16x8";
+  const std::string fn = sp.mtype == KORCH_F16 ? "__builtin_amdgcn_mfma_f32_16x16x32_f16"
+                                               : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
+  const DmaRoles R = dma_roles(sp);
+  const int SB = sp.dsb;
+  const int64_t SAE = (int64_t)sp.BM * 64, SBE = (int64_t)sp.BN * 64, BOFF = 2 * SAE;
+  s << "  auto compute = [&](const int sa, const int sb) {\n";
+  s << "    const " << T << "* Ab = (const " << T << "*)smem + sa * " << SAE << ";\n";
+  s << "    const " << T << "* Bb = (const " << T << "*)smem + " << BOFF << " + sb * " << SBE << ";\n";
+  s << "#pragma unroll\n    for (int kk = 0; kk < 2; ++kk) {\n";
+  s << "      " << V8 << " af[" << sp.FM << "], bf[" << sp.FN << "];\n";
+  // row & 7 == l & 7: the fragment's rows start at multiples of 16
+  s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i) af[i] = *(const " << V8 << "*)(Ab + (wm * " << sp.WTM
+    << " + i * 16 + (l & 15)) * 64 + (((kk * 4 + (l >> 4)) ^ (l & 7)) * 8));\n";
+  s << "#pragma unroll\n      for (int j = 0; j < " << sp.FN << "; ++j) {\n";
+  s << "        const int k_ = kk * 32 + (l >> 4) * 8 + ((l & 15) >> 2), n_ = wn * " << sp.WTN << " + j * 16 + 4 * (l & 3);\n";
+  s << "        bf[j] = __builtin_bit_cast(" << V8 << ", lds_tr_k8(Bb + k_ * " << sp.BN << " + (((n_ >> 3) ^ "
+    << dma_fk(sp, "k_") << ") * 8) + (n_ & 7), " << sp.BN << "));\n      }\n";
+  s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n      for (int j = 0; j < " << sp.FN
+    << "; ++j) acc[i][j] = " << fn << (sp.acc_t ? "(bf[j], af[i]" : "(af[i], bf[j]") << ", acc[i][j], 0, 0, 0);\n";
+  s << "    }\n  };\n";
+  const std::string W0 = "asm volatile(\"s_waitcnt vmcnt(0)\" ::: \"memory\");";
+  s << "  const int nkt_ = kt1 - kt0;\n";
+  const bool unrolled = kconst > 0 && kconst <= 128;
+  if (SB == 3) {
+    const std::string isA = "wv_ < " + std::to_string(R.ga);
+    // tiles 0 (A, even B loaders) and 1 (odd B loaders); the loaders of tile 0 wait
+    s << "  if (" << isA << ") dmaA_(kt0, 0);\n";
+    s << "  else if (par_ < nkt_) dmaB_(kt0 + par_, par_);\n";
+    s << "  if (" << isA << " || par_ == 0) " << W0 << "\n";
+    s << "  __syncthreads();\n";
+    if (unrolled) s << "#pragma unroll\n  for (int j = 0; j < " << kconst << "; ++j) {\n";
+    else s << "  for (int j = 0; j < nkt_; ++j) {\n";
+    s << "    if (" << isA << ") {\n      if (j + 1 < nkt_) dmaA_(kt0 + j + 1, (j + 1) & 1);\n";
+    s << "    } else if (par_ == (j & 1)) {\n      if (j + 2 < nkt_) dmaB_(kt0 + j + 2, (j + 2) % 3);\n    }\n";
+    s << "    compute(j & 1, j % 3);\n";
+    // the A loaders and the loaders of B tile j + 1 wait for everything they issued
+    s << "    if (" << isA << " || par_ != (j & 1)) " << W0 << "\n";
+    s << "    __syncthreads();\n  }\n";
+  } else {
+    s << "  dmaA_(kt0, 0);\n  dmaB_(kt0, 0);\n  " << W0 << "\n  __syncthreads();\n";
+    if (unrolled) s << "#pragma unroll\n  for (int j = 0; j < " << kconst << "; ++j) {\n";
+    else s << "  for (int j = 0; j < nkt_; ++j) {\n";
+    s << "    if (j + 1 < nkt_) {\n      dmaA_(kt0 + j + 1, (j + 1) & 1);\n      dmaB_(kt0 + j + 1, (j + 1) & 1);\n    }\n";
+    s << "    compute(j & 1, j & 1);\n";
+    s << "    " << W0 << "\n    __syncthreads();\n  }\n";
+  }
+  return s.str();
+}
+
 // The MFMA main loop over k-tiles [kt0, kt1) of the contraction.
 std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t kconst, bool kconst_exact, bool ctile) {
   std::ostringstream s;
@@ -873,6 +1110,11 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
   s << "  f32x4 acc[" << sp.FM << "][" << sp.FN << "];\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n  for (int j = 0; j < " << sp.FN
     << "; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};\n";
+  int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
+  std::string wguard = nw < sp.NT / 64 ? "if (wave < " + std::to_string(nw) + ") " : "";
+  if (sp.dma) {
+    s << dma_mainloop(sp, kconst);
+  } else {
   s << "  auto compute = [&](const int buf) {\n";
   s << "    const " << T << "* Ab = As + buf * " << sp.BM * sp.BKP << ";\n";
   int64_t bbuf = b_buf_elems(sp);
@@ -917,8 +1159,6 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
   // unconditional (tile indices clamped to the last tile) so the compiler counts
   // outstanding loads exactly; with a compile-time tile count the loop is
   // unrolled completely (stage and buffer indices are then constants).
-  int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
-  std::string wguard = nw < sp.NT / 64 ? "if (wave < " + std::to_string(nw) + ") " : "";
   auto clampk = [&](const std::string& t) {
     return "(i64)((" + t + ") < kt1 ? (" + t + ") : kt1 - 1) * " + std::to_string(sp.BK);
   };
@@ -1042,6 +1282,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
     s << "  }\n";
   }
   }
+  }
   if (!ctile) return s.str();
   // accumulators -> LDS C tile (fp32)
   s << "  float* Cs = (float*)smem;\n";
@@ -1055,6 +1296,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
 size_t gemm_smem_bytes(const GemmSpec& sp) {
   size_t bbuf = (size_t)b_buf_elems(sp);
   size_t ab = (size_t)2 * ((size_t)sp.BM * sp.BKP + bbuf) * dtype_bytes(sp.mtype);
+  if (sp.dma) ab = (size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype);
   if (sp.acc_t) return std::max(ab, (size_t)sp.OSB);
   size_t c = (size_t)(sp.CROWS ? sp.CROWS : sp.BM) * sp.LDC * 4;
   return std::max(ab, c);
@@ -1323,6 +1565,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
     sp.OSP = sp.BN + 8;
     sp.OSB = sp.BM * sp.OSP * 2;
   }
+  plan_dma(ki, sp, ksplit);
   std::ostringstream s;
   s << source_header((int)gk.args.size());
   if (ksplit) {
@@ -1371,8 +1614,12 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
       sp.sched_w = sp.sched_g = perA + perB;
     }
   }
-  s << operand_loader(ki, sp, true, slot);
-  s << operand_loader(ki, sp, false, slot);
+  if (sp.dma) {
+    s << dma_loader(ki, sp, slot);
+  } else {
+    s << operand_loader(ki, sp, true, slot);
+    s << operand_loader(ki, sp, false, slot);
+  }
   if (ksplit) {
     s << mfma_mainloop(sp, "", KH, KT % 2 == 0, false);
     s << "  float* Cs = (float*)smem;\n";

@@ -57,7 +57,18 @@ struct GemmSpec {
   // Register epilogue: output staging tile in LDS (elements per row; 0 = none).
   int OSP = 0;
   int OSB = 0;  // its bytes
+  // Direct-to-LDS staging (plain 16-bit operands, tiles dividing the problem,
+  // k-tiles of 64): operand tiles go from global memory straight into LDS, in
+  // swizzled layouts, with no register round trip and no LDS write
+  // instructions.  The right operand's chunk c of row k is stored at
+  // c ^ f(k), f(k) = dx0 (k & 1) + dx1 ((k >> 1) & 1) + dx3 ((k >> 3) & 1).
+  bool dma = false;
+  int dx0 = 0, dx1 = 0, dx3 = 0;
+  int dsb = 2;  // right-operand stages (the left operand has two)
 };
+
+// Decides direct-to-LDS staging (sets sp.dma) once tiles and the epilogue are known.
+void plan_dma(const KInfo& ki, GemmSpec& sp, bool ksplit);
 
 // LDS element offset of row k of the [k][n] right-operand tile.
 std::string b_row_off(const GemmSpec& sp, const std::string& k);

@@ -56,6 +56,16 @@ WIDE_TILE_CASE = dict(m=4000, d=176, h=1536)
 # contraction (720 = 11.25 k-tiles of 64).
 BIG_TILE_CASE = dict(m=4000, d=720, h=3072)
 
+# MLP shapes of the direct-to-LDS staging GPU tests (the layered plan's first
+# product takes it): bf16 with 64 x 64 tiles and three right-operand stages;
+# a contraction of two k-tiles (two stages).  Each runs with the path switched
+# off too (KORCH_GEMM_DMA=0), and the full MLP block also with two stages
+# forced (KORCH_GEMM_DMA_2STAGE=1).
+DMA_CASES = [
+    dict(m=1024, d=256, h=768, dtype="bf16"),
+    dict(m=512, d=128, h=512),
+]
+
 # Attention shapes of the attention-kernel GPU tests (few query rows: the keys
 # are split over the waves; fp32 and fp16, padded keys), each run with the key
 # split and without it (KORCH_ATTN_NO_KEY_SPLIT=1).
@@ -132,6 +142,11 @@ def _jobs():
             jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_NO_KSPLIT", flag)))
     jobs.append(("plans", "mlp", WIDE_TILE_CASE, None))
     jobs.append(("plans", "mlp", BIG_TILE_CASE, None))
+    for sz in DMA_CASES:
+        jobs.append(("plans", "mlp", sz, None))
+        jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_DMA", "0")))
+    jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA", "0")))
+    jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_2STAGE", "1")))
     for wl, sz in ATTN_CASES:
         for flag in ("", "1"):
             jobs.append(("env_plans", wl, sz, ("KORCH_ATTN_NO_KEY_SPLIT", flag)))

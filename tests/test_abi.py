@@ -380,14 +380,48 @@ def test_gemm_wide_tile_selection():
 
     (grid, block, _), src = gemm1({})
     assert grid == (256, 1, 1) and block == (512, 1, 1)
-    assert "* 72 + " in src  # A tile rows of 64 + 8 halves (k-tiles of 64)
-    (grid, block, _), _ = gemm1(BIG_TILE_CASE)
+    (grid, block, _), src = gemm1(BIG_TILE_CASE)
     assert grid == (16 * 16, 1, 1) and block == (512, 1, 1)
+    assert "* 80 + " in src  # register-staged A tile rows of 64 + 16 halves (k-tiles of 64)
     (grid, block, _), src = gemm1(WIDE_TILE_CASE)
     assert grid == (32 * 8, 1, 1) and block == (256, 1, 1)
-    assert "* 40 + " in src  # A tile rows of 32 + 8 halves (k-tiles of 32)
+    assert "* 48 + " in src  # A tile rows of 32 + 16 halves (k-tiles of 32)
     (grid, _, _), _ = gemm1(dict(m=500, d=256, h=1056))
     assert grid[0] != 4 * 1056 // 192
+
+
+def test_gemm_direct_to_lds_staging_selection(monkeypatch):
+    """The MLP block's first product (plain fp16 operands, 256 x 192 tiles that
+    divide the problem, k-tiles of 64) stages both operands with direct
+    global-to-LDS loads: 32 + 24 one-KiB blocks per k-tile, two left-operand
+    and three right-operand stages in 136 KiB of LDS, every wait before a
+    barrier a full vmcnt(0).  KORCH_GEMM_DMA=0 restores register staging;
+    ragged rows keep it; KORCH_GEMM_DMA_2STAGE=1 gives two right-operand
+    stages."""
+    import re
+    from paper_2406_09465_amd.warm import BIG_TILE_CASE
+
+    def gemm1(sizes):
+        p = graphs.build("mlp", **sizes).plan("layered")
+        p.compile()
+        return p.kernel_launch(1), p.kernel_source(1)
+
+    monkeypatch.delenv("KORCH_GEMM_DMA", raising=False)
+    monkeypatch.delenv("KORCH_GEMM_DMA_2STAGE", raising=False)
+    (grid, block, lds), src = gemm1({})
+    assert "32 A blocks and 24 B blocks of 1 KiB per k-tile, 2 A stages and 3 B stages" in src
+    assert lds == (2 * 256 + 3 * 192) * 64 * 2
+    assert src.count("global_load_lds_dwordx4") == 2  # the A and the B staging lambda
+    assert set(re.findall(r"s_waitcnt vmcnt\((\d+)\)", src)) == {"0"}
+    assert "stashA" not in src
+    _, src = gemm1(BIG_TILE_CASE)
+    assert "global_load_lds_dwordx4" not in src and "stashA" in src
+    monkeypatch.setenv("KORCH_GEMM_DMA_2STAGE", "1")
+    (_, _, lds), src = gemm1({})
+    assert "2 A stages and 2 B stages" in src and lds == (2 * 256 + 2 * 192) * 64 * 2
+    monkeypatch.setenv("KORCH_GEMM_DMA", "0")
+    _, src = gemm1({})
+    assert "global_load_lds_dwordx4" not in src and "stashA" in src
 
 
 def test_attention_key_split_selection():
