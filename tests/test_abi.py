@@ -424,6 +424,46 @@ def test_gemm_direct_to_lds_staging_selection(monkeypatch):
     assert "global_load_lds_dwordx4" not in src and "stashA" in src
 
 
+@pytest.mark.parametrize("workload,sizes", [("mlp", {}), ("sra", {}), ("mlp", dict(m=1024, d=256, h=768, dtype="bf16"))])
+def test_direct_to_lds_kernels_use_m0_only_for_their_loads(workload, sizes):
+    """Kernels with direct-to-LDS staging set M0 (the loads' LDS address) in
+    inline assembly the compiler does not see: in their disassembly (the
+    compiler's own objdump, on code objects built here) every instruction that
+    names m0 is an s_mov_b32 to it directly followed by the load, so no value
+    the compiler keeps in M0 can be overwritten."""
+    import os
+    import subprocess
+    import tempfile
+    objdump = "/opt/rocm/llvm/bin/llvm-objdump"
+    if not os.path.exists(objdump):
+        pytest.skip("no llvm-objdump")
+    w = graphs.build(workload, **sizes)
+    seen = 0
+    for plan in ("layered", "unfused"):
+        p = w.plan(plan)
+        p.compile()
+        for k in range(p.num_kernels()):
+            if "global_load_lds_dwordx4" not in p.kernel_source(k):
+                continue
+            with tempfile.NamedTemporaryFile(suffix=".co", delete=False) as f:
+                f.write(p.kernel_code(k))
+            try:
+                r = subprocess.run([objdump, "-d", "--mcpu=gfx950", f.name], capture_output=True, text=True)
+            finally:
+                os.unlink(f.name)
+            assert r.returncode == 0, r.stderr[:500]
+            ins = [ln.split("//")[0].strip() for ln in r.stdout.splitlines()]
+            ins = [ln for ln in ins if ln and not ln.endswith(":") and not ln.startswith("Disassembly")]
+            loads = [i for i, ln in enumerate(ins) if ln.startswith("global_load_lds_dwordx4")]
+            assert loads
+            for i, ln in enumerate(ins):
+                if "m0" in ln.replace(",", " ").split():
+                    assert ln.startswith("s_mov_b32 m0,") and ins[i + 1].startswith("global_load_lds_dwordx4"), (plan, k, ln)
+            assert all(ins[i - 1].startswith("s_mov_b32 m0,") for i in loads)
+            seen += 1
+    assert seen
+
+
 def test_attention_key_split_selection():
     """Few query rows split the keys over the waves (one workgroup per 16 rows);
     the SRA workload's 16384 queries keep one workgroup per 64 rows."""
