@@ -19,6 +19,70 @@ namespace korch {
 
 static bool in_vec(const std::vector<int>& v, int x) { return std::find(v.begin(), v.end(), x) != v.end(); }
 
+// The fissioned LayerNorm over the last axis (Korch's operator fission of
+// LayerNorm into reduce and elementwise primitives):
+//   mu = mean(X), D = X - mu, D2 = D^2, var = mean(D2), ve = var + eps,
+//   r = rsqrt(ve), Xh = D r, Yg = Xh gamma, Y = Yg + beta,
+// all inside the kernel, Y the product's left operand and its only use, gamma
+// and beta vectors along the last axis.  The product is then
+//   Y W = r (X diag(gamma) W - mu gamma^T W) + beta^T W   (per row r, mu)
+// with var = mean(X^2) - mu^2: the kernel needs only X, the row sums of X
+// and X^2, and the column sums gamma^T W and beta^T W, which it accumulates
+// from the tiles it stages anyway.
+static bool detect_ln_fold(const KInfo& ki, int Y, GemmSpec& sp) {
+  const Graph& g = ki.g;
+  auto in = [&](int v) { return v >= 0 && ki.in.count(v) > 0; };
+  auto nd = [&](int v) -> const Node& { return g.nodes[v]; };
+  auto bin = [&](int v, int op) { return in(v) && nd(v).op == op && !nd(v).attrs.has_scalar && nd(v).in.size() == 2; };
+  auto last_axis = [&](int v) { return (int)nd(v).axis == (int)nd(nd(v).in[0]).shape.size() - 1 && nd(v).attrs.keepdim; };
+  auto vec_k = [&](int v, int64_t K) {
+    if (ki.in.count(v)) return false;
+    const Shape& sh = nd(v).shape;
+    int64_t n = 1;
+    for (auto x : sh) n *= x;
+    return n == K && !sh.empty() && sh.back() == K;
+  };
+  if (!bin(Y, KORCH_ADD)) return false;
+  for (int s1 = 0; s1 < 2; ++s1) {
+    const int Yg = nd(Y).in[s1], beta = nd(Y).in[1 - s1];
+    if (!bin(Yg, KORCH_MUL)) continue;
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int Xh = nd(Yg).in[s2], gamma = nd(Yg).in[1 - s2];
+      if (!bin(Xh, KORCH_MUL)) continue;
+      for (int s3 = 0; s3 < 2; ++s3) {
+        const int D = nd(Xh).in[s3], r = nd(Xh).in[1 - s3];
+        if (!bin(D, KORCH_SUB) || !in(r) || nd(r).op != KORCH_RSQRT) continue;
+        const int X = nd(D).in[0], mu = nd(D).in[1];
+        if (in(X) || !in(mu) || nd(mu).op != KORCH_REDUCE_MEAN || nd(mu).in[0] != X || !last_axis(mu)) continue;
+        const int ve = nd(r).in[0];
+        if (!in(ve) || nd(ve).op != KORCH_ADD || !nd(ve).attrs.has_scalar || nd(ve).attrs.scalar < 0) continue;
+        const int var = nd(ve).in[0];
+        if (!in(var) || nd(var).op != KORCH_REDUCE_MEAN || !last_axis(var)) continue;
+        const int D2 = nd(var).in[0];
+        if (!in(D2) || nd(D2).op != KORCH_SQUARE || nd(D2).in[0] != D) continue;
+        const Shape& xs = nd(X).shape;
+        if (xs.size() != 2 || nd(Y).shape != xs || nd(D).shape != xs || nd(Xh).shape != xs) continue;
+        const int64_t K = xs.back();
+        if (!vec_k(gamma, K) || !vec_k(beta, K)) continue;
+        const std::set<int> set = {mu, D, D2, var, ve, r, Xh, Yg, Y};
+        // the LayerNorm's values are used only by itself and the product
+        bool ok = true;
+        for (int v : set) {
+          if (std::find(ki.k.outs.begin(), ki.k.outs.end(), v) != ki.k.outs.end()) ok = false;
+          for (int c : g.consumers[v])
+            if (!set.count(c) && !(v == Y && nd(c).op == KORCH_MATMUL)) ok = false;
+        }
+        if (!ok || g.consumers[Y].size() != 1) continue;
+        sp.lnf = true;
+        sp.lnX = X, sp.lng = gamma, sp.lnb = beta, sp.lneps = nd(ve).attrs.scalar;
+        sp.lnset = set;
+        return true;
+      }
+    }
+  }
+  return false;
+}
+
 bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_reduce) {
   const Graph& g = ki.g;
   if (ki.linear.empty()) {
@@ -88,6 +152,7 @@ bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_re
     sp.M = sp.OUT[sp.OUT.size() - 2];
     sp.N = sp.OUT.back();
     sp.K = g.nodes[sp.A].shape.back();
+    if (mms.size() == 1 && detect_ln_fold(ki, sp.A, sp)) sp.A = sp.lnX;
     for (int v : mms) {
       const Shape& s = g.nodes[v].shape;
       if (!std::equal(s.begin(), s.end() - 1, sp.OUT.begin()) || (s.back() != sp.N && s.back() != 1)) {
@@ -116,7 +181,7 @@ bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_re
   std::vector<int> operands = sp.Bs;
   operands.push_back(sp.A);
   for (int v : ki.k.prims) {
-    if (in_vec(sp.mms, v)) continue;
+    if (in_vec(sp.mms, v) || sp.lnset.count(v)) continue;
     bool pro = false, below = false;
     for (int o : operands)
       if (v == o || ki.ancestor(v, o)) pro = true;
@@ -197,10 +262,32 @@ bool analyze_gemm(const KInfo& ki, GemmSpec& sp, std::string* why, bool allow_re
   return true;
 }
 
+static size_t gemm_smem_bytes_fwd(const GemmSpec& sp);
+
+// The generator's decisions for a folded LayerNorm, taken on a copy: tiles,
+// operand layouts, the register epilogue and direct-to-LDS staging must all
+// apply, else the kernel is not supported.
+static bool ln_fold_feasible(const KInfo& ki, GemmSpec sp, std::string* why) {
+  choose_tiles(sp, false);
+  plan_operands(ki, sp);
+  sp.acc_t = reg_epilogue_output(ki, sp) >= 0;
+  if (sp.acc_t) {
+    sp.OSP = sp.BN + 8;
+    sp.OSB = sp.BM * sp.OSP * 2;
+  }
+  plan_dma(ki, sp, false);
+  if (!sp.dma || !sp.acc_t || sp.mtype != KORCH_F16 || sp.K % 64 || gemm_smem_bytes_fwd(sp) > 160 * 1024) {
+    if (why) *why = "gemm: a folded LayerNorm needs fp16 tiles that divide the problem and the register epilogue";
+    return false;
+  }
+  return true;
+}
+
 bool match_gemm(const KInfo& ki, std::string* why) {
   GemmSpec sp;
   if (!analyze_gemm(ki, sp, why, false)) return false;
   if (sp.conv) return false;
+  if (sp.lnf && !ln_fold_feasible(ki, sp, why)) return false;
   if (sp.mms.size() > 1 && sp.Ntot > 128) {
     *why = "gemm: combined right operands wider than one tile";
     return false;
@@ -966,6 +1053,11 @@ void plan_dma(const KInfo& ki, GemmSpec& sp, bool ksplit) {
   sp.dma = true;
 }
 
+// LayerNorm fold: LDS byte offset of gamma and beta (K halves each) and the
+// column sums gamma^T W, beta^T W (BN floats each), after the operand stages.
+static int64_t ln_lds_off(const GemmSpec& sp) { return (int64_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * 2; }
+static int64_t ln_lds_bytes(const GemmSpec& sp) { return sp.lnf ? 4 * sp.K + 8 * (int64_t)sp.BN : 0; }
+
 // Which waves load what.  With two right-operand stages every wave loads
 // blocks of both operands for the next k-tile (wave w: blocks w, w + NW, ...)
 // and waits for all its loads before the barrier that ends the tile.  With
@@ -1026,20 +1118,32 @@ static std::string dma_loader(const KInfo& ki, const GemmSpec& sp, const std::ma
   s << "  const unsigned lds0_ = (unsigned)(size_t)(__attribute__((address_space(3))) void*)smem;\n";
   s << "  const " << T << "* Ag_ = (const " << T << "*)a.p[" << slot.at(sp.A) << "] + (" << boff(sp.A) << ");\n";
   s << "  const " << T << "* Bg_ = (const " << T << "*)a.p[" << slot.at(sp.Bs[0]) << "] + (" << boff(sp.Bs[0]) << ");\n";
-  s << "  i64 doffA_[" << R.PA << "], doffB_[" << R.PB << "];  // element offset of this lane's chunk at k-tile 0\n";
+  // element offsets of this lane's chunks at k-tile 0 (32-bit when both
+  // operands have fewer than 2^31 elements); with three right-operand stages a
+  // wave loads one operand only, and one array holds its offsets
+  const bool small = (double)numel(g.nodes[sp.A].shape) < 2147483648.0 && (double)numel(g.nodes[sp.Bs[0]].shape) < 2147483648.0;
+  const std::string OT_ = small ? "int" : "i64";
+  const std::string aoffs = sp.dsb == 3 ? "doff_" : "doffA_", boffs = sp.dsb == 3 ? "doff_" : "doffB_";
+  if (sp.dsb == 3)
+    s << "  " << OT_ << " doff_[" << std::max(R.PA, R.PB) << "];\n";
+  else
+    s << "  " << OT_ << " doffA_[" << R.PA << "], doffB_[" << R.PB << "];\n";
+  if (sp.dsb == 3) s << "  if (wv_ < " << R.ga << ") {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << R.PA << "; ++i) {\n";
   s << "    const int r = 8 * (wa_ + i * " << R.ga << ") + (l >> 3);\n";
-  s << "    doffA_[i] = (m0 + r) * " << sp.K << "LL + (((l & 7) ^ (l >> 3)) * 8);\n  }\n";
+  s << "    " << aoffs << "[i] = (" << OT_ << ")((m0 + r) * " << sp.K << "LL + (((l & 7) ^ (l >> 3)) * 8));\n  }\n";
+  if (sp.dsb == 3) s << "  } else {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << R.PB << "; ++i) {\n";
   s << "    const int q = (wb_ + i * " << R.gb << ") * 64 + l, k = q / " << P << ", p = q % " << P << ";\n";
-  s << "    doffB_[i] = (i64)k * " << sp.N << "LL + n0 + ((p ^ " << dma_fk(sp, "k") << ") * 8);\n  }\n";
+  s << "    " << boffs << "[i] = (" << OT_ << ")((i64)k * " << sp.N << "LL + n0 + ((p ^ " << dma_fk(sp, "k") << ") * 8));\n  }\n";
+  if (sp.dsb == 3) s << "  }\n";
   const char* ld = "      asm volatile(\"s_mov_b32 m0, %1\\n\\tglobal_load_lds_dwordx4 %0, off\" :: \"v\"(src), \"s\"(la) : \"memory\", \"m0\");\n";
   s << "  auto dmaA_ = [&](const int kt, const int st) {\n#pragma unroll\n    for (int i = 0; i < " << R.PA << "; ++i) {\n";
-  s << "      const " << T << "* src = Ag_ + (i64)kt * 64 + doffA_[i];\n";
+  s << "      const " << T << "* src = Ag_ + (i64)kt * 64 + " << aoffs << "[i];\n";
   s << "      const unsigned la = lds0_ + (unsigned)((st * " << SAE << " + (wa_ + i * " << R.ga << ") * 512) * 2);\n" << ld;
   s << "    }\n  };\n";
   s << "  auto dmaB_ = [&](const int kt, const int st) {\n#pragma unroll\n    for (int i = 0; i < " << R.PB << "; ++i) {\n";
-  s << "      const " << T << "* src = Bg_ + (i64)kt * " << 64 * sp.N << "LL + doffB_[i];\n";
+  s << "      const " << T << "* src = Bg_ + (i64)kt * " << 64 * sp.N << "LL + " << boffs << "[i];\n";
   s << "      const unsigned la = lds0_ + (unsigned)((" << BOFF << " + st * " << SBE << " + (wb_ + i * " << R.gb
     << ") * 512) * 2);\n" << ld;
   s << "    }\n  };\n";
@@ -1058,7 +1162,23 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
   const DmaRoles R = dma_roles(sp);
   const int SB = sp.dsb;
   const int64_t SAE = (int64_t)sp.BM * 64, SBE = (int64_t)sp.BN * 64, BOFF = 2 * SAE;
-  s << "  auto compute = [&](const int sa, const int sb) {\n";
+  const int64_t LNO = ln_lds_off(sp);
+  if (sp.lnf) {
+    // gamma and beta into LDS once; per-lane row sums of X and X^2 (rows of the
+    // lane's A fragments, its quarter of each k-step) and column sums of the
+    // B fragments this wave owns (column blocks j with j % WM == wm)
+    s << "  const " << T << "* lng_ = (const " << T << "*)(smem + " << LNO << ");\n";
+    s << "  const " << T << "* lnb_ = lng_ + " << sp.K << ";\n";
+    s << "  for (int t_ = tid; t_ < " << sp.K / 8 << "; t_ += " << sp.NT << ") {\n";
+    s << "    *(uint4*)((" << T << "*)lng_ + 8 * t_) = *(const uint4*)((const " << T << "*)a.p[" << sp.lng_slot << "] + 8 * t_);\n";
+    s << "    *(uint4*)((" << T << "*)lnb_ + 8 * t_) = *(const uint4*)((const " << T << "*)a.p[" << sp.lnb_slot << "] + 8 * t_);\n";
+    s << "  }\n";
+    const int TJ = (sp.FN + sp.WM - 1) / sp.WM;  // column blocks per wave
+    s << "  float lnsx_[" << sp.FM << "] = {}, lnsq_[" << sp.FM << "] = {}, lncs_[" << TJ << "] = {}, lncc_[" << TJ << "] = {};\n";
+    s << "  typedef _Float16 h2_ __attribute__((ext_vector_type(2)));\n";
+  }
+  s << "  auto compute = [&](const int sa, const int sb, const int kt) {\n";
+  s << "    (void)kt;\n";
   s << "    const " << T << "* Ab = (const " << T << "*)smem + sa * " << SAE << ";\n";
   s << "    const " << T << "* Bb = (const " << T << "*)smem + " << BOFF << " + sb * " << SBE << ";\n";
   s << "#pragma unroll\n    for (int kk = 0; kk < 2; ++kk) {\n";
@@ -1070,12 +1190,37 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
   s << "        const int k_ = kk * 32 + (l >> 4) * 8 + ((l & 15) >> 2), n_ = wn * " << sp.WTN << " + j * 16 + 4 * (l & 3);\n";
   s << "        bf[j] = __builtin_bit_cast(" << V8 << ", lds_tr_k8(Bb + k_ * " << sp.BN << " + (((n_ >> 3) ^ "
     << dma_fk(sp, "k_") << ") * 8) + (n_ & 7), " << sp.BN << "));\n      }\n";
+  if (sp.lnf) {
+    // the lane's eight k of this k-step: kt * 64 + kk * 32 + 8 (l >> 4) ..
+    s << "      const " << V8 << " gs_ = *(const " << V8 << "*)(lng_ + kt * 64 + kk * 32 + 8 * (l >> 4));\n";
+    s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i) {\n";
+    s << "#pragma unroll\n        for (int h = 0; h < 4; ++h) {\n";
+    s << "          const h2_ x2 = {af[i][2 * h], af[i][2 * h + 1]};\n";
+    s << "          lnsx_[i] = __builtin_amdgcn_fdot2(x2, h2_{(_Float16)1.0f, (_Float16)1.0f}, lnsx_[i], false);\n";
+    s << "          lnsq_[i] = __builtin_amdgcn_fdot2(x2, x2, lnsq_[i], false);\n";
+    s << "        }\n";
+    s << "        af[i] = af[i] * gs_;\n";
+    s << "      }\n";
+    s << "      const " << V8 << " bs_ = *(const " << V8 << "*)(lnb_ + kt * 64 + kk * 32 + 8 * (l >> 4));\n";
+    // column block j belongs to the wave with wm == j % WM (a uniform branch;
+    // the accumulator index j / WM is a constant of the unrolled loop)
+    for (int j = 0; j < sp.FN; ++j) {
+      const std::string J = std::to_string(j), T_ = std::to_string(j / sp.WM);
+      s << "      if (wm == " << j % sp.WM << ") {\n";
+      s << "#pragma unroll\n        for (int h = 0; h < 4; ++h) {\n";
+      s << "          const h2_ w2 = {bf[" << J << "][2 * h], bf[" << J << "][2 * h + 1]};\n";
+      s << "          lncs_[" << T_ << "] = __builtin_amdgcn_fdot2(w2, h2_{gs_[2 * h], gs_[2 * h + 1]}, lncs_[" << T_ << "], false);\n";
+      s << "          lncc_[" << T_ << "] = __builtin_amdgcn_fdot2(w2, h2_{bs_[2 * h], bs_[2 * h + 1]}, lncc_[" << T_ << "], false);\n";
+      s << "        }\n      }\n";
+    }
+  }
   s << "#pragma unroll\n      for (int i = 0; i < " << sp.FM << "; ++i)\n#pragma unroll\n      for (int j = 0; j < " << sp.FN
     << "; ++j) acc[i][j] = " << fn << (sp.acc_t ? "(bf[j], af[i]" : "(af[i], bf[j]") << ", acc[i][j], 0, 0, 0);\n";
   s << "    }\n  };\n";
   const std::string W0 = "asm volatile(\"s_waitcnt vmcnt(0)\" ::: \"memory\");";
   s << "  const int nkt_ = kt1 - kt0;\n";
-  const bool unrolled = kconst > 0 && kconst <= 128;
+  // a folded LayerNorm's statistics leave too few registers for the unrolled loop
+  const bool unrolled = kconst > 0 && kconst <= 128 && !sp.lnf;
   if (SB == 3) {
     const std::string isA = "wv_ < " + std::to_string(R.ga);
     // tiles 0 (A, even B loaders) and 1 (odd B loaders); the loaders of tile 0 wait
@@ -1087,7 +1232,7 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
     else s << "  for (int j = 0; j < nkt_; ++j) {\n";
     s << "    if (" << isA << ") {\n      if (j + 1 < nkt_) dmaA_(kt0 + j + 1, (j + 1) & 1);\n";
     s << "    } else if (par_ == (j & 1)) {\n      if (j + 2 < nkt_) dmaB_(kt0 + j + 2, (j + 2) % 3);\n    }\n";
-    s << "    compute(j & 1, j % 3);\n";
+    s << "    compute(j & 1, j % 3, kt0 + j);\n";
     // the A loaders and the loaders of B tile j + 1 wait for everything they issued
     s << "    if (" << isA << " || par_ != (j & 1)) " << W0 << "\n";
     s << "    __syncthreads();\n  }\n";
@@ -1096,8 +1241,36 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
     if (unrolled) s << "#pragma unroll\n  for (int j = 0; j < " << kconst << "; ++j) {\n";
     else s << "  for (int j = 0; j < nkt_; ++j) {\n";
     s << "    if (j + 1 < nkt_) {\n      dmaA_(kt0 + j + 1, (j + 1) & 1);\n      dmaB_(kt0 + j + 1, (j + 1) & 1);\n    }\n";
-    s << "    compute(j & 1, j & 1);\n";
+    s << "    compute(j & 1, j & 1, kt0 + j);\n";
     s << "    " << W0 << "\n    __syncthreads();\n  }\n";
+  }
+  if (sp.lnf) {
+    // row statistics: the four lanes of a row (l, l ^ 16, l ^ 32, l ^ 48) hold
+    // its four quarters; var = mean(X^2) - mu^2 (clamped at 0)
+    s << "  float lnmu_[" << sp.FM << "], lnr_[" << sp.FM << "];\n";
+    s << "#pragma unroll\n  for (int i = 0; i < " << sp.FM << "; ++i) {\n";
+    s << "    float a_ = lnsx_[i], b_ = lnsq_[i];\n";
+    s << "    a_ += __shfl_xor(a_, 16); a_ += __shfl_xor(a_, 32);\n";
+    s << "    b_ += __shfl_xor(b_, 16); b_ += __shfl_xor(b_, 32);\n";
+    s << "    const float mu_ = a_ * " << flit(1.0 / (double)sp.K) << ";\n";
+    s << "    lnmu_[i] = mu_;\n";
+    s << "    lnr_[i] = f_rsqrt(k_max(b_ * " << flit(1.0 / (double)sp.K) << " - mu_ * mu_, 0.0f) + " << flit(sp.lneps) << ");\n";
+    s << "  }\n";
+    // column sums of this wave's column blocks into LDS (after the operand stages)
+    s << "  float* lns_ = (float*)(smem + " << LNO + 4 * sp.K << ");\n";
+    s << "  float* lnc_ = lns_ + " << sp.BN << ";\n";
+    for (int j = 0; j < sp.FN; ++j) {
+      const std::string T_ = std::to_string(j / sp.WM);
+      s << "  if (wm == " << j % sp.WM << ") {\n";
+      s << "    float c0_ = lncs_[" << T_ << "], c1_ = lncc_[" << T_ << "];\n";
+      s << "    c0_ += __shfl_xor(c0_, 16); c0_ += __shfl_xor(c0_, 32);\n";
+      s << "    c1_ += __shfl_xor(c1_, 16); c1_ += __shfl_xor(c1_, 32);\n";
+      s << "    if ((l >> 4) == 0) {\n";
+      s << "      lns_[wn * " << sp.WTN << " + " << j * 16 << " + l] = c0_;\n";
+      s << "      lnc_[wn * " << sp.WTN << " + " << j * 16 << " + l] = c1_;\n";
+      s << "    }\n  }\n";
+    }
+    s << "  __syncthreads();\n";
   }
   return s.str();
 }
@@ -1293,10 +1466,12 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
   return s.str();
 }
 
+static size_t gemm_smem_bytes_fwd(const GemmSpec& sp) { return gemm_smem_bytes(sp); }
+
 size_t gemm_smem_bytes(const GemmSpec& sp) {
   size_t bbuf = (size_t)b_buf_elems(sp);
   size_t ab = (size_t)2 * ((size_t)sp.BM * sp.BKP + bbuf) * dtype_bytes(sp.mtype);
-  if (sp.dma) ab = (size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype);
+  if (sp.dma) ab = (size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype) + (size_t)ln_lds_bytes(sp);
   if (sp.acc_t) return std::max(ab, (size_t)sp.OSB);
   size_t c = (size_t)(sp.CROWS ? sp.CROWS : sp.BM) * sp.LDC * 4;
   return std::max(ab, c);
@@ -1342,7 +1517,8 @@ std::string gemm_reg_epilogue(const KInfo& ki, const GemmSpec& sp, const std::ma
   em.provide = [&](int node, const std::vector<Ix>& idx, std::string* out) {
     if (node != sp.mms[0]) return false;
     if (Emitter::key(node, idx) != pkey) fail(KORCH_E_UNSUPPORTED, "gemm: epilogue reads the product at another index");
-    *out = "acc[i][j][e]";
+    // folded LayerNorm: r (acc - mu gamma^T W) + beta^T W
+    *out = sp.lnf ? "(lnr_[i] * (acc[i][j][e] - lnmu_[i] * lns_[nl + e]) + lnc_[nl + e])" : "acc[i][j][e]";
     return true;
   };
   const std::string v = em.value(o, broadcast_index(on.shape, sp.OUT, it));
@@ -1550,7 +1726,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   // MFMAs and loads, one group's waits covered by the other's products.
   const size_t op_bytes = (size_t)2 * ((size_t)sp.BM * sp.BKP + (size_t)b_buf_elems(sp)) * dtype_bytes(sp.mtype);
   const size_t ksplit_lds = std::max(2 * op_bytes, (size_t)sp.BM * sp.LDC * 4);
-  const bool ksplit = !sp.conv && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 && sp.NT == 256 &&
+  const bool ksplit = !sp.conv && !sp.lnf && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 && sp.NT == 256 &&
                       ksplit_lds <= 160 * 1024 && !getenv("KORCH_GEMM_NO_KSPLIT");
   const int64_t KH = (KT + 1) / 2;
   {
@@ -1566,6 +1742,15 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
     sp.OSB = sp.BM * sp.OSP * 2;
   }
   plan_dma(ki, sp, ksplit);
+  if (sp.lnf) {
+    // the fold needs direct-to-LDS staging (X tiles in their swizzled layout),
+    // the register epilogue (each lane holds its rows' statistics) and fp16
+    if (!sp.dma || !sp.acc_t || sp.mtype != KORCH_F16 || ksplit || sp.K % 64)
+      fail(KORCH_E_UNSUPPORTED, "gemm: a folded LayerNorm needs fp16 tiles that divide the problem and the register epilogue");
+    sp.lng_slot = slot.at(sp.lng);
+    sp.lnb_slot = slot.at(sp.lnb);
+    if (gemm_smem_bytes(sp) > 160 * 1024) fail(KORCH_E_UNSUPPORTED, "gemm: folded LayerNorm exceeds the LDS");
+  }
   std::ostringstream s;
   s << source_header((int)gk.args.size());
   if (ksplit) {

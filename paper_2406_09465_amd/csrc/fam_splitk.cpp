@@ -26,6 +26,10 @@ struct SplitInfo {
 static bool analyze_splitk(const KInfo& ki, GemmSpec& sp, SplitInfo& si, std::string* why) {
   const Graph& g = ki.g;
   if (!analyze_gemm(ki, sp, why, true)) return false;
+  if (sp.lnf) {
+    *why = "splitk: a folded LayerNorm runs in the gemm family";
+    return false;
+  }
   if (sp.conv || sp.mms.size() != 1) {
     *why = "splitk: needs exactly one matmul";
     return false;

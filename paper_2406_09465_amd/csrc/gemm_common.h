@@ -65,6 +65,17 @@ struct GemmSpec {
   bool dma = false;
   int dx0 = 0, dx1 = 0, dx3 = 0;
   int dsb = 2;  // right-operand stages (the left operand has two)
+  // LayerNorm folded into the product (see detect_ln_fold): the left operand
+  // is LN(X) = (X - mu) r gamma + beta over X's last axis; the kernel stages X,
+  // multiplies X gamma by the right operand W, accumulates each row's sum and
+  // sum of squares from the staged X and the column sums gamma^T W and
+  // beta^T W from the staged W, and provides the product as
+  // r (acc - mu gamma^T W) + beta^T W.
+  bool lnf = false;
+  int lnX = -1, lng = -1, lnb = -1;
+  int lng_slot = -1, lnb_slot = -1;  // kernel argument slots of gamma and beta
+  double lneps = 0;
+  std::set<int> lnset;  // the LayerNorm's primitives (mean ... affine)
 };
 
 // Decides direct-to-LDS staging (sets sp.dma) once tiles and the epilogue are known.

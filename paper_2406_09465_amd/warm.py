@@ -66,6 +66,15 @@ DMA_CASES = [
     dict(m=512, d=128, h=512),
 ]
 
+# MLP shapes of the folded-LayerNorm GPU tests: plans whose first kernel holds
+# the LayerNorm, the first product and (or not) the GELU.
+LN_FOLD_CASES = [{}, dict(m=1024, d=256, h=768)]
+LN_FOLD_PLANS = {
+    "gelu": [(["mu", "D", "D2", "var", "ve", "r", "Xh", "Yg", "Y", "H0", "Hg"], ["Hg"]), (["Zo", "out"], ["out"])],
+    "product": [(["mu", "D", "D2", "var", "ve", "r", "Xh", "Yg", "Y", "H0"], ["H0"]), (["Hg"], ["Hg"]),
+                (["Zo", "out"], ["out"])],
+}
+
 # Attention shapes of the attention-kernel GPU tests (few query rows: the keys
 # are split over the waves; fp32 and fp16, padded keys), each run with the key
 # split and without it (KORCH_ATTN_NO_KEY_SPLIT=1).
@@ -146,6 +155,8 @@ def _jobs():
         jobs.append(("plans", "mlp", sz, None))
         jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_DMA", "0")))
     jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA", "0")))
+    for sz in LN_FOLD_CASES:
+        jobs.append(("ln_fold", "mlp", sz, None))
     jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_2STAGE", "1")))
     for wl, sz in ATTN_CASES:
         for flag in ("", "1"):
@@ -183,6 +194,13 @@ def _run_job(job, part=0, parts=1):
             failures.append((w, sz, f"{kind} {extra}", str(e)[:200]))
         return failures
     wl = graphs.build(w, **sz)
+    if kind == "ln_fold":
+        for name, ks in LN_FOLD_PLANS.items():
+            try:
+                graphs.Plan(wl.graph, [([wl.ids[n] for n in p], [wl.ids[n] for n in o]) for p, o in ks]).compile()
+            except KorchError as e:
+                failures.append((w, sz, f"ln_fold {name}", str(e)[:200]))
+        return failures
     if kind == "plans":
         for pn in ("unfused", "layered", "fused"):
             try:
