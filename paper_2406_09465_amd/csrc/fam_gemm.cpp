@@ -1033,7 +1033,12 @@ void plan_dma(const KInfo& ki, GemmSpec& sp, bool ksplit) {
   sp.dma = false;
   const char* e = getenv("KORCH_GEMM_DMA");
   if (e && atoi(e) == 0) return;
-  if (sp.conv || ksplit || sp.mms.size() != 1 || sp.Bs.size() != 1 || !sp.b_kn) return;
+  if (sp.conv || sp.mms.size() != 1 || sp.Bs.size() != 1 || !sp.b_kn) return;
+  // With an intra-workgroup split of K the two groups' stages leave room for
+  // the left operand one k-tile ahead only: the MLP block's second product then
+  // took 34.0 us after a cache flush against 29.1 with register staging (26.7
+  // against 27.3 warm), so the split keeps register staging unless asked.
+  if (ksplit && !(getenv("KORCH_GEMM_DMA_KSPLIT") && atoi(getenv("KORCH_GEMM_DMA_KSPLIT")) != 0)) return;
   if (sp.mtype != KORCH_F16 && sp.mtype != KORCH_BF16) return;
   if (ki.in.count(sp.A) || ki.in.count(sp.Bs[0])) return;  // operands computed in the kernel
   if (sp.BK != 64 || sp.K % 64 || sp.M % sp.BM || sp.N % sp.BN || sp.BN % 16) return;
@@ -1041,12 +1046,14 @@ void plan_dma(const KInfo& ki, GemmSpec& sp, bool ksplit) {
   const int NW = sp.NT / 64;
   // a third right-operand stage (loaded two k-tiles ahead by wave groups of
   // their own) when it fits and the waves split into the three loading groups
-  sp.dsb = (size_t)(2 * sp.BM + 3 * sp.BN) * 64 * 2 <= 160 * 1024 && sp.K / 64 >= 3 && NW % 4 == 0 &&
+  // an intra-workgroup split of K gives each of its two groups stages of their own
+  const size_t lds = ksplit ? 80 * 1024 : 160 * 1024;
+  sp.dsb = (size_t)(2 * sp.BM + 3 * sp.BN) * 64 * 2 <= lds && sp.K / 64 >= (ksplit ? 6 : 3) && NW % 4 == 0 &&
                    (sp.BM / 8) % (NW / 2) == 0 && (sp.BN / 8) % (NW / 4) == 0 && !getenv("KORCH_GEMM_DMA_2STAGE")
                ? 3
                : 2;
   if (sp.dsb == 2 && ((sp.BM / 8) % NW || (sp.BN / 8) % NW)) return;  // equal load counts per wave
-  if ((size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * 2 > 160 * 1024) return;
+  if ((size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * 2 > lds) return;
   int x0 = 0, x1 = 0, x3 = 0;
   if (!dma_b_swizzle(sp.BN / 8, x0, x1, x3)) return;
   sp.dx0 = x0, sp.dx1 = x1, sp.dx3 = x3;
@@ -1115,7 +1122,7 @@ static std::string dma_loader(const KInfo& ki, const GemmSpec& sp, const std::ma
   } else {
     s << "  const int wa_ = wv_, wb_ = wv_;\n";
   }
-  s << "  const unsigned lds0_ = (unsigned)(size_t)(__attribute__((address_space(3))) void*)smem;\n";
+  s << "  const unsigned lds0_ = (unsigned)(size_t)(__attribute__((address_space(3))) void*)gsm_;\n";
   s << "  const " << T << "* Ag_ = (const " << T << "*)a.p[" << slot.at(sp.A) << "] + (" << boff(sp.A) << ");\n";
   s << "  const " << T << "* Bg_ = (const " << T << "*)a.p[" << slot.at(sp.Bs[0]) << "] + (" << boff(sp.Bs[0]) << ");\n";
   // element offsets of this lane's chunks at k-tile 0 (32-bit when both
@@ -1153,7 +1160,7 @@ static std::string dma_loader(const KInfo& ki, const GemmSpec& sp, const std::ma
 // Main loop over the k-tiles with direct-to-LDS staging.  A tile j + 1 goes to
 // the A stage tile j - 1 used and B tile j + dsb - 1 to the B stage tile j - 1
 // used; both are issued as tile j's products start.
-static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
+static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst, bool kconst_exact) {
   std::ostringstream s;
   const std::string T = ctype(sp.mtype);
   const std::string V8 = sp.mtype == KORCH_F16 ? "f16x8" : "bf16x8";
@@ -1179,8 +1186,8 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
   }
   s << "  auto compute = [&](const int sa, const int sb, const int kt) {\n";
   s << "    (void)kt;\n";
-  s << "    const " << T << "* Ab = (const " << T << "*)smem + sa * " << SAE << ";\n";
-  s << "    const " << T << "* Bb = (const " << T << "*)smem + " << BOFF << " + sb * " << SBE << ";\n";
+  s << "    const " << T << "* Ab = (const " << T << "*)gsm_ + sa * " << SAE << ";\n";
+  s << "    const " << T << "* Bb = (const " << T << "*)gsm_ + " << BOFF << " + sb * " << SBE << ";\n";
   s << "#pragma unroll\n    for (int kk = 0; kk < 2; ++kk) {\n";
   s << "      " << V8 << " af[" << sp.FM << "], bf[" << sp.FN << "];\n";
   // row & 7 == l & 7: the fragment's rows start at multiples of 16
@@ -1232,7 +1239,7 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
     else s << "  for (int j = 0; j < nkt_; ++j) {\n";
     s << "    if (" << isA << ") {\n      if (j + 1 < nkt_) dmaA_(kt0 + j + 1, (j + 1) & 1);\n";
     s << "    } else if (par_ == (j & 1)) {\n      if (j + 2 < nkt_) dmaB_(kt0 + j + 2, (j + 2) % 3);\n    }\n";
-    s << "    compute(j & 1, j % 3, kt0 + j);\n";
+    s << "    " << (kconst_exact ? "" : "if (j < nkt_) ") << "compute(j & 1, j % 3, kt0 + j);\n";
     // the A loaders and the loaders of B tile j + 1 wait for everything they issued
     s << "    if (" << isA << " || par_ != (j & 1)) " << W0 << "\n";
     s << "    __syncthreads();\n  }\n";
@@ -1241,7 +1248,7 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst) {
     if (unrolled) s << "#pragma unroll\n  for (int j = 0; j < " << kconst << "; ++j) {\n";
     else s << "  for (int j = 0; j < nkt_; ++j) {\n";
     s << "    if (j + 1 < nkt_) {\n      dmaA_(kt0 + j + 1, (j + 1) & 1);\n      dmaB_(kt0 + j + 1, (j + 1) & 1);\n    }\n";
-    s << "    compute(j & 1, j & 1, kt0 + j);\n";
+    s << "    " << (kconst_exact ? "" : "if (j < nkt_) ") << "compute(j & 1, j & 1, kt0 + j);\n";
     s << "    " << W0 << "\n    __syncthreads();\n  }\n";
   }
   if (sp.lnf) {
@@ -1286,7 +1293,7 @@ std::string mfma_mainloop(const GemmSpec& sp, const std::string& hook, int64_t k
   int nw = sp.WM * sp.WN;  // waves that own a sub-tile (the rest only stage operands)
   std::string wguard = nw < sp.NT / 64 ? "if (wave < " + std::to_string(nw) + ") " : "";
   if (sp.dma) {
-    s << dma_mainloop(sp, kconst);
+    s << dma_mainloop(sp, kconst, kconst_exact);
   } else {
   s << "  auto compute = [&](const int buf) {\n";
   s << "    const " << T << "* Ab = As + buf * " << sp.BM * sp.BKP << ";\n";
@@ -1742,6 +1749,9 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
     sp.OSB = sp.BM * sp.OSP * 2;
   }
   plan_dma(ki, sp, ksplit);
+  // with direct-to-LDS staging each k-group's operand stages take (2 BM + dsb BN) x 64 elements
+  const size_t grp_bytes = sp.dma ? (size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype) : op_bytes;
+  const size_t ksplit_lds_ = std::max(2 * grp_bytes, (size_t)sp.BM * sp.LDC * 4);
   if (sp.lnf) {
     // the fold needs direct-to-LDS staging (X tiles in their swizzled layout),
     // the register epilogue (each lane holds its rows' statistics) and fp16
@@ -1756,8 +1766,11 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   if (ksplit) {
     const std::string T = ctype(sp.mtype);
     s << "extern \"C\" __global__ void __launch_bounds__(512) " << gk.name << "(KArgs a) {\n";
-    s << "  __shared__ __attribute__((aligned(16))) char smem[" << ksplit_lds << "];\n";
+    s << "  __shared__ __attribute__((aligned(16))) char smem[" << ksplit_lds_ << "];\n";
     s << "  const int kgrp = threadIdx.x >> 8;  // which half of the k-tiles\n";
+    if (sp.dma)
+      s << "  char* gsm_ = smem + __builtin_amdgcn_readfirstlane(kgrp) * " << grp_bytes
+        << ";  // this group's operand stages (wave-uniform)\n";
     s << "  " << T << "* As = (" << T << "*)(smem + kgrp * " << op_bytes << ");\n";
     s << "  " << T << "* Bs = As + " << 2 * sp.BM * sp.BKP << ";\n";
     s << "  const int tid = threadIdx.x & 255, l = tid & 63, wave = tid >> 6;\n";
@@ -1766,6 +1779,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   } else {
     s << "extern \"C\" __global__ void __launch_bounds__(" << sp.NT << ") " << gk.name << "(KArgs a) {\n";
     s << gemm_prologue_common(sp);
+    if (sp.dma) s << "  char* gsm_ = smem;  // operand stages\n";
   }
   // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
   // L2.  Renumber them so every XCD owns a contiguous range of tiles, and order
@@ -1850,7 +1864,7 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   gk.source = s.str();
   gk.grid[0] = (int)total;
   gk.block[0] = ksplit ? 512 : sp.NT;
-  gk.lds_bytes = ksplit ? (int)ksplit_lds : (int)gemm_smem_bytes(sp);
+  gk.lds_bytes = ksplit ? (int)ksplit_lds_ : (int)gemm_smem_bytes(sp);
   if (gk.lds_bytes > 160 * 1024) fail(KORCH_E_UNSUPPORTED, "gemm: tiles need more than 160 KiB of LDS");
   ki.fill_cost(gk);
   return gk;

@@ -158,6 +158,7 @@ def _jobs():
     for sz in LN_FOLD_CASES:
         jobs.append(("ln_fold", "mlp", sz, None))
     jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_2STAGE", "1")))
+    jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_KSPLIT", "1")))
     for wl, sz in ATTN_CASES:
         for flag in ("", "1"):
             jobs.append(("env_plans", wl, sz, ("KORCH_ATTN_NO_KEY_SPLIT", flag)))

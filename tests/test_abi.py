@@ -416,6 +416,20 @@ def test_gemm_direct_to_lds_staging_selection(monkeypatch):
     assert "stashA" not in src
     _, src = gemm1(BIG_TILE_CASE)
     assert "global_load_lds_dwordx4" not in src and "stashA" in src
+    # the second product's intra-workgroup split of K keeps register staging;
+    # asked for direct-to-LDS staging, each group of four waves has its own
+    # 68 KiB of stages (two groups, 136 KiB)
+    p = graphs.build("mlp").plan("layered")
+    p.compile()
+    assert "global_load_lds_dwordx4" not in p.kernel_source(2)
+    monkeypatch.setenv("KORCH_GEMM_DMA_KSPLIT", "1")
+    p = graphs.build("mlp").plan("layered")
+    p.compile()
+    (_, block2, lds2), src2 = p.kernel_launch(2), p.kernel_source(2)
+    assert block2 == (512, 1, 1) and lds2 == 2 * (2 * 128 + 3 * 96) * 64 * 2
+    assert "16 A blocks and 12 B blocks of 1 KiB per k-tile, 2 A stages and 3 B stages" in src2
+    assert "readfirstlane(kgrp)" in src2
+    monkeypatch.delenv("KORCH_GEMM_DMA_KSPLIT")
     monkeypatch.setenv("KORCH_GEMM_DMA_2STAGE", "1")
     (_, _, lds), src = gemm1({})
     assert "2 A stages and 2 B stages" in src and lds == (2 * 256 + 2 * 192) * 64 * 2

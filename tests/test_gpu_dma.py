@@ -38,6 +38,25 @@ def _run(sizes, raw):
     return w, r, r.run(raw), sum("global_load_lds_dwordx4" in s for s in srcs), srcs
 
 
+def test_dma_staging_k_split_matches_register_staging(monkeypatch):
+    """The MLP block's second product (an intra-workgroup split of K) with
+    direct-to-LDS staging asked for (KORCH_GEMM_DMA_KSPLIT=1): oracle parity
+    and the same bytes as register staging."""
+    print("\n[case] mlp layered, k-split product with direct-to-LDS staging", flush=True)
+    raw, ref = reference("mlp", {})
+    monkeypatch.delenv("KORCH_GEMM_DMA", raising=False)
+    monkeypatch.setenv("KORCH_GEMM_DMA_KSPLIT", "1")
+    w, r, out, _, srcs = _run({}, raw)
+    assert "global_load_lds_dwordx4" in srcs[2]
+    ok, mx, rel = close(out["out"], ref["out"], TOL[w.dtype])
+    assert ok, f"max abs err {mx:.3e}, normwise rel {rel:.3e}"
+    monkeypatch.delenv("KORCH_GEMM_DMA_KSPLIT")
+    _, r0, _, _, srcs0 = _run({}, raw)
+    assert "global_load_lds_dwordx4" not in srcs0[2]
+    for a, b in zip(r.outs, r0.outs):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
 @pytest.mark.parametrize("stages", ["", "2"])
 @pytest.mark.parametrize("sizes", [{}] + DMA_CASES, ids=lambda s: "x".join(str(v) for v in s.values()) or "full")
 def test_dma_staging_matches_register_staging(sizes, stages, monkeypatch):
