@@ -162,6 +162,25 @@ def counters(args):
                f(m["SQ_LDS_BANK_CONFLICT"] / m["SQ_ACTIVE_INST_LDS"] if m.get("SQ_ACTIVE_INST_LDS") else None),
                f(share("SQ_WAIT_INST_LDS")), f(share("SQ_WAIT_INST_ANY")), f(share("SQ_ACTIVE_INST_VALU"))]
         lines.append("| " + " | ".join(row) + " |")
+    if any("TCP_TCC_READ_REQ" in m or "TCC_HIT" in m for m in med.values()):
+        # memory-side counters: TCP counters sum over the compute units' L1s,
+        # TCC over the L2 channels, GRBM_GUI_ACTIVE over the XCDs
+        lines += ["", "Memory side: `L2 round trip` = TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ (clocks from an L1 "
+                  "miss to its L2 answer, averaged over requests); `L1 pending stall` = TCP_PENDING_STALL_CYCLES / "
+                  f"({args.cus} L1s x GRBM_GUI_ACTIVE / {args.xcds}), the share of the kernel's cycles an L1 could not "
+                  "accept requests because too many were in flight; `L2 hit` = TCC_HIT / (TCC_HIT + TCC_MISS); "
+                  "`L2 to memory` = TCC_EA0_RDREQ (read requests from L2 to the Infinity Fabric).", "",
+                  "| kernel | L2 round trip (clk) | L1 pending stall | L2 hit | L2 to memory |", "|---|---|---|---|---|"]
+        for k in sorted(med):
+            m = med[k]
+            gui = m.get("GRBM_GUI_ACTIVE")
+            rt = m["TCP_TCC_READ_REQ_LATENCY"] / m["TCP_TCC_READ_REQ"] if m.get("TCP_TCC_READ_REQ") else None
+            ps = (m["TCP_PENDING_STALL_CYCLES"] / (args.cus * gui / args.xcds)
+                  if "TCP_PENDING_STALL_CYCLES" in m and gui else None)
+            hit = m["TCC_HIT"] / (m["TCC_HIT"] + m["TCC_MISS"]) if m.get("TCC_HIT") is not None and "TCC_MISS" in m else None
+            ea = m.get("TCC_EA0_RDREQ")
+            lines.append("| " + " | ".join([k, "" if rt is None else f"{rt:.0f}", "" if ps is None else f"{ps:.3f}",
+                                            "" if hit is None else f"{hit:.3f}", "" if ea is None else f"{ea:.0f}"]) + " |")
     lines += ["", "Raw medians:", "", "| kernel | counter | value |", "|---|---|---|"]
     for k in sorted(med):
         for c in sorted(med[k]):
@@ -195,6 +214,8 @@ def main():
     c.add_argument("--prefix", default="korch_k")
     c.add_argument("--simds", type=int, default=1024)
     c.add_argument("--ghz", type=float, default=2.4)
+    c.add_argument("--cus", type=int, default=256)
+    c.add_argument("--xcds", type=int, default=8)
     c.add_argument("--cmd", action="append", default=[])
     a = ap.parse_args()
     {"stats": stats, "pmc": pmc, "counters": counters}[a.mode](a)
