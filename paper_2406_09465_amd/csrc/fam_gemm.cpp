@@ -1053,7 +1053,26 @@ void plan_dma(const KInfo& ki, GemmSpec& sp, bool ksplit) {
                ? 3
                : 2;
   if (sp.dsb == 2 && ((sp.BM / 8) % NW || (sp.BN / 8) % NW)) return;  // equal load counts per wave
-  if ((size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * 2 > lds) return;
+  // deep staging when asked: S stages of each operand, both loaded S - 1
+  // k-tiles ahead by G = S - 1 wave groups per operand (group g loads the
+  // k-tiles j with j % G == g); S = 3, or 5 with KORCH_GEMM_DMA_STAGES=5 (one
+  // wave per group: slower, 34.2 us warm against 30.0 for the MLP block's
+  // second product, the same 37.5 after a cache flush)
+  sp.dsa = 2;
+  if (sp.dsb == 3 && (sp.want_a3 || (getenv("KORCH_GEMM_DMA_A3") && atoi(getenv("KORCH_GEMM_DMA_A3")) != 0))) {
+    const char* se = getenv("KORCH_GEMM_DMA_STAGES");
+    for (int S : {3, 5}) {
+      if ((se ? atoi(se) : 3) != S) continue;
+      const int G = S - 1;
+      if (NW % (2 * G)) continue;
+      const int per = NW / (2 * G);  // waves per loading group
+      if ((size_t)(S * sp.BM + S * sp.BN) * 64 * 2 <= lds && (sp.BM / 8) % per == 0 && (sp.BN / 8) % per == 0) {
+        sp.dsa = sp.dsb = S;
+        break;
+      }
+    }
+  }
+  if ((size_t)(sp.dsa * sp.BM + sp.dsb * sp.BN) * 64 * 2 > lds) return;
   int x0 = 0, x1 = 0, x3 = 0;
   if (!dma_b_swizzle(sp.BN / 8, x0, x1, x3)) return;
   sp.dx0 = x0, sp.dx1 = x1, sp.dx3 = x3;
@@ -1062,7 +1081,7 @@ void plan_dma(const KInfo& ki, GemmSpec& sp, bool ksplit) {
 
 // LayerNorm fold: LDS byte offset of gamma and beta (K halves each) and the
 // column sums gamma^T W, beta^T W (BN floats each), after the operand stages.
-static int64_t ln_lds_off(const GemmSpec& sp) { return (int64_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * 2; }
+static int64_t ln_lds_off(const GemmSpec& sp) { return (int64_t)(sp.dsa * sp.BM + sp.dsb * sp.BN) * 64 * 2; }
 static int64_t ln_lds_bytes(const GemmSpec& sp) { return sp.lnf ? 4 * sp.K + 8 * (int64_t)sp.BN : 0; }
 
 // Which waves load what.  With two right-operand stages every wave loads
@@ -1082,7 +1101,9 @@ struct DmaRoles {
 static DmaRoles dma_roles(const GemmSpec& sp) {
   DmaRoles r;
   r.NW = sp.NT / 64;
-  if (sp.dsb == 3) {
+  if (sp.dsa >= 3) {
+    r.ga = r.gb = r.NW / (2 * (sp.dsa - 1));
+  } else if (sp.dsb == 3) {
     r.ga = r.NW / 2, r.gb = r.NW / 4;
   } else {
     r.ga = r.NW, r.gb = r.NW;
@@ -1099,7 +1120,7 @@ static std::string dma_loader(const KInfo& ki, const GemmSpec& sp, const std::ma
   const std::string T = ctype(sp.mtype);
   const DmaRoles R = dma_roles(sp);
   const int P = sp.BN / 8;
-  const int64_t SAE = (int64_t)sp.BM * 64, SBE = (int64_t)sp.BN * 64, BOFF = 2 * SAE;
+  const int64_t SAE = (int64_t)sp.BM * 64, SBE = (int64_t)sp.BN * 64, BOFF = sp.dsa * SAE;
   auto boff = [&](int node) {
     const Shape& sh = g.nodes[node].shape;
     Shape ob(sp.OUT.begin(), sp.OUT.begin() + sp.nb);
@@ -1114,9 +1135,12 @@ static std::string dma_loader(const KInfo& ki, const GemmSpec& sp, const std::ma
   };
   std::ostringstream s;
   s << "  // direct-to-LDS staging: " << sp.BM / 8 << " A blocks and " << sp.BN / 8 << " B blocks of 1 KiB per k-tile, "
-    << "2 A stages and " << sp.dsb << " B stages\n";
+    << sp.dsa << " A stages and " << sp.dsb << " B stages\n";
   s << "  const int wv_ = __builtin_amdgcn_readfirstlane(wave);\n";
-  if (sp.dsb == 3) {
+  if (sp.dsa >= 3) {
+    s << "  const int par_ = wv_ / " << R.ga << " % " << sp.dsa - 1 << ", wa_ = wv_ % " << R.ga << ", wb_ = wv_ % " << R.gb
+      << ";  // the residue mod " << sp.dsa - 1 << " of the k-tiles the wave's group loads; loader index in the group\n";
+  } else if (sp.dsb == 3) {
     s << "  const int wa_ = wv_, wb_ = (wv_ - " << R.ga << ") % " << R.gb << ", par_ = (wv_ - " << R.ga << ") / " << R.gb
       << ";  // A loader index; B loader index and k-tile parity\n";
   } else {
@@ -1135,7 +1159,8 @@ static std::string dma_loader(const KInfo& ki, const GemmSpec& sp, const std::ma
     s << "  " << OT_ << " doff_[" << std::max(R.PA, R.PB) << "];\n";
   else
     s << "  " << OT_ << " doffA_[" << R.PA << "], doffB_[" << R.PB << "];\n";
-  if (sp.dsb == 3) s << "  if (wv_ < " << R.ga << ") {\n";
+  const int nA = sp.dsa >= 3 ? (sp.dsa - 1) * R.ga : R.ga;  // waves loading A
+  if (sp.dsb == 3) s << "  if (wv_ < " << nA << ") {\n";
   s << "#pragma unroll\n  for (int i = 0; i < " << R.PA << "; ++i) {\n";
   s << "    const int r = 8 * (wa_ + i * " << R.ga << ") + (l >> 3);\n";
   s << "    " << aoffs << "[i] = (" << OT_ << ")((m0 + r) * " << sp.K << "LL + (((l & 7) ^ (l >> 3)) * 8));\n  }\n";
@@ -1168,7 +1193,7 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst, bool kconst_
                                                : "__builtin_amdgcn_mfma_f32_16x16x32_bf16";
   const DmaRoles R = dma_roles(sp);
   const int SB = sp.dsb;
-  const int64_t SAE = (int64_t)sp.BM * 64, SBE = (int64_t)sp.BN * 64, BOFF = 2 * SAE;
+  const int64_t SAE = (int64_t)sp.BM * 64, SBE = (int64_t)sp.BN * 64, BOFF = sp.dsa * SAE;
   const int64_t LNO = ln_lds_off(sp);
   if (sp.lnf) {
     // gamma and beta into LDS once; per-lane row sums of X and X^2 (rows of the
@@ -1228,7 +1253,26 @@ static std::string dma_mainloop(const GemmSpec& sp, int64_t kconst, bool kconst_
   s << "  const int nkt_ = kt1 - kt0;\n";
   // a folded LayerNorm's statistics leave too few registers for the unrolled loop
   const bool unrolled = kconst > 0 && kconst <= 128 && !sp.lnf;
-  if (SB == 3) {
+  if (sp.dsa >= 3) {
+    // 2G loading groups (G = S - 1): A and B, one group per residue of the
+    // k-tile index mod G.  Group g loads tiles g, g + G, ...: tile j + G during
+    // tile j when j % G == g, and waits at the end of tile j when
+    // (j + 1) % G == g, before its tile j + 1 is read (it has issued nothing
+    // since that tile, so the full wait waits for that tile only).
+    const int S = sp.dsa, G = S - 1;
+    const std::string isA = "wv_ < " + std::to_string(G * R.ga), Gs = std::to_string(G), Ss = std::to_string(S);
+    s << "  if (par_ < nkt_) {\n    if (" << isA << ") dmaA_(kt0 + par_, par_);\n    else dmaB_(kt0 + par_, par_);\n  }\n";
+    s << "  if (par_ == 0) " << W0 << "\n";
+    s << "  __syncthreads();\n";
+    if (unrolled) s << "#pragma unroll\n  for (int j = 0; j < " << kconst << "; ++j) {\n";
+    else s << "  for (int j = 0; j < nkt_; ++j) {\n";
+    s << "    if (par_ == j % " << Gs << " && j + " << Gs << " < nkt_) {\n";
+    s << "      if (" << isA << ") dmaA_(kt0 + j + " << Gs << ", (j + " << Gs << ") % " << Ss << ");\n";
+    s << "      else dmaB_(kt0 + j + " << Gs << ", (j + " << Gs << ") % " << Ss << ");\n    }\n";
+    s << "    " << (kconst_exact ? "" : "if (j < nkt_) ") << "compute(j % " << Ss << ", j % " << Ss << ", kt0 + j);\n";
+    s << "    if (par_ == (j + 1) % " << Gs << ") " << W0 << "\n";
+    s << "    __syncthreads();\n  }\n";
+  } else if (SB == 3) {
     const std::string isA = "wv_ < " + std::to_string(R.ga);
     // tiles 0 (A, even B loaders) and 1 (odd B loaders); the loaders of tile 0 wait
     s << "  if (" << isA << ") dmaA_(kt0, 0);\n";
@@ -1478,7 +1522,7 @@ static size_t gemm_smem_bytes_fwd(const GemmSpec& sp) { return gemm_smem_bytes(s
 size_t gemm_smem_bytes(const GemmSpec& sp) {
   size_t bbuf = (size_t)b_buf_elems(sp);
   size_t ab = (size_t)2 * ((size_t)sp.BM * sp.BKP + bbuf) * dtype_bytes(sp.mtype);
-  if (sp.dma) ab = (size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype) + (size_t)ln_lds_bytes(sp);
+  if (sp.dma) ab = (size_t)(sp.dsa * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype) + (size_t)ln_lds_bytes(sp);
   if (sp.acc_t) return std::max(ab, (size_t)sp.OSB);
   size_t c = (size_t)(sp.CROWS ? sp.CROWS : sp.BM) * sp.LDC * 4;
   return std::max(ab, c);
@@ -1706,6 +1750,39 @@ std::string gemm_prologue_common(const GemmSpec& sp) {
   return s.str();
 }
 
+// Eight waves over the whole contraction, both operands staged direct-to-LDS
+// three k-tiles deep (loaded two k-tiles ahead), in place of the
+// intra-workgroup split of K (whose two groups of stages leave room for the
+// left operand one k-tile ahead only); asked for with KORCH_GEMM_DMA8=1.  The
+// MLP block's second product (4096 x 768 x 3072, 128 x 96 tiles, waves of
+// 32 x 48) alone took 30.0 us warm and 37.6 after a 512 MiB read, against 32.1
+// and 40.9 with the split and register staging (33.4 / 46.8 with eight waves
+// and two left-operand stages).  Inside the block's flushed step, after the
+// first product has written its left operand, it takes 31.0 us against 29.5
+// (26.5 against 29.1 warm): the split keeps two groups' loads in flight, twice
+// the bytes, while the weights come from HBM.  The split stays the default.
+static bool eight_wave_dma(const KInfo& ki, GemmSpec& sp, int64_t tiles, int64_t KT) {
+  const char* e = getenv("KORCH_GEMM_DMA8");
+  if (!(e && atoi(e) != 0)) return false;
+  if (sp.conv || sp.lnf || sp.mms.size() != 1 || tiles > 256 || KT < 16 || sp.NT != 256) return false;
+  if (sp.BM % 32 || sp.BN % 32) return false;
+  GemmSpec t = sp;
+  t.WM = sp.BM / 32;
+  t.WN = 2;
+  t.NT = 64 * t.WM * t.WN;
+  if (t.NT != 512) return false;
+  t.WTM = t.BM / t.WM;
+  t.WTN = t.BN / t.WN;
+  t.FM = t.WTM / 16;
+  t.FN = t.WTN / 16;
+  t.want_a3 = true;
+  plan_dma(ki, t, false);
+  if (!t.dma || t.dsa < 3) return false;
+  if (t.WM > 1 && !getenv("KORCH_GEMM_FULL_CTILE")) t.CROWS = t.WTM;
+  sp = t;
+  return true;
+}
+
 GenKernel gen_gemm(const KInfo& ki, int index) {
   GemmSpec sp;
   std::string why;
@@ -1733,8 +1810,9 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
   // MFMAs and loads, one group's waits covered by the other's products.
   const size_t op_bytes = (size_t)2 * ((size_t)sp.BM * sp.BKP + (size_t)b_buf_elems(sp)) * dtype_bytes(sp.mtype);
   const size_t ksplit_lds = std::max(2 * op_bytes, (size_t)sp.BM * sp.LDC * 4);
-  const bool ksplit = !sp.conv && !sp.lnf && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 && sp.NT == 256 &&
-                      ksplit_lds <= 160 * 1024 && !getenv("KORCH_GEMM_NO_KSPLIT");
+  const bool dma8 = eight_wave_dma(ki, sp, ntn * ntm * sp.batch, KT);
+  const bool ksplit = !dma8 && !sp.conv && !sp.lnf && sp.mms.size() == 1 && ntn * ntm * sp.batch <= 256 && KT >= 16 &&
+                      sp.NT == 256 && ksplit_lds <= 160 * 1024 && !getenv("KORCH_GEMM_NO_KSPLIT");
   const int64_t KH = (KT + 1) / 2;
   {
     // register relief 1: a tile's k-steps all before the barrier (one set of
@@ -1749,8 +1827,8 @@ GenKernel gen_gemm(const KInfo& ki, int index) {
     sp.OSB = sp.BM * sp.OSP * 2;
   }
   plan_dma(ki, sp, ksplit);
-  // with direct-to-LDS staging each k-group's operand stages take (2 BM + dsb BN) x 64 elements
-  const size_t grp_bytes = sp.dma ? (size_t)(2 * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype) : op_bytes;
+  // with direct-to-LDS staging each k-group's operand stages take (dsa BM + dsb BN) x 64 elements
+  const size_t grp_bytes = sp.dma ? (size_t)(sp.dsa * sp.BM + sp.dsb * sp.BN) * 64 * dtype_bytes(sp.mtype) : op_bytes;
   const size_t ksplit_lds_ = std::max(2 * grp_bytes, (size_t)sp.BM * sp.LDC * 4);
   if (sp.lnf) {
     // the fold needs direct-to-LDS staging (X tiles in their swizzled layout),

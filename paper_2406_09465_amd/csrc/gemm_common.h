@@ -64,7 +64,9 @@ struct GemmSpec {
   // c ^ f(k), f(k) = dx0 (k & 1) + dx1 ((k >> 1) & 1) + dx3 ((k >> 3) & 1).
   bool dma = false;
   int dx0 = 0, dx1 = 0, dx3 = 0;
-  int dsb = 2;  // right-operand stages (the left operand has two)
+  int dsb = 2;  // right-operand stages
+  int dsa = 2;  // left-operand stages (3: loaded two k-tiles ahead like the right operand)
+  bool want_a3 = false;  // ask plan_dma for three left-operand stages
   // LayerNorm folded into the product (see detect_ln_fold): the left operand
   // is LN(X) = (X - mu) r gamma + beta over X's last axis; the kernel stages X,
   // multiplies X gamma by the right operand W, accumulates each row's sum and

@@ -66,6 +66,16 @@ DMA_CASES = [
     dict(m=512, d=128, h=512),
 ]
 
+# MLP shapes whose second product, asked for eight waves over the whole
+# contraction with three direct-to-LDS stages of each operand
+# (KORCH_GEMM_DMA8=1; 128-row tiles dividing the problem, at most one per
+# compute unit), takes them: odd numbers of k-tiles (31, and 17 in bf16 over
+# 240 tiles).  Each also runs register-staged without the split.
+DMA8_CASES = [
+    dict(m=4096, d=768, h=1984),
+    dict(m=3840, d=768, h=1088, dtype="bf16"),
+]
+
 # MLP shapes of the folded-LayerNorm GPU tests: plans whose first kernel holds
 # the LayerNorm, the first product and (or not) the GELU.
 LN_FOLD_CASES = [{}, dict(m=1024, d=256, h=768)]
@@ -151,13 +161,19 @@ def _jobs():
             jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_NO_KSPLIT", flag)))
     jobs.append(("plans", "mlp", WIDE_TILE_CASE, None))
     jobs.append(("plans", "mlp", BIG_TILE_CASE, None))
-    for sz in DMA_CASES:
-        jobs.append(("plans", "mlp", sz, None))
+    for sz in DMA8_CASES + [{}]:
+        jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_DMA8", "1")))
+        jobs.append(("env_plans", "mlp", sz, (("KORCH_GEMM_DMA8", "1"), ("KORCH_GEMM_DMA_STAGES", "5"))))
+    for sz in DMA_CASES + DMA8_CASES + [{}]:
+        if sz:
+            jobs.append(("plans", "mlp", sz, None))
         jobs.append(("env_plans", "mlp", sz, ("KORCH_GEMM_DMA", "0")))
-    jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA", "0")))
+        jobs.append(("env_plans", "mlp", sz, (("KORCH_GEMM_NO_KSPLIT", "1"),)))
+        jobs.append(("env_plans", "mlp", sz, (("KORCH_GEMM_NO_KSPLIT", "1"), ("KORCH_GEMM_DMA", "0"))))
     for sz in LN_FOLD_CASES:
         jobs.append(("ln_fold", "mlp", sz, None))
     jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_2STAGE", "1")))
+    jobs.append(("env_plans", "mlp", {}, (("KORCH_GEMM_NO_KSPLIT", "1"), ("KORCH_GEMM_DMA_2STAGE", "1"))))
     jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_KSPLIT", "1")))
     for wl, sz in ATTN_CASES:
         for flag in ("", "1"):
@@ -210,23 +226,26 @@ def _run_job(job, part=0, parts=1):
                 failures.append((w, sz, pn, str(e)[:200]))
     elif kind == "env_plans":
         import os
-        var, val = extra
-        prev = os.environ.get(var)
-        if val:
-            os.environ[var] = val
-        else:
-            os.environ.pop(var, None)
+        pairs = (extra,) if isinstance(extra[0], str) else extra  # one (var, value) or several
+        prev = {var: os.environ.get(var) for var, _ in pairs}
+        for var, val in pairs:
+            if val:
+                os.environ[var] = val
+            else:
+                os.environ.pop(var, None)
+        tag = " ".join(f"{var}={val}" for var, val in pairs)
         try:
             for pn in ("layered", "fused"):
                 try:
                     wl.plan(pn).compile()
                 except KorchError as e:
-                    failures.append((w, sz, f"{pn} {var}={val}", str(e)[:200]))
+                    failures.append((w, sz, f"{pn} {tag}", str(e)[:200]))
         finally:
-            if prev is None:
-                os.environ.pop(var, None)
-            else:
-                os.environ[var] = prev
+            for var, old in prev.items():
+                if old is None:
+                    os.environ.pop(var, None)
+                else:
+                    os.environ[var] = old
     elif kind in ("sampled", "sampled_layouts"):
         if kind == "sampled_layouts":
             from ._abi import RW_LAYOUT_VARIANTS

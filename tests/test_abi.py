@@ -336,25 +336,24 @@ def test_timed_execute_rejects_a_kernel_outside_the_range():
     assert code(lambda: p.execute_timed(1, 1, [0] * 6, [0], 0, 0, 0, 0, 0, 0)) == -1
 
 
-def test_gemm_k_split_selection():
+def test_gemm_k_split_selection(monkeypatch):
     """GEMM2 of the MLP block (256 tiles, 48 k-tiles) and of the odd-k test shape
-    use the intra-workgroup split of K; GEMM1 (512 tiles) and
-    KORCH_GEMM_NO_KSPLIT=1 do not."""
+    use the intra-workgroup split of K; GEMM1 (256 x 192 tiles of eight waves)
+    and KORCH_GEMM_NO_KSPLIT=1 do not.  Asked for (KORCH_GEMM_DMA8=1), the split
+    gives way to eight waves over the whole contraction where both operands can
+    be staged three k-tiles deep (tiles of 128 rows dividing the problem), and
+    stays for ragged rows and for 64-row tiles."""
     from paper_2406_09465_amd.warm import GEMM_CASES
 
     def sources(sizes, flag):
-        prev = os.environ.pop("KORCH_GEMM_NO_KSPLIT", None)
+        monkeypatch.delenv("KORCH_GEMM_NO_KSPLIT", raising=False)
         if flag:
-            os.environ["KORCH_GEMM_NO_KSPLIT"] = flag
-        try:
-            p = graphs.build("mlp", **sizes).plan("layered")
-            p.compile()
-            return [p.kernel_source(k) for k in range(p.num_kernels())], [p.kernel_launch(k) for k in range(3)]
-        finally:
-            os.environ.pop("KORCH_GEMM_NO_KSPLIT", None)
-            if prev is not None:
-                os.environ["KORCH_GEMM_NO_KSPLIT"] = prev
+            monkeypatch.setenv("KORCH_GEMM_NO_KSPLIT", flag)
+        p = graphs.build("mlp", **sizes).plan("layered")
+        p.compile()
+        return [p.kernel_source(k) for k in range(p.num_kernels())], [p.kernel_launch(k) for k in range(3)]
 
+    monkeypatch.delenv("KORCH_GEMM_DMA8", raising=False)
     for sz in [{}] + GEMM_CASES:
         src, launch = sources(sz, "")
         assert "kgrp" in src[2] and launch[2][1][0] == 512, sz
@@ -362,6 +361,11 @@ def test_gemm_k_split_selection():
         assert "kgrp" not in src[2] and launch[2][1][0] == 256, sz
     src, _ = sources({}, "")
     assert "kgrp" not in src[1]
+    monkeypatch.setenv("KORCH_GEMM_DMA8", "1")
+    for sz, dma8 in zip([{}] + GEMM_CASES, [True, False, False]):
+        src, launch = sources(sz, "")
+        assert launch[2][1][0] == 512, sz
+        assert ("3 A stages and 3 B stages" in src[2]) == dma8 and ("kgrp" in src[2]) != dma8, sz
 
 
 def test_gemm_wide_tile_selection():
@@ -408,6 +412,9 @@ def test_gemm_direct_to_lds_staging_selection(monkeypatch):
 
     monkeypatch.delenv("KORCH_GEMM_DMA", raising=False)
     monkeypatch.delenv("KORCH_GEMM_DMA_2STAGE", raising=False)
+    monkeypatch.delenv("KORCH_GEMM_DMA8", raising=False)
+    monkeypatch.delenv("KORCH_GEMM_DMA_A3", raising=False)
+    monkeypatch.delenv("KORCH_GEMM_DMA_STAGES", raising=False)
     (grid, block, lds), src = gemm1({})
     assert "32 A blocks and 24 B blocks of 1 KiB per k-tile, 2 A stages and 3 B stages" in src
     assert lds == (2 * 256 + 3 * 192) * 64 * 2
@@ -416,12 +423,30 @@ def test_gemm_direct_to_lds_staging_selection(monkeypatch):
     assert "stashA" not in src
     _, src = gemm1(BIG_TILE_CASE)
     assert "global_load_lds_dwordx4" not in src and "stashA" in src
-    # the second product's intra-workgroup split of K keeps register staging;
-    # asked for direct-to-LDS staging, each group of four waves has its own
-    # 68 KiB of stages (two groups, 136 KiB)
+    # asked for (KORCH_GEMM_DMA8=1), the second product (one 128 x 96 tile per
+    # compute unit, K = 3072) runs eight waves of 32 x 48 over the whole
+    # contraction with three stages of each operand (both loaded two k-tiles
+    # ahead by their own wave groups per k-tile parity) instead of the
+    # intra-workgroup split of K; with KORCH_GEMM_DMA_STAGES=5, five stages
+    # loaded four ahead by one wave per residue of the k-tile index mod 4
+    monkeypatch.setenv("KORCH_GEMM_DMA8", "1")
+    for stages, par in ((3, "par_ = wv_ / 2 % 2"), (5, "par_ = wv_ / 1 % 4")):
+        monkeypatch.setenv("KORCH_GEMM_DMA_STAGES", str(stages))
+        p = graphs.build("mlp").plan("layered")
+        p.compile()
+        (_, block2, lds2), src2 = p.kernel_launch(2), p.kernel_source(2)
+        assert f"16 A blocks and 12 B blocks of 1 KiB per k-tile, {stages} A stages and {stages} B stages" in src2
+        assert block2 == (512, 1, 1) and lds2 == stages * (128 + 96) * 64 * 2
+        assert "kgrp" not in src2 and par in src2
+        assert set(re.findall(r"s_waitcnt vmcnt\((\d+)\)", src2)) == {"0"}
+    monkeypatch.delenv("KORCH_GEMM_DMA_STAGES")
+    monkeypatch.delenv("KORCH_GEMM_DMA8")
+    # by default the split keeps register staging; asked for direct-to-LDS
+    # staging, each group of four waves has its own 68 KiB of stages (two
+    # groups, 136 KiB)
     p = graphs.build("mlp").plan("layered")
     p.compile()
-    assert "global_load_lds_dwordx4" not in p.kernel_source(2)
+    assert "global_load_lds_dwordx4" not in p.kernel_source(2) and "kgrp" in p.kernel_source(2)
     monkeypatch.setenv("KORCH_GEMM_DMA_KSPLIT", "1")
     p = graphs.build("mlp").plan("layered")
     p.compile()

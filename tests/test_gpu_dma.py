@@ -2,10 +2,14 @@
 
 Products whose operands are plain 16-bit tensors and whose tiles divide the
 problem stage both operand tiles with direct global-to-LDS loads in swizzled
-layouts (the MLP block's first product in the layered plan).  The staging
-changes no arithmetic: the same MFMAs run in the same order on the same
-values, so each case must give the same bytes as the register-staged kernel
-(KORCH_GEMM_DMA=0) and match the float64 oracle within the dtype tolerance.
+layouts (the MLP block's first product in the layered plan; asked for, the
+second as eight waves over the whole contraction with three or five stages of
+each operand).
+The staging changes no arithmetic: every output element sums the same
+products in the same k order, so each case must give the same bytes as the
+register-staged kernel over the whole contraction (KORCH_GEMM_DMA=0 and
+KORCH_GEMM_NO_KSPLIT=1) and match the float64 oracle within the dtype
+tolerance.
 Repeated executions, with and without a cache flush between them, must give
 identical bytes (the waits before each barrier cover every load a tile
 needs).
@@ -15,7 +19,7 @@ import ctypes as C
 
 import pytest
 
-from paper_2406_09465_amd.warm import DMA_CASES
+from paper_2406_09465_amd.warm import DMA8_CASES, DMA_CASES
 from tests.helpers import TOL, close
 from tests.test_gpu_parity import reference
 
@@ -45,9 +49,10 @@ def test_dma_staging_k_split_matches_register_staging(monkeypatch):
     print("\n[case] mlp layered, k-split product with direct-to-LDS staging", flush=True)
     raw, ref = reference("mlp", {})
     monkeypatch.delenv("KORCH_GEMM_DMA", raising=False)
+    monkeypatch.delenv("KORCH_GEMM_DMA8", raising=False)
     monkeypatch.setenv("KORCH_GEMM_DMA_KSPLIT", "1")
     w, r, out, _, srcs = _run({}, raw)
-    assert "global_load_lds_dwordx4" in srcs[2]
+    assert "global_load_lds_dwordx4" in srcs[2] and "kgrp" in srcs[2]
     ok, mx, rel = close(out["out"], ref["out"], TOL[w.dtype])
     assert ok, f"max abs err {mx:.3e}, normwise rel {rel:.3e}"
     monkeypatch.delenv("KORCH_GEMM_DMA_KSPLIT")
@@ -65,6 +70,9 @@ def test_dma_staging_matches_register_staging(sizes, stages, monkeypatch):
     print(f"\n[case] mlp {sizes} layered, direct-to-LDS staging, stages={stages or 'default'}", flush=True)
     raw, ref = reference("mlp", sizes)
     monkeypatch.delenv("KORCH_GEMM_DMA", raising=False)
+    # no intra-workgroup split of K in either run, so both sum each output's
+    # products in one k order
+    monkeypatch.setenv("KORCH_GEMM_NO_KSPLIT", "1")
     if stages:
         monkeypatch.setenv("KORCH_GEMM_DMA_2STAGE", "1")
     else:
@@ -84,19 +92,52 @@ def test_dma_staging_matches_register_staging(sizes, stages, monkeypatch):
         assert a.dtype == b.dtype and torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
-def test_dma_staging_repeats_bitwise(monkeypatch):
-    """The full MLP block's layered plan, 100 back-to-back executions and 20
-    after a 512 MiB cache flush each (loads from HBM take longer than one
-    k-tile's products): identical bytes every time."""
+@pytest.mark.parametrize("stages", ["3", "5"])
+@pytest.mark.parametrize("sizes", [{}] + DMA8_CASES, ids=lambda s: "x".join(str(v) for v in s.values()) or "full")
+def test_eight_wave_dma_matches_register_staging(sizes, stages, monkeypatch):
+    """Second products on the eight-wave path (KORCH_GEMM_DMA8=1), 48 k-tiles
+    and odd numbers of them (the loading groups of each operand take the
+    k-tiles by residue mod 2, or mod 4 with five stages, so the last tiles fall
+    to different groups): oracle parity, and the same bytes as register staging
+    over the whole contraction."""
+    print(f"\n[case] mlp {sizes} layered, eight waves, {stages} stages per operand", flush=True)
+    raw, ref = reference("mlp", sizes)
+    for var in ("KORCH_GEMM_DMA", "KORCH_GEMM_NO_KSPLIT", "KORCH_GEMM_DMA_2STAGE"):
+        monkeypatch.delenv(var, raising=False)
+    monkeypatch.setenv("KORCH_GEMM_DMA8", "1")
+    monkeypatch.setenv("KORCH_GEMM_DMA_STAGES", stages)
+    w, r, out, _, srcs = _run(sizes, raw)
+    assert f"{stages} A stages and {stages} B stages" in srcs[2] and "kgrp" not in srcs[2]
+    ok, mx, rel = close(out["out"], ref["out"], TOL[w.dtype])
+    assert ok, f"mlp {sizes}: max abs err {mx:.3e}, normwise rel {rel:.3e}"
+    monkeypatch.setenv("KORCH_GEMM_DMA", "0")
+    monkeypatch.setenv("KORCH_GEMM_NO_KSPLIT", "1")
+    monkeypatch.delenv("KORCH_GEMM_DMA8")
+    monkeypatch.delenv("KORCH_GEMM_DMA_STAGES")
+    _, r0, _, ndma0, _ = _run(sizes, raw)
+    assert ndma0 == 0
+    for a, b in zip(r.outs, r0.outs):
+        assert a.dtype == b.dtype and torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("dma8", ["", "1"])
+def test_dma_staging_repeats_bitwise(dma8, monkeypatch):
+    """The full MLP block's layered plan (and with the second product on the
+    eight-wave path), 100 back-to-back executions and 20 after a 512 MiB cache
+    flush each (loads from HBM take longer than one k-tile's products):
+    identical bytes every time."""
     from paper_2406_09465_amd import graphs
     from paper_2406_09465_amd._abi import lib
     from paper_2406_09465_amd.runner import PlanRunner
     from synthetic import workloads as W
-    monkeypatch.delenv("KORCH_GEMM_DMA", raising=False)
-    monkeypatch.delenv("KORCH_GEMM_DMA_2STAGE", raising=False)
-    print("\n[case] mlp layered, direct-to-LDS staging, repeated", flush=True)
+    for var in ("KORCH_GEMM_DMA", "KORCH_GEMM_DMA8", "KORCH_GEMM_NO_KSPLIT", "KORCH_GEMM_DMA_2STAGE", "KORCH_GEMM_DMA_STAGES"):
+        monkeypatch.delenv(var, raising=False)
+    if dma8:
+        monkeypatch.setenv("KORCH_GEMM_DMA8", dma8)
+    print(f"\n[case] mlp layered, direct-to-LDS staging, repeated, dma8={dma8}", flush=True)
     r = PlanRunner(graphs.build("mlp"), "layered")
-    assert any("global_load_lds_dwordx4" in r.plan.kernel_source(i) for i in range(r.plan.num_kernels()))
+    assert "global_load_lds_dwordx4" in r.plan.kernel_source(1)
+    assert ("3 A stages and 3 B stages" in r.plan.kernel_source(2)) == bool(dma8)
     r.set_inputs(W.inputs("mlp"))
     r.launch()
     torch.cuda.synchronize()

@@ -30,10 +30,10 @@ def _gpu():
 def test_gemm_k_split(sizes, plan, no_split, monkeypatch):
     from paper_2406_09465_amd import graphs
     from paper_2406_09465_amd.runner import PlanRunner
+    monkeypatch.delenv("KORCH_GEMM_NO_KSPLIT", raising=False)
+    monkeypatch.delenv("KORCH_GEMM_DMA8", raising=False)
     if no_split:
         monkeypatch.setenv("KORCH_GEMM_NO_KSPLIT", no_split)
-    else:
-        monkeypatch.delenv("KORCH_GEMM_NO_KSPLIT", raising=False)
     print(f"\n[case] mlp {sizes} {plan} no_split={no_split}", flush=True)
     w = graphs.build("mlp", **sizes)
     raw, ref = reference("mlp", sizes)
