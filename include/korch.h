@@ -169,7 +169,9 @@ typedef enum {
   KORCH_RW_MERGE_PRODUCTS = 4,     /* A . B1, A . B2 -> column slices of A . concat(B1, B2)          */
   KORCH_RW_FOLD_SCALE = 8,         /* (A . B) * s -> A . (B * s), s varying only along the output
                                       columns (channels); also for convolutions and for division    */
-  KORCH_RW_ALL = 15,
+  KORCH_RW_SPLIT_MOMENTS = 32,     /* D = X - mean(X) over a non-last axis read by a variance (mean of
+                                      D^2) and by other nodes: the square reads its own copy X - m  */
+  KORCH_RW_ALL = 47,
   KORCH_RW_LAYOUT_VARIANTS = 16    /* layout as a plan variable (Section 8): each computed operand of
                                       a product is followed by transpose(transpose(x)) of its last
                                       two axes, so a plan may store x in either layout; applied once,

@@ -49,8 +49,8 @@ OPS = {
 }
 OP_NAMES = {v: k for k, v in OPS.items()}
 # primitive-graph transformation rules (korch_rewrite_rule)
-RW_DEFER_DIV, RW_REDUCE_AS_PRODUCT, RW_MERGE_PRODUCTS, RW_FOLD_SCALE, RW_ALL = 1, 2, 4, 8, 15
-RW_LAYOUT_VARIANTS = 16
+RW_DEFER_DIV, RW_REDUCE_AS_PRODUCT, RW_MERGE_PRODUCTS, RW_FOLD_SCALE, RW_ALL = 1, 2, 4, 8, 47
+RW_LAYOUT_VARIANTS, RW_SPLIT_MOMENTS = 16, 32
 FAMILIES = {0: "none", 1: "pointwise", 2: "row", 3: "colreduce", 4: "gemm", 5: "conv", 6: "attention", 7: "splitk"}
 
 E_UNSUPPORTED = -20

@@ -476,8 +476,74 @@ GenKernel gen_row(const KInfo& ki, int index) {
 // order (deterministic).  Elementwise / layout prologue and epilogue allowed.
 // ---------------------------------------------------------------------------
 
+// Column moments: a kernel holding a mean m = mean(X) over a non-last axis, the
+// centred values D = X - m (or m - X), their squares and v = mean(D^2) (the variance of a
+// normalization fissioned into primitives, Section 3), with X's elementwise or
+// layout prologue and an epilogue over the reduced shape.  D and D^2 stay
+// inside the kernel (neither is an output nor read by another of its nodes).
+struct Moments {
+  int r1 = -1, r2 = -1, D = -1, D2 = -1;
+};
+
+static bool detect_moments(const KInfo& ki, Moments& mo, std::string* why) {
+  const Graph& g = ki.g;
+  auto no = [&](const char* m) {
+    if (why) *why = std::string("colreduce moments: ") + m;
+    return false;
+  };
+  if (!ki.linear.empty() || ki.reduces.size() != 2) return no("needs two reductions and no linear primitive");
+  int a = ki.reduces[0], b = ki.reduces[1];
+  if (ki.ancestor(b, a)) std::swap(a, b);
+  const Node& na = g.nodes[a];
+  const Node& nb = g.nodes[b];
+  if (na.op != KORCH_REDUCE_MEAN || nb.op != KORCH_REDUCE_MEAN) return no("both reductions must be means");
+  const int X = na.in[0];
+  const Shape& S = g.nodes[X].shape;
+  if (g.nodes[nb.in[0]].shape != S || na.axis != nb.axis || na.shape != nb.shape) return no("reductions differ in shape");
+  if (na.axis == (int)S.size() - 1) return no("last-axis reduction belongs to the row family");
+  const int D2 = nb.in[0];
+  const Node& n2 = g.nodes[D2];
+  int D = -1;
+  if (n2.op == KORCH_SQUARE)
+    D = n2.in[0];
+  else if (n2.op == KORCH_MUL && n2.in.size() == 2 && n2.in[0] == n2.in[1])
+    D = n2.in[0];
+  else
+    return no("the second mean is not over a square");
+  const Node& nd = g.nodes[D];
+  // X - m, or m - X (the same squares)
+  if (nd.op != KORCH_SUB || nd.attrs.has_scalar || nd.in.size() != 2 ||
+      !((nd.in[0] == X && nd.in[1] == a) || (nd.in[0] == a && nd.in[1] == X)))
+    return no("the squared values are not X minus its mean");
+  if (!ki.in.count(D) || !ki.in.count(D2)) return no("centred values computed outside the kernel");
+  for (int o : ki.k.outs)
+    if (o == D || o == D2) return no("centred values are an output");
+  for (int c : g.consumers[D])
+    if (ki.in.count(c) && c != D2) return no("centred values read by another node of the kernel");
+  for (int c : g.consumers[D2])
+    if (ki.in.count(c) && c != b) return no("squares read by another node of the kernel");
+  for (int v : ki.k.prims) {
+    if (v == a || v == b || v == D || v == D2) continue;
+    const bool pro = ki.ancestor(v, a), epi = ki.ancestor(a, v) || ki.ancestor(b, v);
+    if (pro && !epi) {
+      if (g.nodes[v].shape != S && op_kind(g.nodes[v].op) != Kind::Layout) return no("prologue node shape differs");
+      if (std::find(ki.k.outs.begin(), ki.k.outs.end(), v) != ki.k.outs.end()) return no("prologue node is an output");
+    } else if (epi && !pro) {
+      if (g.nodes[v].shape != na.shape) return no("epilogue node shape differs from the reduced shape");
+    } else {
+      return no("node unrelated to the reductions");
+    }
+  }
+  mo.r1 = a, mo.r2 = b, mo.D = D, mo.D2 = D2;
+  return true;
+}
+
 bool match_colreduce(const KInfo& ki, std::string* why) {
   const Graph& g = ki.g;
+  if (ki.linear.empty() && ki.reduces.size() == 2) {
+    Moments mo;
+    return detect_moments(ki, mo, why);
+  }
   if (!ki.linear.empty() || ki.reduces.size() != 1) {
     *why = "colreduce: needs exactly one reduction and no linear primitive";
     return false;
@@ -520,9 +586,256 @@ bool match_colreduce(const KInfo& ki, std::string* why) {
 // the last to finish (device-scope counter, one release by thread 0, reset by
 // that workgroup) sums them in split order (deterministic) and runs the
 // epilogue.
+// Column moments in one pass over X (the kernel detect_moments accepts).  The
+// geometry is the column reduction's (BB lanes along the kept columns, LY rows
+// along the reduced axis, SPLIT workgroups along it).  Each thread runs
+// Welford's update over its rows, keeping a count n, a mean and M2 (the sum
+// of squared deviations from the running mean); triples merge with Chan,
+// Golub and LeVeque's pairwise formula
+//   n = na + nb,  mean = ma + (mb - ma) nb / n,  M2 = M2a + M2b + (mb - ma)^2 na nb / n,
+// always with the lower lane, wave or split as a, in a fixed order (lanes by
+// butterflies, then the four waves, then the splits' partials in split
+// order), so results are deterministic.  The mean m and v = M2 / L are what
+// the graph's two means compute (up to rounding); X is read once.
+static GenKernel gen_colmoments(const KInfo& ki, int index, const Moments& mo) {
+  const Graph& g = ki.g;
+  GenKernel gk;
+  gk.family = KORCH_FAM_COLREDUCE;
+  gk.name = kernel_name(index, "colreduce");
+  std::map<int, int> slot;
+  ki.assign_args(gk, slot);
+  const Node& rn = g.nodes[mo.r1];
+  const int X = rn.in[0];
+  const Shape& S = g.nodes[X].shape;
+  const int ax = rn.axis;
+  const int R = (int)S.size();
+  int64_t A = 1, B = 1, Lr = S[ax];
+  for (int d = 0; d < ax; ++d) A *= S[d];
+  for (int d = ax + 1; d < R; ++d) B *= S[d];
+  const int64_t Bin = S[R - 1];
+  const int VB = Bin % 8 == 0 ? 8 : (Bin % 4 == 0 ? 4 : (Bin % 2 == 0 ? 2 : 1));
+  const int64_t BV = B / VB;
+  const int BB = BV >= 64 ? 64 : (int)pow2ceil(BV);
+  const int LY = 256 / BB;
+  const int64_t ctiles = (BV + BB - 1) / BB;
+  int64_t SPLIT = std::max<int64_t>(1, std::min<int64_t>((256 + ctiles * A - 1) / (ctiles * A), Lr / (4 * LY)));
+  const int64_t chunk = (Lr + SPLIT - 1) / SPLIT;
+  SPLIT = (Lr + chunk - 1) / chunk;
+  std::vector<Ix> xi(S.size());
+  for (int d = 0; d < ax; ++d) xi[d] = Ix::var("a" + std::to_string(d));
+  xi[ax] = Ix::var("l");
+  for (int d = ax + 1; d < R; ++d)
+    xi[d] = d == R - 1 ? Ix::var("b" + std::to_string(d), 1, VB) : Ix::var("b" + std::to_string(d));
+  Emitter pe(g);
+  pe.inset = ki.in;
+  pe.argslot = slot;
+  pe.vec = VB;
+  const std::string xv = pe.value(X, xi);
+  std::vector<Ix> ri;
+  for (int d = 0; d < ax; ++d) ri.push_back(xi[d]);
+  if ((int)rn.shape.size() == R) ri.push_back(Ix::k(0));
+  for (int d = ax + 1; d < R; ++d) ri.push_back(xi[d]);
+  Emitter ee(g);
+  ee.inset = ki.in;
+  ee.argslot = slot;
+  ee.vec = VB;
+  const std::string k1 = Emitter::key(mo.r1, ri), k2 = Emitter::key(mo.r2, ri);
+  ee.provide = [&](int node, const std::vector<Ix>& idx, std::string* out) {
+    if (node != mo.r1 && node != mo.r2) return false;
+    if (Emitter::key(node, idx) != (node == mo.r1 ? k1 : k2))
+      fail(KORCH_E_UNSUPPORTED, "colreduce moments: reduction read at another index");
+    *out = node == mo.r1 ? "s1_[e]" : "s2_[e]";
+    return true;
+  };
+  for (int o : ki.k.outs) {
+    const Node& on = g.nodes[o];
+    auto bi = broadcast_index(on.shape, rn.shape, ri);
+    std::string v = ee.value(o, bi);
+    auto strd = strides_of(on.shape);
+    Ix off = Ix::k(0);
+    for (size_t d = 0; d < bi.size(); ++d) off = ix_add(off, ix_mulk(bi[d], strd[d], VB));
+    ee.body << "        "
+            << out_store(g, o, "((" + ctype(on.dtype) + "*)a.p[" + std::to_string(ki.out_slot(o)) + "])", off.at(), 0, v)
+            << ";\n";
+  }
+  int scr_slot = -1, cnt_slot = -1;
+  if (SPLIT > 1) {
+    ArgRef scr;
+    scr.kind = ArgRef::Scratch;
+    scr.bytes = (size_t)(2 * A * SPLIT * B) * 4;  // mean and M2 planes (a split's count is its row count)
+    scr_slot = (int)gk.args.size();
+    gk.args.push_back(scr);
+    ArgRef cnt;
+    cnt.kind = ArgRef::Counter;
+    cnt.bytes = (size_t)(A * ctiles) * (SPLIT > 32 ? (SPLIT + 15) / 16 + 1 : 1) * 128;
+    cnt_slot = (int)gk.args.size();
+    gk.args.push_back(cnt);
+  }
+  const std::string VBs = std::to_string(VB), BBs = std::to_string(BB);
+  std::ostringstream s;
+  s << source_header((int)gk.args.size());
+  s << "extern \"C\" __global__ void __launch_bounds__(256) " << gk.name << "(KArgs a) {\n";
+  s << "  __shared__ float red[3 * 256 * " << VB << "];\n";
+  if (SPLIT > 1) s << "  __shared__ int last_;\n";
+  s << "  const int tid = threadIdx.x, bl = tid % " << BB << ", ly = tid / " << BB << ";\n";
+  s << "  const i64 bv0 = (i64)blockIdx.x * " << BB << " + bl;\n";
+  s << "  const bool bv = bv0 < " << BV << "LL;\n";
+  s << "  const i64 bi = (bv ? bv0 : " << BV - 1 << "LL) * " << VB << ";\n";
+  s << "  const i64 ay = blockIdx.y;\n  i64 q_ = ay;\n";
+  for (int d = ax - 1; d >= 0; --d) s << "  const i64 a" << d << " = q_ % " << S[d] << "LL; q_ /= " << S[d] << "LL;\n";
+  s << "  q_ = bi;\n";
+  for (int d = R - 1; d > ax; --d) s << "  const i64 b" << d << " = q_ % " << S[d] << "LL; q_ /= " << S[d] << "LL;\n";
+  s << "  const i64 l0 = (i64)blockIdx.z * " << chunk << ", l1 = l0 + " << chunk << " < " << Lr << "LL ? l0 + " << chunk
+    << " : " << Lr << "LL;\n";
+  // Welford over this thread's rows (one count for its VB columns)
+  s << "  float cn_ = 0.0f, mu_[" << VB << "], m2_[" << VB << "];\n";
+  s << "#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) mu_[e] = 0.0f, m2_[e] = 0.0f;\n";
+  s << "#pragma unroll 4\n  for (i64 l = l0 + ly; l < l1; l += " << LY << ") {\n" << pe.pre.str();
+  s << "    cn_ += 1.0f;\n    const float inv_ = __builtin_amdgcn_rcpf(cn_);\n";
+  s << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n" << pe.body.str();
+  s << "      const float x_ = " << xv << ";\n";
+  s << "      const float d_ = x_ - mu_[e];\n      mu_[e] += d_ * inv_;\n      m2_[e] += d_ * (x_ - mu_[e]);\n    }\n  }\n";
+  // merge (na, ma, qa) (the lower) with (nb, mb, qb): f = nb / n, w = na nb / n
+  s << "  const int wv_ = tid >> 6, lane_ = tid & 63;\n";
+  if (BB < 64) {
+    s << "#pragma unroll\n  for (int m_ = " << BB << "; m_ < 64; m_ <<= 1) {\n";
+    s << "    const bool lo_ = (lane_ & m_) == 0;\n";
+    s << "    const float on_ = __shfl_xor(cn_, m_, 64);\n";
+    s << "    const float na_ = lo_ ? cn_ : on_, nb_ = lo_ ? on_ : cn_;\n";
+    s << "    const float nt_ = na_ + nb_, f_ = nt_ > 0.0f ? nb_ * __builtin_amdgcn_rcpf(nt_) : 0.0f, w_ = na_ * f_;\n";
+    s << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n";
+    s << "      const float om_ = __shfl_xor(mu_[e], m_, 64), oq_ = __shfl_xor(m2_[e], m_, 64);\n";
+    s << "      const float ma_ = lo_ ? mu_[e] : om_, d_ = (lo_ ? om_ : mu_[e]) - ma_;\n";
+    s << "      mu_[e] = ma_ + d_ * f_;\n      m2_[e] = m2_[e] + oq_ + d_ * d_ * w_;\n    }\n";
+    s << "    cn_ = nt_;\n  }\n";
+  }
+  // The four waves' triples through LDS; then one thread per column of the
+  // tile (TC = BB * VB columns) merges them in wave order, and (with a split
+  // reduced axis) stores the column's partial triple.  The column's final mean
+  // and M2 end in LDS (cm_, cq_), where the threads of row 0 read them.
+  const int TC = BB * VB;
+  const std::string PL = std::to_string(4 * TC);  // floats per plane of the wave triples
+  s << "  __shared__ float cm_[" << TC << "], cq_[" << TC << "];\n";
+  s << "  if (lane_ < " << BB << ") {\n";
+  s << "    red[wv_ * " << BB << " + lane_] = cn_;\n";
+  s << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n";
+  s << "      red[" << PL << " + wv_ * " << TC << " + lane_ * " << VB << " + e] = mu_[e];\n";
+  s << "      red[2 * " << PL << " + wv_ * " << TC << " + lane_ * " << VB << " + e] = m2_[e];\n    }\n  }\n";
+  s << "  __syncthreads();\n";
+  if (SPLIT > 1) s << "  float* part = (float*)a.p[" << scr_slot << "];\n";
+  s << "  for (int c = tid; c < " << TC << "; c += 256) {\n";
+  s << "    float n_ = red[c / " << VB << "], m_ = red[" << PL << " + c], q_ = red[2 * " << PL << " + c];\n";
+  s << "#pragma unroll\n    for (int w = 1; w < 4; ++w) {\n";
+  s << "      const float nb_ = red[w * " << BB << " + c / " << VB << "], nt_ = n_ + nb_;\n";
+  s << "      const float f_ = nt_ > 0.0f ? nb_ * __builtin_amdgcn_rcpf(nt_) : 0.0f;\n";
+  s << "      const float d_ = red[" << PL << " + w * " << TC << " + c] - m_;\n";
+  s << "      q_ = q_ + red[2 * " << PL << " + w * " << TC << " + c] + d_ * d_ * (n_ * f_);\n";
+  s << "      m_ = m_ + d_ * f_;\n      n_ = nt_;\n    }\n";
+  if (SPLIT > 1) {
+    const std::string PP = std::to_string(A * SPLIT * B);  // floats per partial plane
+    s << "    const i64 gc_ = (i64)blockIdx.x * " << TC << " + c;\n";
+    s << "    if (gc_ < " << B << "LL) {\n";
+    s << "      const i64 o_ = (ay * " << SPLIT << " + blockIdx.z) * " << B << "LL + gc_;\n";
+    s << "      coherent_store(&part[o_], m_);\n";
+    s << "      coherent_store(&part[" << PP << "LL + o_], q_);\n    }\n";
+  } else {
+    s << "    cm_[c] = m_;\n    cq_[c] = q_;\n";
+  }
+  s << "  }\n";
+  if (SPLIT > 1) {
+    const std::string PP = std::to_string(A * SPLIT * B);
+    s << "  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are performed\n";
+    s << "  __syncthreads();\n";
+    s << "  const i64 tix = ay * " << ctiles << " + blockIdx.x;\n";
+    s << "  if (tid == 0) {\n    int* cnt = (int*)a.p[" << cnt_slot << "];\n";
+    if (SPLIT > 32) {
+      const int64_t NG = (SPLIT + 15) / 16;
+      s << "    const int grp_ = blockIdx.z / 16, gsz_ = " << SPLIT << " - grp_ * 16 < 16 ? " << SPLIT << " - grp_ * 16 : 16;\n";
+      s << "    int* c1 = cnt + (tix * " << NG + 1 << " + 1 + grp_) * 32;\n";
+      s << "    int* c2 = cnt + tix * " << (NG + 1) * 32 << ";\n";
+      s << "    last_ = false;\n";
+      s << "    if (__hip_atomic_fetch_add(c1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gsz_ - 1) {\n";
+      s << "      __hip_atomic_store(c1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
+      s << "      last_ = __hip_atomic_fetch_add(c2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == " << NG - 1 << ";\n";
+      s << "      if (last_) __hip_atomic_store(c2, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n    }\n  }\n";
+    } else {
+      s << "    const int old = __hip_atomic_fetch_add(cnt + tix * 32, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n";
+      s << "    last_ = (old == " << SPLIT - 1 << ");\n";
+      s << "    if (last_) __hip_atomic_store(cnt + tix * 32, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
+    }
+    s << "  __syncthreads();\n  if (!last_) return;\n";
+    // each thread merges one group of splits (z = g, g + G, ...) of one column
+    // in split order; then one thread per column merges the groups in order
+    const int G = TC <= 256 ? 256 / TC : 1;
+    // batches of loads: two per split, within the 63 loads a wave may have in flight
+    const int64_t NZ = (SPLIT + G - 1) / G, NBT = std::min<int64_t>(NZ, 31);
+    const std::string GT = std::to_string(G * TC);
+    s << "  {\n    const i64 cb = (i64)blockIdx.x * " << TC << ";\n";
+    s << "    for (int c = tid % " << std::min(TC, 256) << "; c < " << TC << "; c += 256) {\n";
+    s << "      const int g = " << (G > 1 ? "tid / " + std::to_string(TC) : std::string("0")) << ";\n";
+    s << "      float tn_ = 0.0f, tm_ = 0.0f, tq_ = 0.0f;\n";
+    s << "      if (cb + c < " << B << "LL)\n        for (int z0 = g; z0 < " << SPLIT << "; z0 += " << NBT * G << ") {\n";
+    s << "          float vn_[" << NBT << "], vm_[" << NBT << "], vq_[" << NBT << "];\n";
+    s << "#pragma unroll\n          for (int j = 0; j < " << NBT << "; ++j) {\n";
+    s << "            const int z = z0 + j * " << G << ";\n";
+    s << "            const i64 o_ = (ay * " << SPLIT << " + z) * " << B << "LL + cb + c;\n";
+    // split z holds rows [z chunk, min((z + 1) chunk, L))
+    s << "            vn_[j] = z < " << SPLIT << " ? (float)(" << Lr << "LL - (i64)z * " << chunk << " < " << chunk << " ? " << Lr
+      << "LL - (i64)z * " << chunk << " : " << chunk << ") : 0.0f;\n";
+    s << "            vm_[j] = z < " << SPLIT << " ? coherent_load(&part[o_]) : 0.0f;\n";
+    s << "            vq_[j] = z < " << SPLIT << " ? coherent_load(&part[" << PP << "LL + o_]) : 0.0f;\n";
+    s << "          }\n";
+    // the batch's triples merge as a pairwise tree (j with j + h, h = 1, 2, 4,
+    // ...; a fixed order, log-depth dependency chains), then into the running one
+    for (int64_t h = 1; h < NBT; h *= 2)
+      for (int64_t j = 0; j + h < NBT; j += 2 * h) {
+        const std::string a_ = std::to_string(j), b_ = std::to_string(j + h);
+        s << "          {\n            const float nt_ = vn_[" << a_ << "] + vn_[" << b_ << "], f_ = nt_ > 0.0f ? vn_[" << b_
+          << "] * __builtin_amdgcn_rcpf(nt_) : 0.0f, d_ = vm_[" << b_ << "] - vm_[" << a_ << "];\n";
+        s << "            vq_[" << a_ << "] = vq_[" << a_ << "] + vq_[" << b_ << "] + d_ * d_ * (vn_[" << a_ << "] * f_);\n";
+        s << "            vm_[" << a_ << "] = vm_[" << a_ << "] + d_ * f_;\n            vn_[" << a_ << "] = nt_;\n          }\n";
+      }
+    s << "          {\n            const float nt_ = tn_ + vn_[0], f_ = nt_ > 0.0f ? vn_[0] * __builtin_amdgcn_rcpf(nt_) : 0.0f, d_ = vm_[0] - tm_;\n";
+    s << "            tq_ = tq_ + vq_[0] + d_ * d_ * (tn_ * f_);\n            tm_ = tm_ + d_ * f_;\n            tn_ = nt_;\n";
+    s << "          }\n        }\n";
+    s << "      red[g * " << TC << " + c] = tn_;\n";
+    s << "      red[" << GT << " + g * " << TC << " + c] = tm_;\n";
+    s << "      red[2 * " << GT << " + g * " << TC << " + c] = tq_;\n";
+    s << "    }\n  }\n  __syncthreads();\n";
+    s << "  for (int c = tid; c < " << TC << "; c += 256) {\n";
+    s << "    float n_ = red[c], m_ = red[" << GT << " + c], q_ = red[2 * " << GT << " + c];\n";
+    if (G > 1) {
+      s << "#pragma unroll\n    for (int g = 1; g < " << G << "; ++g) {\n";
+      s << "      const float nb_ = red[g * " << TC << " + c], nt_ = n_ + nb_, f_ = nt_ > 0.0f ? nb_ * __builtin_amdgcn_rcpf(nt_) : 0.0f;\n";
+      s << "      const float d_ = red[" << GT << " + g * " << TC << " + c] - m_;\n";
+      s << "      q_ = q_ + red[2 * " << GT << " + g * " << TC << " + c] + d_ * d_ * (n_ * f_);\n";
+      s << "      m_ = m_ + d_ * f_;\n      n_ = nt_;\n    }\n";
+    }
+    s << "    cm_[c] = m_;\n    cq_[c] = q_;\n  }\n";
+  }
+  s << "  __syncthreads();\n";
+  s << "  float s1_[" << VB << "], q1_[" << VB << "];\n";
+  s << "#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) s1_[e] = cm_[bl * " << VB << " + e], q1_[e] = cq_[bl * " << VB << " + e];\n";
+  s << "  if (ly == 0 && bv) {\n    float s2_[" << VB << "];\n";
+  s << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) s2_[e] = q1_[e] / " << flit((double)Lr) << ";\n";
+  s << "    const i64 l = 0; (void)l;\n" << ee.pre.str() << "#pragma unroll\n    for (int e = 0; e < " << VB
+    << "; ++e) {\n" << ee.body.str() << "    }\n  }\n}\n";
+  gk.source = s.str();
+  gk.grid[0] = (int)ctiles;
+  gk.grid[1] = (int)A;
+  gk.grid[2] = (int)SPLIT;
+  ki.fill_cost(gk);
+  return gk;
+}
+
 GenKernel gen_colreduce(const KInfo& ki, int index) {
   const Graph& g = ki.g;
   std::string why;
+  if (ki.linear.empty() && ki.reduces.size() == 2) {
+    Moments mo;
+    if (!detect_moments(ki, mo, &why)) fail(KORCH_E_UNSUPPORTED, why);
+    return gen_colmoments(ki, index, mo);
+  }
   if (!match_colreduce(ki, &why)) fail(KORCH_E_UNSUPPORTED, why);
   GenKernel gk;
   gk.family = KORCH_FAM_COLREDUCE;

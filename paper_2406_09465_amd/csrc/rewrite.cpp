@@ -385,6 +385,46 @@ std::vector<Subst> fold_scale(const Graph& g) {
   return out;
 }
 
+// Centred values D = X - m, with m the mean of X over a non-last axis, that
+// feed both a variance (mean of D^2 over the same axis) and other nodes: the
+// square reads m - X instead, a node of its own (the same magnitudes, since
+// rounding is symmetric, so the same squares).  D then no longer ties the
+// variance chain to its other readers, so one kernel can hold the mean and
+// the variance (one pass over X) and export m, from which a later kernel
+// recomputes D.  Rows (a last-axis mean) are left alone: one row kernel holds
+// the whole normalization.
+std::vector<Subst> split_moments(const Graph& g) {
+  std::vector<Subst> out;
+  for (const Node& q : g.nodes) {
+    int D = -1;
+    if (q.op == KORCH_SQUARE)
+      D = q.in[0];
+    else if (q.op == KORCH_MUL && !q.attrs.has_scalar && q.in.size() == 2 && q.in[0] == q.in[1])
+      D = q.in[0];
+    else
+      continue;
+    const Node& d = g.nodes[D];
+    if (d.op != KORCH_SUB || d.attrs.has_scalar || d.in.size() != 2) continue;
+    const Node& m = g.nodes[d.in[1]];
+    if (m.op != KORCH_REDUCE_MEAN || m.in[0] != d.in[0]) continue;
+    if (m.axis == (int)g.nodes[m.in[0]].shape.size() - 1) continue;
+    if (g.consumers[D].size() < 2) continue;
+    bool variance = false;
+    for (int c : g.consumers[q.id])
+      if (g.nodes[c].op == KORCH_REDUCE_MEAN && g.nodes[c].axis == m.axis) variance = true;
+    if (!variance) continue;
+    const int X = d.in[0], M = m.id, qop = q.op, ddt = d.dtype, qdt = q.dtype;
+    const korch_attrs da = d.attrs, qa = q.attrs;
+    Subst sub;
+    sub[q.id] = [=](Builder& b) {
+      int dc = b.add(KORCH_SUB, {b.get(M), b.get(X)}, da, ddt);
+      return qop == KORCH_SQUARE ? b.add(KORCH_SQUARE, {dc}, qa, qdt) : b.add(KORCH_MUL, {dc, dc}, qa, qdt);
+    };
+    out.push_back(sub);
+  }
+  return out;
+}
+
 // The layout-variant graph (see the header comment).  Eligible: a computed
 // tensor (not a graph input or output, not a layout node or constant) of rank
 // >= 2 whose last two axes both exceed 1 and that some product or convolution
@@ -443,6 +483,7 @@ Graph rewrite_graph(const Graph& g0, uint32_t rules, int* applied) {
   if (rules & KORCH_RW_REDUCE_AS_PRODUCT) active.push_back(reduce_as_product);
   if (rules & KORCH_RW_MERGE_PRODUCTS) active.push_back(merge_products);
   if (rules & KORCH_RW_FOLD_SCALE) active.push_back(fold_scale);
+  if (rules & KORCH_RW_SPLIT_MOMENTS) active.push_back(split_moments);
   for (int iter = 0; iter < 256; ++iter) {
     bool changed = false;
     for (Rule r : active) {

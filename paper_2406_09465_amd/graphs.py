@@ -295,6 +295,39 @@ def rewritten(w: Workload, rules=None):
     return Workload(w.name, w.dtype, g2, ids, list(w.input_names), list(w.output_names), sizes=dict(w.sizes)), n
 
 
+def moments_plan(w: Workload):
+    """Two kernels for an InstanceNorm whose graph went through the
+    split-moments transformation (its variance squares m - X, a node of its
+    own): the column moments {mean, m - X, square, variance, + eps, rsqrt}
+    exporting the mean and the reciprocal deviation (one pass over X), then
+    everything else (X - m recomputed, the normalization and what follows).
+    None when the graph has no such variance."""
+    g = w.graph
+    n = g.num_nodes()
+    op = {v: g.node_info(v)[0] for v in range(n)}
+    ins = {v: g.node_inputs(v) for v in range(n) if op[v] != "input"}
+    cons = {v: [c for c in ins if v in ins[c]] for v in range(n)}
+    for var in (v for v in range(n) if op[v] == "reduce_mean"):
+        sq = ins[var][0]
+        if op[sq] != "square" or op[ins[sq][0]] != "sub":
+            continue
+        dc = ins[sq][0]
+        mu, x = ins[dc]
+        if op[mu] != "reduce_mean" or ins[mu][0] != x:
+            continue
+        k0 = {mu, dc, sq, var}
+        if op[x] == "reshape":
+            k0.add(x)
+        last = var
+        while len(cons[last]) == 1 and op[cons[last][0]] in ("add", "rsqrt") and g.node_info(cons[last][0])[2] == g.node_info(var)[2]:
+            last = cons[last][0]
+            k0.add(last)
+        prims = [v for v in range(n) if op[v] != "input"]
+        return [(sorted(k0), sorted([mu, last])),
+                (sorted(v for v in prims if v not in k0), sorted(o for o in g.outputs() if o not in k0))]
+    return None
+
+
 def plan_record(w: Workload, kernels, rules=0):
     """JSON-able record of a plan of ``w`` (or of its rewritten graph when
     ``rules`` is non-zero): node ids, plus names where the workload names them."""

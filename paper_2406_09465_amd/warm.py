@@ -85,6 +85,14 @@ LN_FOLD_PLANS = {
                 (["Zo", "out"], ["out"])],
 }
 
+# InstanceNorm shapes of the column-moments GPU tests (the split-moments
+# transformation, then the two-kernel plan graphs.moments_plan builds): the
+# full size (196 splits of the reduced axis, two-level arrival), 1600 rows (3
+# splits), and one workgroup with ragged channels (24) or fewer rows than a
+# workgroup has row lanes (15).  Each also with the mean and the reciprocal
+# deviation as extra outputs.
+MOMENTS_CASES = [{}, dict(hh=40, ww=40, c=16), dict(hh=13, ww=11, c=24), dict(hh=3, ww=5, c=8)]
+
 # Attention shapes of the attention-kernel GPU tests (few query rows: the keys
 # are split over the waves; fp32 and fp16, padded keys), each run with the key
 # split and without it (KORCH_ATTN_NO_KEY_SPLIT=1).
@@ -172,6 +180,8 @@ def _jobs():
         jobs.append(("env_plans", "mlp", sz, (("KORCH_GEMM_NO_KSPLIT", "1"), ("KORCH_GEMM_DMA", "0"))))
     for sz in LN_FOLD_CASES:
         jobs.append(("ln_fold", "mlp", sz, None))
+    for sz in MOMENTS_CASES:
+        jobs.append(("moments", "instnorm", sz, None))
     jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_2STAGE", "1")))
     jobs.append(("env_plans", "mlp", {}, (("KORCH_GEMM_NO_KSPLIT", "1"), ("KORCH_GEMM_DMA_2STAGE", "1"))))
     jobs.append(("env_plans", "mlp", {}, ("KORCH_GEMM_DMA_KSPLIT", "1")))
@@ -209,6 +219,14 @@ def _run_job(job, part=0, parts=1):
             wl.plan("unfused").compile()
         except KorchError as e:
             failures.append((w, sz, f"{kind} {extra}", str(e)[:200]))
+        return failures
+    if kind == "moments":
+        for extra in ((), ("mu", "r")):
+            w2, _ = graphs.rewritten(graphs.build(w, extra_outputs=extra, **sz))
+            try:
+                graphs.Plan(w2.graph, graphs.moments_plan(w2)).compile()
+            except KorchError as e:
+                failures.append((w, sz, f"moments {extra}", str(e)[:200]))
         return failures
     wl = graphs.build(w, **sz)
     if kind == "ln_fold":

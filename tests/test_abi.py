@@ -336,6 +336,48 @@ def test_timed_execute_rejects_a_kernel_outside_the_range():
     assert code(lambda: p.execute_timed(1, 1, [0] * 6, [0], 0, 0, 0, 0, 0, 0)) == -1
 
 
+def test_column_moments_kernel():
+    """After the split-moments transformation InstanceNorm's mean, centred
+    squares and variance (with + eps and rsqrt) form one column-reduction
+    kernel that reads X once (Welford per thread, Chan's merge, three fp32
+    partial planes per split) and exports the mean and the reciprocal
+    deviation; the normalization recomputes X - m from them.  The chooser's
+    candidates include it.  Kernels that would have to export the centred
+    values, or whose square is not of X minus its mean, are not moments
+    kernels."""
+    import re
+    w2, n = graphs.rewritten(graphs.build("instnorm"))
+    assert n >= 1
+    ks = graphs.moments_plan(w2)
+    assert ks is not None and len(ks) == 2
+    p = graphs.Plan(w2.graph, ks)
+    p.compile()
+    assert p.kernel_info(0)[0] == "colreduce" and p.kernel_info(1)[0] == "pointwise"
+    src = p.kernel_source(0)
+    assert "cn_ += 1.0f" in src and src.count("ldv<8>(") == 1  # one vector load of X per row
+    assert "coherent_store(&part[6272LL + o_], q_);" in src  # 196 splits x 32 channels per plane
+    body = src[src.index('extern "C"'):]
+    assert len(re.findall(r"st1_out\(", body)) == 2  # the mean and rsqrt(var + eps) only
+    g = w2.graph
+    cands = {(tuple(a), tuple(b)) for a, b in g.candidates(max_prims=64, max_outs=3, only_supported=True)}
+    assert (tuple(ks[0][0]), tuple(ks[0][1])) in cands
+    # the centred values as an output: not a moments kernel
+    ops = {v: g.node_info(v)[0] for v in range(g.num_nodes())}
+    sq = next(v for v in ops if ops[v] == "square")
+    dc = g.node_inputs(sq)[0]
+    assert g.family(sorted(ks[0][0]), sorted(ks[0][1] + [dc])) == "none"
+    # in the original graph the same kernel computes the variance, but the mean
+    # has no reader outside it (X - m is inside), so it cannot be an output
+    # (Definition 3) and the normalization could not recompute X - m
+    w = graphs.build("instnorm")
+    ids = w.ids
+    assert w.graph.family([ids[k] for k in ("mu", "D", "D2", "var")], [ids["var"]]) == "colreduce"
+    with pytest.raises(K.KorchError):
+        graphs.Plan(w.graph, [([ids[k] for k in ("mu", "D", "D2", "var")], [ids["mu"], ids["var"]])] +
+                    [(sorted(set(range(w.graph.num_nodes())) - set(w.graph.inputs()) -
+                             {ids[k] for k in ("mu", "D2", "var")}), [ids["out"]])])
+
+
 def test_gemm_k_split_selection(monkeypatch):
     """GEMM2 of the MLP block (256 tiles, 48 k-tiles) and of the odd-k test shape
     use the intra-workgroup split of K; GEMM1 (256 x 192 tiles of eight waves)

@@ -23,7 +23,8 @@ SMALL = {
     "instnorm": dict(hh=6, ww=5, c=8),
 }
 RULESETS = [K.RW_DEFER_DIV, K.RW_REDUCE_AS_PRODUCT, K.RW_MERGE_PRODUCTS,
-            K.RW_REDUCE_AS_PRODUCT | K.RW_MERGE_PRODUCTS, K.RW_FOLD_SCALE, K.RW_ALL, K.RW_LAYOUT_VARIANTS,
+            K.RW_REDUCE_AS_PRODUCT | K.RW_MERGE_PRODUCTS, K.RW_FOLD_SCALE, K.RW_SPLIT_MOMENTS, K.RW_ALL,
+            K.RW_LAYOUT_VARIANTS,
             K.RW_ALL | K.RW_LAYOUT_VARIANTS]
 
 
@@ -121,6 +122,29 @@ def test_attention_normalizes_after_the_product():
     assert g2.node_info(g2.node_inputs(out)[0])[0] == "matmul"
     g3, _ = w.graph.rewrite(K.RW_ALL)
     assert "reduce_sum" not in kinds(g3) and kinds(g3).count("matmul") == 2
+
+
+def test_instnorm_variance_squares_its_own_copy():
+    """Split moments: InstanceNorm's centred values X - m (m the mean over the
+    pixels, a non-last axis) feed the variance and the normalization; the
+    variance's square then reads m - X, a node of its own, while X - m keeps
+    the normalization.  LayerNorm rows (a last-axis mean) are left alone."""
+    w = graphs.build("instnorm", **SMALL["instnorm"])
+    g2, n = w.graph.rewrite(K.RW_SPLIT_MOMENTS)
+    assert n == 1
+    ops = kinds(g2)
+    assert ops.count("sub") == 2 and ops.count("reduce_mean") == 2
+    sq = next(v for v in range(g2.num_nodes()) if ops[v] == "square")
+    dc = g2.node_inputs(sq)[0]
+    mu, x = g2.node_inputs(dc)
+    assert ops[dc] == "sub" and ops[mu] == "reduce_mean" and g2.node_inputs(mu) == [x]
+    d = next(v for v in range(g2.num_nodes()) if ops[v] == "sub" and v != dc)
+    assert g2.node_inputs(d) == [x, mu]
+    readers = [v for v in range(g2.num_nodes()) if ops[v] != "input" and d in g2.node_inputs(v)]
+    assert len(readers) == 1 and ops[readers[0]] == "mul"
+    for wl in ("mlp", "sra"):
+        _, n = graphs.build(wl, **SMALL[wl]).graph.rewrite(K.RW_SPLIT_MOMENTS)
+        assert n == 0, wl
 
 
 def test_merge_refuses_a_cycle():
