@@ -392,7 +392,8 @@ std::vector<Subst> fold_scale(const Graph& g) {
 // variance chain to its other readers, so one kernel can hold the mean and
 // the variance (one pass over X) and export m, from which a later kernel
 // recomputes D.  Rows (a last-axis mean) are left alone: one row kernel holds
-// the whole normalization.
+// the whole normalization (with its rows split too, the MLP block's cheapest
+// plan was predicted at 58.63 us against 58.59 for the unsplit graph's).
 std::vector<Subst> split_moments(const Graph& g) {
   std::vector<Subst> out;
   for (const Node& q : g.nodes) {
