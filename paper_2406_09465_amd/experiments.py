@@ -45,13 +45,15 @@ LIMITS = dict(max_prims=64, max_outs=3)
 def _compile_share(args):
     workload, sizes, part, parts = args
     w = graphs.build(workload, **sizes)
-    cands = w.graph.candidates(only_supported=True, **LIMITS)
+    w2, napp = graphs.rewritten(w)
     bad = 0
-    for c in cands[part::parts]:
-        try:
-            w.graph.compile_candidate(*c)
-        except Exception:
-            bad += 1
+    for g in ([w.graph, w2.graph] if napp else [w.graph]):  # the transformed graph too, where a rule applies
+        cands = g.candidates(only_supported=True, **LIMITS)
+        for c in cands[part::parts]:
+            try:
+                g.compile_candidate(*c)
+            except Exception:
+                bad += 1
     return bad
 
 
@@ -83,8 +85,11 @@ def shapes(workload, out, warmup=10, reps=100):
              f"Candidates compiled in {time.time() - t0:.0f} s. Costs are medians of {reps} launches after "
              f"{warmup} warm-up launches, each timed by its own dispatch after a read of 512 MiB (cold caches) and "
              "a read of its computed inputs (cache-resident, as a producing kernel leaves them).", "",
-             "| sizes | candidates | chosen kernels | chosen cost (us) | fewest kernels | their cost (us) | chosen plan |",
-             "|---|---|---|---|---|---|---|"]
+             "The last column is the cheapest plan of the graph after the primitive-graph transformations "
+             "(`korch_graph_rewrite`, all rules), where any applies; the chooser of the bench keeps the cheaper graph.", "",
+             "| sizes | candidates | chosen kernels | chosen cost (us) | fewest kernels | their cost (us) | chosen plan | "
+             "transformed graph: cost (us), kernels |",
+             "|---|---|---|---|---|---|---|---|"]
     for sz in SWEEPS[workload]:
         w = graphs.build(workload, **sz)
         cands = w.graph.candidates(only_supported=True, **LIMITS)
@@ -94,8 +99,13 @@ def shapes(workload, out, warmup=10, reps=100):
         nf, cf_ = fewest_kernels(view, cands, costs)
         names = {v: k for k, v in w.ids.items()}
         plan = " ; ".join("{" + ",".join(names[v] for v in o) + "}" for _, o in ch.kernels)
+        w2, napp = graphs.rewritten(w)
+        rw = "none applies"
+        if napp:
+            ch2 = chooser.korch_plan(w2.graph, **LIMITS, warmup=warmup, reps=reps)
+            rw = f"{ch2.cost_us:.2f}, {len(ch2.kernels)}"
         lines.append(f"| {sz} | {sum(c is not None for c in costs)} | {len(ch.kernels)} | {ch.cost_us:.2f} | {nf} | "
-                     f"{cf_:.2f} | {plan} |")
+                     f"{cf_:.2f} | {plan} | {rw} |")
         print(lines[-1], flush=True)
     open(out, "w").write("\n".join(lines) + "\n")
 
