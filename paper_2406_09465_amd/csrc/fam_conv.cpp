@@ -203,7 +203,12 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   const int NV = d.NP / 8;
   const int WV = d.taps * d.CP * NV;
   const int WPT = (WV + 255) / 256;
-  s << "  fetch_halo(t);\n";
+  // When every slot holds a weight vector the loads are unconditional: a
+  // guarded load makes the compiler wait for all loads in flight at the join.
+  const bool wall = WV % 256 == 0 && Cin == d.CP && N == d.NP;
+  const std::string wguard = wall ? std::string("true")
+                                  : "v < " + std::to_string(WV) + " && c < " + std::to_string(Cin) + " && nv * 8 < " +
+                                        std::to_string(N);
   s << "  {\n    uint4 wv[" << WPT << "];\n";
   s << "#pragma unroll\n    for (int i = 0; i < " << WPT << "; ++i) {\n";
   s << "      const int v = tid + i * 256;\n";
@@ -211,8 +216,8 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
     << ";\n";
   s << "      wv[i] = uint4{0u, 0u, 0u, 0u};\n";
   if (sp.pro.empty()) {
-    s << "      if (v < " << WV << " && c < " << Cin << " && nv * 8 < " << N << ") wv[i] = *(const uint4*)(" << Wt
-      << " + ((i64)tap * " << Cin << " + c) * " << N << " + nv * 8);\n";
+    s << "      if (" << wguard << ") wv[i] = *(const uint4*)(" << Wt << " + ((i64)tap * " << Cin << " + c) * " << N
+      << " + nv * 8);\n";
   } else {
     // the weights are computed by the kernel's prologue (e.g. scaled per
     // output channel): evaluated here, once per workgroup, 8 channels at a time
@@ -222,7 +227,7 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
     em.vec = 8;
     std::vector<Ix> idx = {Ix::var("ky_"), Ix::var("kx_"), Ix::var("c"), Ix::var("n_", 1, 8)};
     std::string val = em.value(sp.Bs[0], idx);
-    s << "      if (v < " << WV << " && c < " << Cin << " && nv * 8 < " << N << ") {\n";
+    s << "      if (" << wguard << ") {\n";
     s << "        const int ky_ = tap / " << sp.KW << ", kx_ = tap % " << sp.KW << ";\n";
     s << "        const i64 n_ = (i64)nv * 8;\n";
     s << "        (void)ky_; (void)kx_; (void)n_;\n";
@@ -233,9 +238,12 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
     s << "        wv[i] = __builtin_bit_cast(uint4, w_);\n      }\n";
   }
   s << "    }\n";
+  // the first halo's loads go out behind the weights' (the weights are waited
+  // for first, and loads complete in order)
+  s << "    fetch_halo(t);\n";
   s << "#pragma unroll\n    for (int i = 0; i < " << WPT << "; ++i) {\n";
   s << "      const int v = tid + i * 256;\n";
-  s << "      if (v < " << WV << ") *(uint4*)(Ws + (v / " << NV << ") * " << d.WP << " + (v % " << NV << ") * 8) = wv[i];\n";
+  s << "      if (" << (wall ? std::string("true") : "v < " + std::to_string(WV)) << ") *(uint4*)(Ws + (v / " << NV << ") * " << d.WP << " + (v % " << NV << ") * 8) = wv[i];\n";
   s << "    }\n  }\n";
   s << "  __syncthreads();\n";
   s << "  " << V8 << " bfr[" << d.taps << "][" << d.CC << "][" << d.FN << "];\n";
