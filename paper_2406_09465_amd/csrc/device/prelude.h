@@ -127,6 +127,19 @@ __device__ __forceinline__ void st16_out(void* base, i64 boff, uint4 v) {
   const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4o_, v), r, (unsigned)boff, 0, 16);
 }
+// ---- loads that read zero where a condition fails, without a branch ------
+// A guarded load (`if (ok) x = *p;`) becomes a branch around the load, and the
+// compiler waits for every load in flight where the branches join.  A buffer
+// load whose offset is out of range returns zero instead, so these loads are
+// issued back to back.  `boff` is a byte offset from `base` (tensors below 2 GiB).
+__device__ __forceinline__ uint4 ld16_or_zero(const void* base, i64 boff, bool ok) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, 0x00020000);
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (unsigned)boff : 0x80000000u, 0, 0));
+}
+__device__ __forceinline__ float ld4f_or_zero(const float* base, i64 eoff, bool ok) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, 0x7fffffff, 0x00020000);
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, ok ? (unsigned)(eoff * 4) : 0x80000000u, 0, 0));
+}
 template <typename T> __device__ __forceinline__ void st1_out(T* base, i64 off, float v) {
   stv_out<1, T>(base, off, &v);
 }

@@ -235,18 +235,34 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   // LDS write (one round trip to memory); the query fragments of the
   // half-precision paths are loaded before them as well.
   const int VL = 16 / dtype_bytes(a.dtype);
+  // branch-free (buffer) loads need byte offsets below 2 GiB
+  const bool small = (double)a.batch * std::max(a.nq * a.d, a.nk * std::max(a.d, a.dv)) * dtype_bytes(a.dtype) < 2147483648.0;
   const std::string VT = "vec_t<" + std::to_string(VL) + ", " + T + ">";
   const std::string V8 = a.dtype == KORCH_F16 ? "f16x8" : "bf16x8";
   const int64_t QF = f32 ? 0 : dpad / 32;  // query fragments per lane
+  const bool qpre = f32 && small;  // fp32 query values loaded up front
+  if (qpre) {
+    s << "  const i64 qr_ = " << (ksplit ? "(i64)blockIdx.x * 16" : "(i64)blockIdx.x * 64 + wave * 16") << " + (l & 15);\n";
+    s << "  float qf_[" << dpad / 4 << "];\n";
+    s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 4 << "; ++kk) {\n";
+    s << "    const int dim = kk * 4 + (l >> 4);\n";
+    s << "    qf_[kk] = ld4f_or_zero(" << Q << ", qoff + qr_ * " << a.d << " + dim, qr_ < " << a.nq << "LL && dim < " << a.d
+      << ");\n  }\n";
+  }
   if (!f32) {
     s << "  const i64 qr_ = " << (ksplit ? "(i64)blockIdx.x * 16" : "(i64)blockIdx.x * 64 + wave * 16") << " + (l & 15);\n";
     s << "  " << V8 << " qa_[" << QF << "];\n";
     s << "#pragma unroll\n  for (int kk = 0; kk < " << QF << "; ++kk) {\n";
     s << "    const int dim = kk * 32 + (l >> 4) * 8;\n";
-    s << "    if (qr_ < " << a.nq << "LL && dim + 8 <= " << a.d << ") qa_[kk] = *(const " << V8 << "*)(" << Q << " + qoff + qr_ * "
-      << a.d << " + dim);\n";
-    s << "    else {\n#pragma unroll\n      for (int j = 0; j < 8; ++j) qa_[kk][j] = (qr_ < " << a.nq << "LL && dim + j < " << a.d
-      << ") ? " << Q << "[qoff + qr_ * " << a.d << " + dim + j] : fromf<" << T << ">(0.0f);\n    }\n  }\n";
+    if (small && dpad == a.d) {
+      s << "    qa_[kk] = __builtin_bit_cast(" << V8 << ", ld16_or_zero(" << Q << ", (qoff + qr_ * " << a.d << " + dim) * 2, qr_ < "
+        << a.nq << "LL));\n  }\n";
+    } else {
+      s << "    if (qr_ < " << a.nq << "LL && dim + 8 <= " << a.d << ") qa_[kk] = *(const " << V8 << "*)(" << Q << " + qoff + qr_ * "
+        << a.d << " + dim);\n";
+      s << "    else {\n#pragma unroll\n      for (int j = 0; j < 8; ++j) qa_[kk][j] = (qr_ < " << a.nq << "LL && dim + j < " << a.d
+        << ") ? " << Q << "[qoff + qr_ * " << a.d << " + dim + j] : fromf<" << T << ">(0.0f);\n    }\n  }\n";
+    }
   }
   const bool vecK = !a.k_is_kt && a.d % VL == 0 && dpad % VL == 0;
   const bool vecV = a.dv % VL == 0 && dvp % VL == 0;
@@ -255,20 +271,32 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     s << "  " << VT << " kx_[" << NIK << "], vx_[" << std::max<int64_t>(NIV, 1) << "];\n";
     s << "#pragma unroll\n  for (int j = 0; j < " << NIK << "; ++j) {\n";
     s << "    const int i = tid + j * 256, key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
-    s << "    kx_[j] = " << VT << "{};\n";
-    s << "    if (i < " << nkp * dpad / VL << " && dim < " << a.d << " && key < " << a.nk << ") kx_[j] = *(const " << VT << "*)(" << K
-      << " + koff + (i64)key * " << a.d << " + dim);\n  }\n";
+    if (small) {
+      s << "    kx_[j] = __builtin_bit_cast(" << VT << ", ld16_or_zero(" << K << ", (koff + (i64)key * " << a.d << " + dim) * "
+        << dtype_bytes(a.dtype) << ", i < " << nkp * dpad / VL << " && dim < " << a.d << " && key < " << a.nk << "));\n  }\n";
+    } else {
+      s << "    kx_[j] = " << VT << "{};\n";
+      s << "    if (i < " << nkp * dpad / VL << " && dim < " << a.d << " && key < " << a.nk << ") kx_[j] = *(const " << VT << "*)("
+        << K << " + koff + (i64)key * " << a.d << " + dim);\n  }\n";
+    }
     s << "#pragma unroll\n  for (int j = 0; j < " << NIV << "; ++j) {\n";
     s << "    const int i = tid + j * 256, key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
-    s << "    vx_[j] = " << VT << "{};\n";
-    s << "    if (i < " << nkp * dvp / VL << " && key < " << a.nk << " && dim < " << a.dv << ") vx_[j] = *(const " << VT << "*)(" << V
-      << " + voff + (i64)key * " << a.dv << " + dim);\n  }\n";
+    if (small) {
+      s << "    vx_[j] = __builtin_bit_cast(" << VT << ", ld16_or_zero(" << V << ", (voff + (i64)key * " << a.dv << " + dim) * "
+        << dtype_bytes(a.dtype) << ", i < " << nkp * dvp / VL << " && key < " << a.nk << " && dim < " << a.dv << "));\n  }\n";
+    } else {
+      s << "    vx_[j] = " << VT << "{};\n";
+      s << "    if (i < " << nkp * dvp / VL << " && key < " << a.nk << " && dim < " << a.dv << ") vx_[j] = *(const " << VT << "*)("
+        << V << " + voff + (i64)key * " << a.dv << " + dim);\n  }\n";
+    }
     s << "#pragma unroll\n  for (int j = 0; j < " << NIK << "; ++j) {\n";
     s << "    const int i = tid + j * 256, key = i / " << dpad / VL << ", dim = (i % " << dpad / VL << ") * " << VL << ";\n";
-    s << "    if (i < " << nkp * dpad / VL << ") *(" << VT << "*)(Ks + key * " << KSP << " + dim) = kx_[j];\n  }\n";
+    s << "    if (" << ((nkp * dpad / VL) % 256 == 0 ? std::string("true") : "i < " + std::to_string(nkp * dpad / VL)) << ") *(" << VT
+      << "*)(Ks + key * " << KSP << " + dim) = kx_[j];\n  }\n";
     s << "#pragma unroll\n  for (int j = 0; j < " << NIV << "; ++j) {\n";
     s << "    const int i = tid + j * 256, key = i / " << dvp / VL << ", dim = (i % " << dvp / VL << ") * " << VL << ";\n";
-    s << "    if (i < " << nkp * dvp / VL << ") *(" << VT << "*)(Vs + key * " << VP << " + dim) = vx_[j];\n  }\n";
+    s << "    if (" << ((nkp * dvp / VL) % 256 == 0 ? std::string("true") : "i < " + std::to_string(nkp * dvp / VL)) << ") *(" << VT
+      << "*)(Vs + key * " << VP << " + dim) = vx_[j];\n  }\n";
   } else {
     if (vecK) {
       s << "#pragma unroll 4\n  for (int i = tid; i < " << nkp * dpad / VL << "; i += 256) {\n";
@@ -347,7 +375,10 @@ GenKernel gen_attention(const KInfo& ki, int index) {
     if (f32) {
       s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 4 << "; ++kk) {\n";
       s << "    const int dim = kk * 4 + (l >> 4);\n";
-      s << "    const float qa = (qv && dim < " << a.d << ") ? " << Q << "[qoff + qr * " << a.d << " + dim] : 0.0f;\n";
+      if (qpre)
+        s << "    const float qa = qf_[kk];\n";
+      else
+        s << "    const float qa = (qv && dim < " << a.d << ") ? " << Q << "[qoff + qr * " << a.d << " + dim] : 0.0f;\n";
       s << "#pragma unroll\n    for (int f = 0; f < " << NFW << "; ++f) sc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, Ks[(kb + f * 16 + (l & 15)) * "
         << KSP << " + dim], sc[f], 0, 0, 0);\n  }\n";
     } else {
@@ -427,7 +458,10 @@ GenKernel gen_attention(const KInfo& ki, int index) {
   if (f32) {
     s << "#pragma unroll\n  for (int kk = 0; kk < " << dpad / 4 << "; ++kk) {\n";
     s << "    const int dim = kk * 4 + (l >> 4);\n";
-    s << "    const float qa = (qv && dim < " << a.d << ") ? " << Q << "[qoff + qr * " << a.d << " + dim] : 0.0f;\n";
+    if (qpre)
+      s << "    const float qa = qf_[kk];\n";
+    else
+      s << "    const float qa = (qv && dim < " << a.d << ") ? " << Q << "[qoff + qr * " << a.d << " + dim] : 0.0f;\n";
     s << "#pragma unroll\n    for (int f = 0; f < " << NF << "; ++f) sc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, Ks[(f * 16 + (l & 15)) * "
       << KSP << " + dim], sc[f], 0, 0, 0);\n  }\n";
   } else {
