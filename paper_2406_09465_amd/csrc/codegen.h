@@ -101,6 +101,8 @@ struct Emitter {
   std::ostringstream body;             // statements inside the lane loop
   std::function<bool(int, const std::vector<Ix>&, std::string*)> provide;
   bool force_gather = false;           // all loads per-lane (guarded contexts)
+  std::string gather_guard;            // when set, gathers read zero where it is false, without a branch
+  int n_guard_fallback = 0;            // gathers of tensors too large for that form
   int tmp = 0;
   int guard_depth = 0;                 // enclosing guards whose condition varies with the vector lane
   // Enclosing guards whose condition is the same for every lane of a vector

@@ -386,6 +386,12 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
     std::string v = fresh("x");
     if (gcond.empty())
       pre << "  float " << v << "[" << vec << "]; ldv<" << vec << ">(" << v << ", " << P << " + " << off.b << ");\n";
+    else if ((vec * dtype_bytes(n.dtype) == 4 || vec * dtype_bytes(n.dtype) == 8 || vec * dtype_bytes(n.dtype) == 16) &&
+             (double)numel(n.shape) * dtype_bytes(n.dtype) < 2147483648.0)
+      // a branch-free load: a guarded one makes the compiler wait for every
+      // load in flight where the branches join
+      pre << "  float " << v << "[" << vec << "]; ldv_or_zero<" << vec << ">(" << v << ", " << P << ", " << off.b << ", " << gcond
+          << ");\n";
     else
       pre << "  float " << v << "[" << vec << "] = {}; if (" << gcond << ") ldv<" << vec << ">(" << v << ", " << P << " + "
           << off.b << ");\n";
@@ -393,6 +399,13 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
   }
   ++n_gather;
   std::string v = fresh("g");
+  if (!gather_guard.empty()) {
+    if ((double)numel(n.shape) * dtype_bytes(n.dtype) < 2147483648.0) {
+      body << "    const float " << v << " = ld1_or_zero(" << P << ", " << off.at() << ", " << gather_guard << ");\n";
+      return v;
+    }
+    ++n_guard_fallback;
+  }
   body << "    const float " << v << " = ld1(" << P << " + " << off.at() << ");\n";
   return v;
 }

@@ -140,6 +140,39 @@ __device__ __forceinline__ float ld4f_or_zero(const float* base, i64 eoff, bool 
   const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, 0x7fffffff, 0x00020000);
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, ok ? (unsigned)(eoff * 4) : 0x80000000u, 0, 0));
 }
+// V consecutive elements at element offset `off` of `base` into fp32
+// registers, zeros where `ok` is false, without a branch (V * sizeof(T) of 4,
+// 8 or 16 bytes; tensors below 2 GiB).
+template <int V, typename T>
+__device__ __forceinline__ void ldv_or_zero(float* d, const T* base, i64 off, bool ok) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), 0, 0x7fffffff, 0x00020000);
+  const unsigned o = ok ? (unsigned)(off * (i64)sizeof(T)) : 0x80000000u;
+  typedef typename VecOf<V, T>::type VT;
+  constexpr int B = V * (int)sizeof(T);
+  static_assert(V > 1 && (B == 4 || B == 8 || B == 16), "ldv_or_zero: 4, 8 or 16 bytes of two or more elements");
+  VT v;
+  if constexpr (B == 16) {
+    v = __builtin_bit_cast(VT, __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, 0));
+  } else if constexpr (B == 8) {
+    v = __builtin_bit_cast(VT, __builtin_amdgcn_raw_buffer_load_b64(r, o, 0, 0));
+  } else {
+    v = __builtin_bit_cast(VT, __builtin_amdgcn_raw_buffer_load_b32(r, o, 0, 0));
+  }
+#pragma unroll
+  for (int i = 0; i < V; ++i) d[i] = tof(v[i]);
+}
+// One element at element offset `off` of `base` as fp32, zero where `ok` is
+// false, without a branch (tensors below 2 GiB).
+template <typename T> __device__ __forceinline__ float ld1_or_zero(const T* base, i64 off, bool ok) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), 0, 0x7fffffff, 0x00020000);
+  const unsigned o = ok ? (unsigned)(off * (i64)sizeof(T)) : 0x80000000u;
+  if constexpr (sizeof(T) == 4) {
+    return tof(__builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, o, 0, 0)));
+  } else {
+    static_assert(sizeof(T) == 2, "ld1_or_zero: 2- or 4-byte elements");
+    return tof(__builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b16(r, o, 0, 0)));
+  }
+}
 template <typename T> __device__ __forceinline__ void st1_out(T* base, i64 off, float v) {
   stv_out<1, T>(base, off, &v);
 }

@@ -748,9 +748,24 @@ std::string operand_loader(const KInfo& ki, const GemmSpec& sp, bool isA, const 
     } else {
       std::string cond = axis_k ? "(" + rowv + " < " + rowlim + " && " + kv + " + e < " + std::to_string(sp.K) + ")"
                                 : "(" + rowv + " + e < " + rowlim + " && " + kv + " < " + std::to_string(sp.K) + ")";
-      o << "#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) {\n        dst[e] = 0.0f;\n        if "
-        << cond << " {\n"
-        << em.pre.str() << em.body.str() << "        dst[e] = " << val << ";\n        }\n      }\n";
+      // gathers that read zero out of range are issued without a branch (a
+      // guarded load waits for every load in flight at the join); the value
+      // is selected afterwards, as the prologue of a zero need not be zero
+      Emitter eg(g);
+      eg.inset = sp.pro;
+      eg.argslot = slot;
+      eg.vec = V;
+      eg.force_gather = true;
+      eg.gather_guard = "ok_";
+      std::string gval = eg.value(node, idx);
+      if (eg.n_guard_fallback == 0) {
+        o << "#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) {\n        const bool ok_ = " << cond << ";\n"
+          << eg.pre.str() << eg.body.str() << "        dst[e] = ok_ ? (" << gval << ") : 0.0f;\n      }\n";
+      } else {
+        o << "#pragma unroll\n      for (int e = 0; e < " << V << "; ++e) {\n        dst[e] = 0.0f;\n        if "
+          << cond << " {\n"
+          << em.pre.str() << em.body.str() << "        dst[e] = " << val << ";\n        }\n      }\n";
+      }
     }
     return o.str();
   };
