@@ -66,6 +66,21 @@ void KInfo::fill_cost(GenKernel& gk) const {
 
 static thread_local std::string g_kernel_prefix = "korch_k";
 void set_kernel_prefix(const std::string& prefix) { g_kernel_prefix = prefix; }
+// Header of a thread's loop over the reduced axis of a column reduction (rows
+// l0 + ly, + LY, ... below l1).  When every split holds `chunk` rows and a
+// thread's share is a few rows, the loop has a fixed trip count and is
+// unrolled, so all of its loads are issued before the first is used; the
+// compiler splits a runtime-bounded loop into a first load, a wait, and the rest.
+static std::string row_loop(int64_t chunk, int64_t Lr, int64_t LY) {
+  std::ostringstream o;
+  if (Lr % chunk == 0 && chunk % LY == 0 && chunk / LY <= 8)
+    o << "#pragma unroll\n  for (int it_ = 0; it_ < " << chunk / LY << "; ++it_) {\n    const i64 l = l0 + ly + (i64)it_ * " << LY
+      << ";\n";
+  else
+    o << "#pragma unroll 4\n  for (i64 l = l0 + ly; l < l1; l += " << LY << ") {\n";
+  return o.str();
+}
+
 std::string kernel_name(int index, const char* fam) { return g_kernel_prefix + std::to_string(index) + "_" + fam; }
 
 static int64_t pow2ceil(int64_t x) {
@@ -690,7 +705,7 @@ static GenKernel gen_colmoments(const KInfo& ki, int index, const Moments& mo) {
   // Welford over this thread's rows (one count for its VB columns)
   s << "  float cn_ = 0.0f, mu_[" << VB << "], m2_[" << VB << "];\n";
   s << "#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) mu_[e] = 0.0f, m2_[e] = 0.0f;\n";
-  s << "#pragma unroll 4\n  for (i64 l = l0 + ly; l < l1; l += " << LY << ") {\n" << pe.pre.str();
+  s << row_loop(chunk, Lr, LY) << pe.pre.str();
   s << "    cn_ += 1.0f;\n    const float inv_ = __builtin_amdgcn_rcpf(cn_);\n";
   s << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n" << pe.body.str();
   s << "      const float x_ = " << xv << ";\n";
@@ -778,12 +793,17 @@ static GenKernel gen_colmoments(const KInfo& ki, int index, const Moments& mo) {
     s << "          float vn_[" << NBT << "], vm_[" << NBT << "], vq_[" << NBT << "];\n";
     s << "#pragma unroll\n          for (int j = 0; j < " << NBT << "; ++j) {\n";
     s << "            const int z = z0 + j * " << G << ";\n";
-    s << "            const i64 o_ = (ay * " << SPLIT << " + z) * " << B << "LL + cb + c;\n";
+    // the address is clamped to a split that exists and the value selected
+    // afterwards: a guarded (atomic) load is a branch, and each join waits
+    // for every load in flight
+    s << "            const i64 o_ = (ay * " << SPLIT << " + (z < " << SPLIT << " ? z : " << SPLIT - 1 << ")) * " << B
+      << "LL + cb + c;\n";
     // split z holds rows [z chunk, min((z + 1) chunk, L))
     s << "            vn_[j] = z < " << SPLIT << " ? (float)(" << Lr << "LL - (i64)z * " << chunk << " < " << chunk << " ? " << Lr
       << "LL - (i64)z * " << chunk << " : " << chunk << ") : 0.0f;\n";
-    s << "            vm_[j] = z < " << SPLIT << " ? coherent_load(&part[o_]) : 0.0f;\n";
-    s << "            vq_[j] = z < " << SPLIT << " ? coherent_load(&part[" << PP << "LL + o_]) : 0.0f;\n";
+    s << "            const float lm_ = coherent_load(&part[o_]), lq_ = coherent_load(&part[" << PP << "LL + o_]);\n";
+    s << "            vm_[j] = z < " << SPLIT << " ? lm_ : 0.0f;\n";
+    s << "            vq_[j] = z < " << SPLIT << " ? lq_ : 0.0f;\n";
     s << "          }\n";
     // the batch's triples merge as a pairwise tree (j with j + h, h = 1, 2, 4,
     // ...; a fixed order, log-depth dependency chains), then into the running one
@@ -964,7 +984,7 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
   s << "  const i64 l0 = (i64)blockIdx.z * " << chunk << ", l1 = l0 + " << chunk << " < " << Lr << "LL ? l0 + " << chunk
     << " : " << Lr << "LL;\n";
   s << "  float acc[" << VB << "];\n#pragma unroll\n  for (int e = 0; e < " << VB << "; ++e) acc[e] = " << ident << ";\n";
-  s << "#pragma unroll 4\n  for (i64 l = l0 + ly; l < l1; l += " << LY << ") {\n" << pe.pre.str() << pdecl.str()
+  s << row_loop(chunk, Lr, LY) << pe.pre.str() << pdecl.str()
     << "#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n" << pe.body.str() << "      acc[e] = "
     << comb("acc[e]", xv) << ";\n    }\n" << pafter.str() << "  }\n";
   // combine the LY rows of this workgroup in a fixed order: first the rows of
@@ -1027,8 +1047,10 @@ GenKernel gen_colreduce(const KInfo& ki, int index) {
     s << "      if (cb + c < " << B << "LL)\n        for (int z0 = g; z0 < " << SPLIT << "; z0 += " << NBT * G << ") {\n";
     s << "          float v_[" << NBT << "];\n#pragma unroll\n          for (int j = 0; j < " << NBT << "; ++j) {\n";
     s << "            const int z = z0 + j * " << G << ";\n";
-    s << "            v_[j] = z < " << SPLIT << " ? coherent_load(&part[(ay * " << SPLIT << " + z) * " << B
-      << "LL + cb + c]) : " << ident << ";\n          }\n";
+    // clamped address, value selected after the load (no branch around it)
+    s << "            const float l_ = coherent_load(&part[(ay * " << SPLIT << " + (z < " << SPLIT << " ? z : " << SPLIT - 1
+      << ")) * " << B << "LL + cb + c]);\n";
+    s << "            v_[j] = z < " << SPLIT << " ? l_ : " << ident << ";\n          }\n";
     s << "#pragma unroll\n          for (int j = 0; j < " << NBT << "; ++j) t_ = " << comb("t_", "v_[j]") << ";\n        }\n";
     s << "      red[g * " << TC << " + c] = t_;\n    }\n  }\n  __syncthreads();\n";
     s << "  if (ly == 0 && bv) {\n#pragma unroll\n    for (int e = 0; e < " << VB << "; ++e) {\n";
