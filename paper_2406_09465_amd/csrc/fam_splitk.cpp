@@ -109,7 +109,12 @@ bool match_splitk(const KInfo& ki, std::string* why) {
 }
 
 // Row program over the C tile rows in LDS (full rows of N columns).
-static std::string row_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot) {
+// With `pre` given and one pass over the tile's rows, the row setup and the
+// epilogue's own loads are returned in *pre (the caller emits them ahead of
+// the partial loads, so both go to memory together) and the rest, in a scope
+// the caller opened, is returned.
+static std::string row_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<int, int>& slot,
+                                std::string* pre = nullptr) {
   const Graph& g = ki.g;
   int mm = sp.mms[0];
   Shape F = sp.OUT;
@@ -222,6 +227,21 @@ static std::string row_epilogue(const KInfo& ki, const GemmSpec& sp, const std::
     }
   }
   std::ostringstream s;
+  if (pre && passes == 1) {
+    std::ostringstream h;
+    h << "    const int pass = 0;\n    (void)pass;\n";
+    h << "    const int lane = tid % " << G << ";\n";
+    h << "    const int ml = tid / " << G << ";\n";
+    h << "    const bool rv = ml < " << sp.BM << " && m0 + ml < " << sp.M << "LL;\n";
+    h << "    const int mlc = rv ? ml : 0;\n";
+    h << "    const i64 mc = rv ? m0 + ml : m0;\n";
+    h << "    const i64 row = bz * " << sp.M << "LL + mc;\n";
+    for (int j = 0; j < NC; ++j) h << "    const i64 cb" << j << " = ((i64)" << j << " * " << G << " + lane) * " << VEC << ";\n";
+    *pre = h.str() + loads.str();
+    s << comp.str() << stores.str();
+    return s.str();
+  }
+  if (pre) pre->clear();
   s << "  for (int pass = 0; pass < " << passes << "; ++pass) {\n";
   s << "    const int lane = tid % " << G << ";\n";
   s << "    const int ml = pass * " << RPB << " + tid / " << G << ";\n";
@@ -352,6 +372,23 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   s << "    last_ = (old == " << S - 1 << ");\n";
   s << "    if (last_) __hip_atomic_store(cnt + tix * 32, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);\n  }\n";
   s << "  __syncthreads();\n  if (!last_) return;\n";
+  bool any_tile_out = false;
+  for (int o : ki.k.outs)
+    if (!has(sp.side, o)) any_tile_out = true;
+  // a row-program epilogue's loads go out with the partial loads below
+  std::string epi_pre, epi_rest;
+  const bool row_epi = any_tile_out && !sp.rowred.empty();
+  if (row_epi) {
+    epi_rest = row_epilogue(ki, sp, slot, &epi_pre);
+    if (!epi_pre.empty()) s << "  {\n" << epi_pre;
+  }
+  // the side partials' loads go out before the tile's (from a clamped row,
+  // the sum kept only for rows of the tile), so both wait on one round trip
+  if (nside) {
+    s << "  float sv_[" << S << "];\n  {\n    const int ts_ = tid < " << sp.BM << " ? tid : " << sp.BM - 1 << ";\n";
+    s << "#pragma unroll\n    for (int p = 0; p < " << S << "; ++p) sv_[p] = coherent_load(&sidep[(tix * " << S << " + p) * "
+      << sp.BM << " + ts_]);\n  }\n";
+  }
   // deterministic sum of the partials, split 0 first
   if (vec4) {
     // all partial loads of a thread's float4 issued before they are summed
@@ -370,7 +407,7 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
   }
   if (nside) {
     s << "  if (tid < " << sp.BM << ") {\n    float acc_ = 0.0f;\n";
-    s << "    for (int p = 0; p < " << S << "; ++p) acc_ += coherent_load(&sidep[(tix * " << S << " + p) * " << sp.BM << " + tid]);\n";
+    s << "#pragma unroll\n    for (int p = 0; p < " << S << "; ++p) acc_ += sv_[p];\n";
     s << "    side_s[tid] = acc_;\n  }\n";
   }
   s << "  __syncthreads();\n";
@@ -383,15 +420,12 @@ GenKernel gen_splitk(const KInfo& ki, int index) {
                    "bz * " + std::to_string(sp.M) + "LL + m0 + tid", 0, val)
       << ";\n";
   }
-  bool any_tile_out = false;
-  for (int o : ki.k.outs)
-    if (!has(sp.side, o)) any_tile_out = true;
   if (any_tile_out) {
-    if (sp.rowred.empty())
+    if (!row_epi)
       s << gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(sp.LDC),
                          std::set<int>(sp.side.begin(), sp.side.end()));
     else
-      s << row_epilogue(ki, sp, slot);
+      s << epi_rest << (epi_pre.empty() ? "" : "  }\n");
   }
   s << "}\n";
   gk.source = s.str();
