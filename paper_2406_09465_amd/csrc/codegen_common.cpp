@@ -368,8 +368,13 @@ std::string Emitter::load(int node, const std::vector<Ix>& idx) {
           << " + " << off.b << ");\n  }\n";
       return v;
     }
-    inv << "  float " << v << "[" << vec << "] = {};\n  {\n    " << inv_defs << "\n    if (" << inv_guard << ") ldv<" << vec
-        << ">(" << v << ", " << P << " + " << off.b << ");\n  }\n";
+    const int vb = vec * dtype_bytes(n.dtype);
+    if ((vb == 4 || vb == 8 || vb == 16) && (double)numel(n.shape) * dtype_bytes(n.dtype) < 2147483648.0)
+      inv << "  float " << v << "[" << vec << "];\n  {\n    " << inv_defs << "\n    ldv_or_zero<" << vec << ">(" << v << ", " << P
+          << ", " << off.b << ", " << inv_guard << ");\n  }\n";
+    else
+      inv << "  float " << v << "[" << vec << "] = {};\n  {\n    " << inv_defs << "\n    if (" << inv_guard << ") ldv<" << vec
+          << ">(" << v << ", " << P << " + " << off.b << ");\n  }\n";
     return v + "[e]";
   }
   if (hoist && off.affine && off.c == 0) {

@@ -165,6 +165,11 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
     s << "  int t = blockIdx.x;\n  const int tend = t + 1, tstep = 1;\n";
   }
   s << "  if (t >= tend) return;\n";
+  // per-channel epilogue operands are loaded once per workgroup, first, so that
+  // their round trip overlaps the weights' and the first halo's
+  std::string inv;
+  const std::string epi = gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(d.LDC), {}, d.TW, 0, "0", &inv);
+  s << inv;
   // halo slots: vector v of the halo is pixel v / CV (row, column) and channels (v % CV) * 8
   s << "  const __amdgpu_buffer_rsrc_t rsX = __builtin_amdgcn_make_buffer_rsrc(" << X << ", 0, " << xbytes
     << ", 0x00020000);\n";
@@ -256,10 +261,6 @@ GenKernel gen_conv_direct(const KInfo& ki, GemmSpec& sp, int index) {
   s << "  stash_halo(0);\n  __syncthreads();\n";
   // per-lane part of the halo address of a fragment: pixel column (l & 15), channels (l >> 4) * 8
   s << "  const int lane_off = (l & 15) * " << d.CPP << " + (l >> 4) * 8;\n";
-  // per-channel epilogue operands are loaded once, before the tile loop
-  std::string inv;
-  const std::string epi = gemm_epilogue(ki, sp, slot, "ml * " + std::to_string(d.LDC), {}, d.TW, 0, "0", &inv);
-  s << inv;
   s << "  int b = 0;\n";
   s << "  for (;;) {\n";
   s << "    const int tn = t + tstep;\n    const bool more = tn < tend;\n";
