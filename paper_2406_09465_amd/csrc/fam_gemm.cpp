@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
+#include <regex>
 
 #include "families.h"
 #include "gemm_common.h"
@@ -1741,7 +1742,39 @@ std::string gemm_epilogue(const KInfo& ki, const GemmSpec& sp, const std::map<in
   else
     s << em.inv.str();
   if (rows <= 0) rows = sp.BM;
-  s << "  for (int s_ = tid; s_ < " << rows * (cols / VE) << "; s_ += " << sp.NT << ") {\n";
+  // An epilogue that reads tensors per element (a residual, say) runs a
+  // fixed-trip unrolled loop when every thread has the same number of vectors:
+  // the compiler then issues all of a thread's loads before the first is used
+  // (a runtime-bounded loop loads, waits and stores one vector at a time).
+  const int nvec_ = rows * (cols / VE);
+  if (conv_tw <= 0 && sp.M % sp.BM == 0 && n_full && nvec_ % sp.NT == 0 && nvec_ / sp.NT <= 8 &&
+      em.n_vector + em.n_gather > 0) {
+    // Every thread stores nvec_ / NT vectors and none is guarded: the loads of
+    // all of them (C tile and tensors read per element) are written out first,
+    // then the arithmetic and stores of each.  A loop would load, wait and
+    // store one vector at a time (the compiler cannot move a load above a store
+    // to another tensor), a round trip to memory per vector.
+    const int T_ = nvec_ / sp.NT;
+    std::string setup = "    const int s_ = tid + IT_ * " + std::to_string(sp.NT) + ";\n    const int mlc = s_ / " +
+                        std::to_string(cols / VE) + ", ml = " + row0 + " + mlc, nl = (s_ % " + std::to_string(cols / VE) +
+                        ") * " + std::to_string(VE) + ";\n    (void)mlc;\n    const i64 m = m0 + ml, n = n0 + nl;\n    (void)m; (void)n;\n";
+    std::string loads = setup + cvload.str() + em.pre.str();
+    std::string rest = decl.str() + "#pragma unroll\n      for (int e = 0; e < " + std::to_string(VE) + "; ++e) {\n" +
+                       em.body.str() + "      }\n" + after.str();
+    // names of one vector's code get the vector's suffix; hoisted (ix / iu)
+    // values and everything defined outside are left alone
+    static const std::regex id(R"(\b(s_|mlc|ml|nl|m|n|_(?!ix|iu)[a-z]+[0-9]+)\b)");
+    auto renamed = [&](const std::string& t, int it) {
+      std::string r = std::regex_replace(t, id, "$1_v" + std::to_string(it));
+      return std::regex_replace(r, std::regex(R"(\bIT_\b)"), std::to_string(it));
+    };
+    s << "  {\n";
+    for (int it = 0; it < T_; ++it) s << renamed(loads, it);
+    for (int it = 0; it < T_; ++it) s << "    {\n" << renamed(rest, it) << "    }\n";
+    s << "  }\n";
+    return s.str();
+  }
+  s << "  for (int s_ = tid; s_ < " << nvec_ << "; s_ += " << sp.NT << ") {\n";
   s << "    const int mlc = s_ / " << cols / VE << ", ml = " << row0 << " + mlc, nl = (s_ % " << cols / VE << ") * " << VE
     << ";\n";
   s << "    (void)mlc;\n";
